@@ -1,0 +1,274 @@
+#!/usr/bin/env python3
+"""Throughput of the batched 4x4 Birkhoff projection (forward + backward) on one MI355X.
+
+One step = one pass of the whole path over the batch: the Newton forward kernel
+(H -> P, dual) followed by the implicit-differentiation backward kernel
+(P, dP -> dH), both launched through the C ABI on torch's current stream. Inputs
+are synthetic (workloads/), generated on the host and resident in HBM before the
+timed region. Prints ONE JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload mix_bf16_b2e24]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "4×4 Birkhoff projections/sec fwd+bwd at B=2^24 (fp32); % HBM peak; max marginal err"
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+SRC = os.path.join(ROOT, "paper_2606_07574_amd", "csrc", "birkhoff4.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def in_bytes(dtype_is_bf16: bool) -> int:
+    return 32 if dtype_is_bf16 else 64
+
+
+def traffic_from_profiles(workload: str):
+    """HBM bytes per launch measured by rocprofv3 counters, if they were taken on
+    the current kernel source (profiles/traffic_<workload>.md)."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"source_sha256:\s*([0-9a-f]{64})", text)
+    src = hashlib.sha256(open(SRC, "rb").read()).hexdigest()
+    if not m or m.group(1) != src:
+        return None
+    out = {}
+    for k in ("newton_fwd", "implicit_bwd"):
+        mm = re.search(rf"{k}_hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+        if mm:
+            out[k] = float(mm.group(1))
+    return out or None
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mix_bf16_b2e24")
+    ap.add_argument("--tol", type=float, default=1e-6)
+    ap.add_argument("--max-iter", type=int, default=64)
+    ap.add_argument("--cpu-sample", type=int, default=1 << 20,
+                    help="matrices in the oracle's CPU-baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sk", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="time only the path (for profiler runs)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build runs on one GPU only; the projection shards by batch with "
+              "no communication (see the design notes), so only --gpus 1 is measured.",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2606_07574_amd as b4
+    import workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 2
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = workloads.WORKLOADS[args.workload]
+    B = w.B
+    bf16 = w.storage == "bf16"
+
+    t0 = time.time()
+    ch = workloads.generate(w.name, threads=16)
+    log(f"generated {w.name} B={B} in {time.time() - t0:.1f}s")
+
+    def dev_input(x32, bits):
+        if bits is not None:
+            return torch.from_numpy(bits.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(x32).to(dev)
+
+    # working set per buffer set; rotate sets so the 256 MB last-level cache cannot hold it
+    set_bytes = B * (in_bytes(bf16) + 64 + 32 + ((in_bytes(bf16) + 64) if w.grad else 0))
+    n_sets = max(1, min(8, math.ceil((768 << 20) / set_bytes)))
+    sets = []
+    H0 = dev_input(ch.H, ch.H_bits)
+    G0 = dev_input(ch.dP, ch.dP_bits) if w.grad else None
+    for s in range(n_sets):
+        Hs = H0 if s == 0 else H0.clone()
+        Gs = (G0 if s == 0 else G0.clone()) if w.grad else None
+        sets.append(dict(H=Hs, G=Gs, P=torch.empty(B, 4, 4, device=dev),
+                         dual=torch.empty(B, 8, device=dev),
+                         dH=torch.empty(B, 4, 4, device=dev) if w.grad else None))
+    torch.cuda.synchronize()
+    lib = b4.lib()
+    stream = torch.cuda.current_stream(dev)
+    sptr = stream.cuda_stream
+    hcode = b4.BF16 if bf16 else b4.F32
+
+    def step(k):
+        st = sets[k % n_sets]
+        rc = lib.birkhoff4_fwd_ex(st["H"].data_ptr(), hcode, st["P"].data_ptr(), st["dual"].data_ptr(),
+                                  None, B, args.tol, args.max_iter, sptr)
+        if rc:
+            raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+        ev_mid[k % len(ev_mid)].record(stream)
+        if w.grad:
+            rc = lib.birkhoff4_bwd_ex(st["P"].data_ptr(), st["G"].data_ptr(), hcode if bf16 else b4.F32,
+                                      st["dH"].data_ptr(), B, sptr)
+            if rc:
+                raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+
+    K, W = args.steps, args.warmup
+    ev_start = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    ev_mid = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    ev_end = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    for k in range(W):
+        step(k)
+    torch.cuda.synchronize()
+    log(f"warmup done ({W} steps); timing {K} steps")
+    t_start = time.perf_counter()
+    for k in range(K):
+        ev_start[k].record(stream)
+        step(k)
+        ev_end[k].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    fwd_ms = float(np.mean([ev_start[k].elapsed_time(ev_mid[k]) for k in range(K)]))
+    bwd_ms = float(np.mean([ev_mid[k].elapsed_time(ev_end[k]) for k in range(K)])) if w.grad else 0.0
+    ms_per_step = wall * 1e3 / K
+    value = B * K / wall
+    log(f"timed: {ms_per_step:.3f} ms/step  fwd {fwd_ms:.3f} ms  bwd {bwd_ms:.3f} ms")
+
+    fwd_bytes = B * (in_bytes(bf16) + 64 + 32)
+    bwd_bytes = B * (64 + in_bytes(bf16) + 64)
+    kernels = {"newton_fwd": {"avg_ms": fwd_ms, "alg_bytes_per_launch": fwd_bytes,
+                              "achieved_GBs": fwd_bytes / (fwd_ms * 1e-3) / 1e9}}
+    if w.grad:
+        kernels["implicit_bwd"] = {"avg_ms": bwd_ms, "alg_bytes_per_launch": bwd_bytes,
+                                   "achieved_GBs": bwd_bytes / (bwd_ms * 1e-3) / 1e9}
+    dominant = max(kernels, key=lambda k: kernels[k]["avg_ms"])
+    traffic = traffic_from_profiles(w.name)
+    ach = kernels[dominant]["achieved_GBs"]
+    roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                "traffic": (traffic or {}).get(dominant)}
+    path_bytes = fwd_bytes + (bwd_bytes if w.grad else 0)
+    out = {
+        "metric": METRIC if w.name == "mix_bf16_b2e24" else f"4x4 Birkhoff projections/sec ({w.name})",
+        "value": round(value, 1), "unit": "proj/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "storage": w.storage, "tol": args.tol,
+                   "max_iter": args.max_iter, "passes": "fwd+bwd" if w.grad else "fwd",
+                   "desc": w.desc, "buffer_sets": n_sets},
+        "roofline": roofline,
+        "path_hbm_frac": round(path_bytes * K / wall / 1e9 / HBM_PEAK_GBS, 4),
+        "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in v.items()}
+                    for k, v in kernels.items()},
+    }
+
+    if not args.no_extras:
+        # diagnostics outside the timed region: Newton step histogram, marginal errors
+        st = sets[0]
+        P, dual, it = b4.fwd(st["H"], args.tol, args.max_iter, want_dual=True, want_iters=True)
+        torch.cuda.synchronize()
+        itn = it.cpu().numpy()
+        P64 = P.double()
+        marg = torch.maximum((P64.sum(-1) - 1).abs().amax(-1), (P64.sum(-2) - 1).abs().amax(-1))
+        l1 = (P64.sum(-1) - 1).abs().sum(-1) + (P64.sum(-2) - 1).abs().sum(-1)
+        conv = itn[itn >= 0]
+        # per-wave maximum: what a one-problem-per-lane kernel without refill would pay
+        n64 = (len(itn) // 64) * 64
+        wave_max = np.clip(itn[:n64], 0, None).reshape(-1, 64).max(axis=1).mean() if n64 else float("nan")
+        out["newton_steps"] = {
+            "mean": round(float(conv.mean()), 3) if len(conv) else None,
+            "p50": int(np.percentile(conv, 50)) if len(conv) else None,
+            "p99": int(np.percentile(conv, 99)) if len(conv) else None,
+            "max": int(conv.max()) if len(conv) else None,
+            "mean_of_wave_max": round(float(wave_max), 3),
+            "not_converged": int((itn == -1).sum()), "non_finite": int((itn == -2).sum()),
+            "hist": np.bincount(np.clip(conv, 0, 40), minlength=41).tolist(),
+        }
+        out["max_marginal_err"] = float(marg.max().item())
+        out["marginal_err_L1"] = {"mean": float(l1.mean().item()), "median": float(l1.median().item()),
+                                  "max": float(l1.max().item())}
+        log(f"newton steps: {out['newton_steps']}")
+        log(f"max marginal err {out['max_marginal_err']:.3e}")
+
+        if not args.no_sk:
+            n_sk = 20
+            for k in range(2):
+                b4.sk_fwd(st["H"], n_sk)
+                if w.grad:
+                    b4.sk_bwd(st["H"], st["G"], n_sk)
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e2 = torch.cuda.Event(enable_timing=True)
+            ks = max(3, K // 4)
+            f_ms = b_ms = 0.0
+            for k in range(ks):
+                e0.record(stream)
+                Psk = b4.sk_fwd(sets[k % n_sets]["H"], n_sk)
+                e1.record(stream)
+                if w.grad:
+                    b4.sk_bwd(sets[k % n_sets]["H"], sets[k % n_sets]["G"], n_sk)
+                e2.record(stream)
+                torch.cuda.synchronize()
+                f_ms += e0.elapsed_time(e1)
+                b_ms += e1.elapsed_time(e2) if w.grad else 0.0
+            f_ms /= ks
+            b_ms /= ks
+            S64 = Psk.double()
+            smarg = torch.maximum((S64.sum(-1) - 1).abs().amax(-1), (S64.sum(-2) - 1).abs().amax(-1))
+            sl1 = (S64.sum(-1) - 1).abs().sum(-1) + (S64.sum(-2) - 1).abs().sum(-1)
+            out["sk20_baseline"] = {
+                "value": round(B / ((f_ms + b_ms) * 1e-3), 1), "unit": "proj/s",
+                "fwd_ms": round(f_ms, 4), "bwd_ms": round(b_ms, 4),
+                "max_marginal_err": float(smarg.max().item()),
+                "marginal_err_L1": {"mean": float(sl1.mean().item()), "median": float(sl1.median().item()),
+                                    "max": float(sl1.max().item())},
+            }
+            log(f"sk20: {out['sk20_baseline']}")
+            del Psk, S64
+        del P, P64
+
+    if not args.no_cpu_baseline:
+        import oracle
+        n = min(args.cpu_sample, B)
+        Hs = ch.H[:n].astype(np.float64)
+        Gs = ch.dP[:n].astype(np.float64) if w.grad else None
+        threads = oracle.default_threads()
+        t0 = time.perf_counter()
+        Pr, _, _ = oracle.fwd(Hs, tol=args.tol, threads=threads)
+        if w.grad:
+            oracle.bwd(Pr, Gs, threads=threads)
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(n / dt, 1), "unit": "proj/s", "cores": threads,
+                               "kind": "oracle",
+                               "sample": f"first {n} matrices of {w.name}; fp64 oracle forward "
+                                         f"(tol {args.tol}) + backward, {threads} threads, {dt:.1f} s"}
+        log(f"cpu baseline: {out['cpu_baseline']}")
+
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,133 @@
+/*
+ * birkhoff4.h -- batched 4x4 Birkhoff projection on AMD Instinct MI355X (gfx950).
+ *
+ * The forward pass projects exp(H[b]) onto the Birkhoff polytope of doubly
+ * stochastic 4x4 matrices in the KL geometry (eq. birkhoff_projection), by
+ * Newton's method on the reduced 3-dimensional entropic-OT dual (Sec. 3.1-3.2,
+ * eq. min_fx, eq. grad_hess; cost M = -H, eta = 1, a = b = 1). The backward pass
+ * maps dL/dP to dL/dH by implicit differentiation through the optimality
+ * conditions (Sec. 4, eq. derivative, with the sign flip for H = -M), reading
+ * only P and dP: no iterates or Hessians are stored.
+ *
+ * Conventions shared by every entry point
+ *   - All array arguments are DEVICE pointers on the current HIP device; the
+ *     caller owns them. The library never allocates, frees or synchronises.
+ *   - Work is enqueued on `stream` (0 = the null stream) and the call returns
+ *     at once; errors found on the host are returned before anything is queued.
+ *   - 4x4 arrays are [B][4][4] row-major and contiguous: element (b,i,j) is at
+ *     16*b + 4*i + j. `dual` is [B][8] = (alpha_1..alpha_4, beta_1..beta_4) with
+ *     beta_4 = 0, so that log P_ij - H_ij = alpha_i + beta_j.
+ *   - Every array must be 16-byte aligned, and no output may overlap another
+ *     argument (in-place use is not supported).
+ *   - B = 0 is a no-op returning BIRKHOFF4_OK.
+ *   - Numerical outcomes are not errors: a matrix that does not reach `tol`
+ *     within `max_iter` iterations returns its last accepted (row-stochastic)
+ *     iterate; a matrix with a NaN or infinite entry returns NaN in all its
+ *     outputs. The _ex variants report both cases per matrix.
+ */
+#ifndef BIRKHOFF4_H
+#define BIRKHOFF4_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+enum {
+    BIRKHOFF4_OK = 0,
+    BIRKHOFF4_ERR_NULL = -1,      /* a required pointer is NULL while B > 0 */
+    BIRKHOFF4_ERR_SIZE = -2,      /* B < 0, or too large for the index type */
+    BIRKHOFF4_ERR_TOL = -3,       /* tol < 0 or NaN */
+    BIRKHOFF4_ERR_MAX_ITER = -4,  /* max_iter < 0 or > 10000 */
+    BIRKHOFF4_ERR_DTYPE = -5,     /* unknown storage dtype code */
+    BIRKHOFF4_ERR_ALIGN = -6,     /* an array is not 16-byte aligned */
+    BIRKHOFF4_ERR_OVERLAP = -7,   /* an output overlaps another argument */
+    BIRKHOFF4_ERR_STEPS = -8,     /* Sinkhorn step count out of range */
+    BIRKHOFF4_ERR_DEVICE = -9,    /* HIP device query failed */
+    BIRKHOFF4_ERR_LAUNCH = -10    /* kernel launch failed (hipGetLastError) */
+};
+
+/* Storage dtypes for inputs (outputs are always fp32; compute is always fp32). */
+enum {
+    BIRKHOFF4_F32 = 0,
+    BIRKHOFF4_BF16 = 1
+};
+
+/* Per-matrix status codes written to `iters` by birkhoff4_fwd_ex (values >= 0
+ * are the number of Newton trial steps taken, see below). */
+enum {
+    BIRKHOFF4_NOT_CONVERGED = -1, /* max_iter trial steps did not reach tol */
+    BIRKHOFF4_NON_FINITE = -2     /* the input matrix had a NaN or infinite entry */
+};
+
+/* Forward projection, fp32 input.
+ *
+ * H     [B][4][4] fp32 logits (the paper's residual logits, R = -M).
+ * P     [B][4][4] fp32 output: the projection, rows summing to one by
+ *       construction and every column sum within `tol` of one on return.
+ * dual  [B][8] fp32 output, or NULL to skip it: alpha*(beta*) (eq. alpha_opt)
+ *       and beta* with beta_4 = 0 (Sec. 3.1 gauge).
+ * tol   stopping tolerance on max_j |sum_i P_ij - 1| (the paper uses 1e-6);
+ *       tol = 0 stops a matrix only when its fp32 column sums are exactly one,
+ *       so in practice most run for max_iter trial steps.
+ * max_iter  maximum number of Newton trial steps per matrix, 0..10000 (each is one
+ *       evaluation of the dual at a trial point: a damped Newton step, or a
+ *       backtracking of it with a larger Levenberg-Marquardt shift). 0 returns T at the initial point, which is the
+ *       row softmax of H after the columns are centred (beta_j^(0) = mean of
+ *       column 4 minus mean of column j).
+ */
+int birkhoff4_fwd(const float* H, float* P, float* dual, int64_t B, float tol,
+                  int max_iter, hipStream_t stream);
+
+/* Backward (vector-Jacobian product), fp32 upstream gradient.
+ *
+ * P     [B][4][4] fp32: the projection returned by the forward pass (T*).
+ * dual  accepted for symmetry with the forward pass and not read (the 4x4
+ *       backward needs only T* and G, Sec. 4.2); may be NULL.
+ * dP    [B][4][4] fp32: dL/dP (the paper's G).
+ * dH    [B][4][4] fp32 output: dL/dH = -D of eq. derivative, with Delta taken as
+ *       the Hessian of the reduced dual at P. Rows and columns of dH sum to zero.
+ */
+int birkhoff4_bwd(const float* P, const float* dual, const float* dP, float* dH,
+                  int64_t B, hipStream_t stream);
+
+/* Forward projection with a storage dtype for H and per-matrix diagnostics.
+ * h_dtype is BIRKHOFF4_F32 or BIRKHOFF4_BF16 (H then holds B*16 bf16 values,
+ * widened exactly to fp32). iters is NULL or an int32 [B] output receiving the
+ * number of trial steps taken, or BIRKHOFF4_NOT_CONVERGED / BIRKHOFF4_NON_FINITE.
+ * Other arguments as in birkhoff4_fwd. */
+int birkhoff4_fwd_ex(const void* H, int h_dtype, float* P, float* dual, int32_t* iters,
+                     int64_t B, float tol, int max_iter, hipStream_t stream);
+
+/* Backward with a storage dtype for dP (BIRKHOFF4_F32 or BIRKHOFF4_BF16). */
+int birkhoff4_bwd_ex(const float* P, const void* dP, int dp_dtype, float* dH, int64_t B,
+                     hipStream_t stream);
+
+/* Baseline: n_steps iterations of Sinkhorn-Knopp (eq. sinkhorn_knopp) from
+ * v^(0) = 1 on A = exp(H) (each row shifted by its maximum, which leaves every
+ * iterate diag(u) A diag(v) unchanged); P = diag(u^(n)) A diag(v^(n)), whose
+ * columns sum to one. 1 <= n_steps <= 48. Denominators are clamped at the
+ * smallest normal fp32 so that underflowed rows and columns stay finite. */
+int birkhoff4_sk_fwd(const void* H, int h_dtype, float* P, int64_t B, int n_steps,
+                     hipStream_t stream);
+
+/* Baseline backward: the exact gradient of the n_steps Sinkhorn-Knopp map at H,
+ * applied to dP (reverse mode through the unrolled iterations, recomputed from
+ * H in registers; nothing is stored between the passes). */
+int birkhoff4_sk_bwd(const void* H, int h_dtype, const void* dP, int dp_dtype, float* dH,
+                     int64_t B, int n_steps, hipStream_t stream);
+
+/* Human-readable text for a return code (static storage). */
+const char* birkhoff4_strerror(int code);
+
+/* Library version: major * 10000 + minor * 100 + patch. */
+int birkhoff4_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BIRKHOFF4_H */

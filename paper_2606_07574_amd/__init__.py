@@ -1,0 +1,177 @@
+"""Batched 4x4 Birkhoff projection on MI355X: Python binding of libbirkhoff4.so.
+
+Argument marshalling only. Every step of the projection and of its gradient
+runs in the HIP kernels of ``csrc/birkhoff4.hip`` behind the C ABI declared in
+``include/birkhoff4.h``; PyTorch supplies device memory and the current stream.
+There is no CPU fallback: if the library is missing or the tensors are not on
+a GPU, the calls raise.
+
+    P, dual = fwd(H)                  # eq. birkhoff_projection via Newton (Sec. 3)
+    dH = bwd(P, dP)                   # implicit differentiation (Sec. 4, eq. derivative)
+    P = project(H)                    # autograd-aware: backward calls bwd
+    P = sk_fwd(H, 20); dH = sk_bwd(H, dP, 20)   # Sinkhorn-Knopp baseline
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbirkhoff4.so")
+
+F32, BF16 = 0, 1
+NOT_CONVERGED, NON_FINITE = -1, -2
+DEFAULT_TOL = 1e-6
+DEFAULT_MAX_ITER = 64
+
+_lib = None
+
+
+class Birkhoff4Error(RuntimeError):
+    pass
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise Birkhoff4Error(
+            f"{LIB_PATH} is missing: build it with `python -m paper_2606_07574_amd.build` "
+            "(or __graft_entry__.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i64, f32, i32, st = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float, ctypes.c_int, ctypes.c_void_p
+    sigs = {
+        "birkhoff4_fwd": [vp, vp, vp, i64, f32, i32, st],
+        "birkhoff4_bwd": [vp, vp, vp, vp, i64, st],
+        "birkhoff4_fwd_ex": [vp, i32, vp, vp, vp, i64, f32, i32, st],
+        "birkhoff4_bwd_ex": [vp, vp, i32, vp, i64, st],
+        "birkhoff4_sk_fwd": [vp, i32, vp, i64, i32, st],
+        "birkhoff4_sk_bwd": [vp, i32, vp, i32, vp, i64, i32, st],
+        "birkhoff4_version": [],
+    }
+    for name, args in sigs.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    lib.birkhoff4_strerror.argtypes = [ctypes.c_int]
+    lib.birkhoff4_strerror.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def lib():
+    """The loaded ctypes library (raises if it is not built)."""
+    return _load()
+
+
+def _check(code: int) -> None:
+    if code != 0:
+        msg = _load().birkhoff4_strerror(code).decode()
+        raise Birkhoff4Error(f"birkhoff4 error {code}: {msg}")
+
+
+def _stream(t: torch.Tensor) -> int:
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
+
+
+def _batch(t: torch.Tensor, name: str) -> int:
+    if not t.is_cuda:
+        raise Birkhoff4Error(f"{name} must be a GPU tensor (no CPU path)")
+    if t.dim() < 2 or tuple(t.shape[-2:]) != (4, 4):
+        raise ValueError(f"{name} must have shape [..., 4, 4], got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.numel() // 16
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def fwd(H: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER,
+        want_dual: bool = True, want_iters: bool = False, out: torch.Tensor | None = None):
+    """Project exp(H) onto the Birkhoff polytope, per trailing 4x4 matrix.
+
+    H: float32 or bfloat16 [..., 4, 4] on the GPU. Returns (P, dual, iters):
+    P float32 like H, dual float32 [..., 8] or None, iters int32 [...] or None.
+    """
+    B = _batch(H, "H")
+    lead = H.shape[:-2]
+    P = torch.empty(H.shape, dtype=torch.float32, device=H.device) if out is None else out
+    dual = torch.empty(*lead, 8, dtype=torch.float32, device=H.device) if want_dual else None
+    iters = torch.empty(lead, dtype=torch.int32, device=H.device) if want_iters else None
+    with torch.cuda.device(H.device):
+        _check(_load().birkhoff4_fwd_ex(_ptr(H), _dtype_code(H), _ptr(P), _ptr(dual), _ptr(iters),
+                                        B, float(tol), int(max_iter), _stream(H)))
+    return P, dual, iters
+
+
+def bwd(P: torch.Tensor, dP: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+    """dL/dH from P (the forward output) and dL/dP (float32 or bfloat16)."""
+    B = _batch(P, "P")
+    if _batch(dP, "dP") != B:
+        raise ValueError("P and dP batch sizes differ")
+    if P.dtype != torch.float32:
+        raise TypeError("P must be float32")
+    dH = torch.empty(P.shape, dtype=torch.float32, device=P.device) if out is None else out
+    with torch.cuda.device(P.device):
+        _check(_load().birkhoff4_bwd_ex(_ptr(P), _ptr(dP), _dtype_code(dP), _ptr(dH), B, _stream(P)))
+    return dH
+
+
+def sk_fwd(H: torch.Tensor, n_steps: int = 20) -> torch.Tensor:
+    """n_steps Sinkhorn-Knopp iterations (baseline)."""
+    B = _batch(H, "H")
+    P = torch.empty(H.shape, dtype=torch.float32, device=H.device)
+    with torch.cuda.device(H.device):
+        _check(_load().birkhoff4_sk_fwd(_ptr(H), _dtype_code(H), _ptr(P), B, int(n_steps), _stream(H)))
+    return P
+
+
+def sk_bwd(H: torch.Tensor, dP: torch.Tensor, n_steps: int = 20) -> torch.Tensor:
+    """Gradient of the n_steps Sinkhorn-Knopp map at H, applied to dP (baseline)."""
+    B = _batch(H, "H")
+    if _batch(dP, "dP") != B:
+        raise ValueError("H and dP batch sizes differ")
+    dH = torch.empty(H.shape, dtype=torch.float32, device=H.device)
+    with torch.cuda.device(H.device):
+        _check(_load().birkhoff4_sk_bwd(_ptr(H), _dtype_code(H), _ptr(dP), _dtype_code(dP), _ptr(dH),
+                                        B, int(n_steps), _stream(H)))
+    return dH
+
+
+class Birkhoff4Fn(torch.autograd.Function):
+    """P = proj(exp(H)); the backward is the implicit-differentiation kernel and
+    needs only the saved P (no iterates, no Hessian)."""
+
+    @staticmethod
+    def forward(ctx, H, tol=DEFAULT_TOL, max_iter=DEFAULT_MAX_ITER):
+        P, _, _ = fwd(H.contiguous(), tol, max_iter, want_dual=False)
+        ctx.save_for_backward(P)
+        ctx.in_dtype = H.dtype
+        return P
+
+    @staticmethod
+    def backward(ctx, dP):
+        (P,) = ctx.saved_tensors
+        dH = bwd(P, dP.contiguous())
+        return dH.to(ctx.in_dtype), None, None
+
+
+def project(H: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER) -> torch.Tensor:
+    return Birkhoff4Fn.apply(H, tol, max_iter)
+
+
+def version() -> int:
+    return _load().birkhoff4_version()

@@ -1,0 +1,783 @@
+// birkhoff4.hip -- batched 4x4 Birkhoff projection for gfx950 (MI355X).
+//
+// Forward: Newton's method on the reduced 3-dimensional entropic-OT dual
+// (Sec. 3.1-3.2: eq. min_fx, eq. grad_hess, eq. tij_stable, eq. c_g), with cost
+// M = -H, eta = 1, a = b = 1. Backward: implicit differentiation (Sec. 4,
+// eq. derivative) from P and dP only. Baseline: n-step Sinkhorn-Knopp
+// (eq. sinkhorn_knopp) and its reverse-mode gradient.
+//
+// Mapping: one 4x4 problem per lane; all per-problem state lives in VGPRs. No
+// MFMA (the only products are six 4-long dot products per matrix), no LDS in
+// the Newton and implicit kernels, no atomics.
+//
+// Forward numerics (fp32, log2 domain so that v_exp_f32 applies directly):
+//  * state is U = H*log2(e) + beta - a 1^T with every row re-centred to max 0
+//    after each accepted step, so entries that carry mass are near 0 and keep
+//    full fp32 resolution even when |beta| is in the hundreds (a beta-only state
+//    cannot tune the column sums below ~1e-5 there);
+//  * Hessian of the reduced dual = Laplacian of the column graph with weights
+//    W_jk = sum_i T_ij T_ik (rows of T sum to one), grounded at column 4; the
+//    Newton system is solved by elimination with pivots formed as sums of these
+//    positive weights, plus a Levenberg-Marquardt shift 1e-3 * max_j |g_j| that
+//    vanishes at the solution and keeps directions finite when weights
+//    underflow;
+//  * step: capped at |d|_inf <= 8 (natural-log units), Armijo backtracking on the
+//    reduced dual f, with a gradient-norm test once f no longer resolves the
+//    decrease; each backtrack halves the step and multiplies the shift by 16
+//    (re-solving with the saved weights), and the trial step doubles while full
+//    steps keep descending strongly;
+//  * initial point beta_j = mean_i H_i4 - mean_i H_ij (column centring);
+//  * stop when max over the four columns of |c_j - 1| <= tol.
+//
+// Lane-level work refill: each wave owns a contiguous range of problems; a
+// lane whose problem is finished writes it out and takes the next unclaimed
+// problem of its wave's range at once, so a wave pays the mean number of
+// Newton steps, not the maximum over its 64 lanes.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "birkhoff4.h"
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kCap2 = 8.0f * kLog2e;  // step cap in log2 units
+constexpr float kLM = 1e-3f;            // Levenberg-Marquardt coefficient
+constexpr float kArmijo = 1e-4f;
+constexpr float kFNoise = 4e-6f;        // |delta f| below this is rounding noise
+constexpr float kMaxExpand = 16.0f;
+constexpr float kMaxLMMult = 1e20f;     // keeps the shift finite (|g| <= 4)
+constexpr float kTiny = 1e-30f;
+constexpr float kFltMin = 1.17549435e-38f;
+constexpr int kMaxSkSteps = 48;   // sk_bwd keeps (n+1) x 4 floats per lane in LDS
+constexpr int kMaxIterCap = 10000;
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float lg2(float x) { return __builtin_amdgcn_logf(x); }
+__device__ __forceinline__ float rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+// ---------------------------------------------------------------------------
+// Loads and stores of one 4x4 problem (row-major, 64 B fp32 / 32 B bf16)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void load16_f32(const float* base, int64_t b, float v[16]) {
+    const v4f* p = reinterpret_cast<const v4f*>(base) + 4 * b;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const v4f r = __builtin_nontemporal_load(p + q);
+        v[4 * q + 0] = r.x;
+        v[4 * q + 1] = r.y;
+        v[4 * q + 2] = r.z;
+        v[4 * q + 3] = r.w;
+    }
+}
+
+__device__ __forceinline__ void load16_bf16(const uint16_t* base, int64_t b, float v[16]) {
+    const v4u* p = reinterpret_cast<const v4u*>(base) + 2 * b;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const v4u r = __builtin_nontemporal_load(p + q);
+        const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            v[8 * q + 2 * k + 0] = __uint_as_float(w[k] << 16);
+            v[8 * q + 2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
+        }
+    }
+}
+
+template <int DT>
+__device__ __forceinline__ void load16(const void* base, int64_t b, float v[16]) {
+    if constexpr (DT == BIRKHOFF4_BF16)
+        load16_bf16(static_cast<const uint16_t*>(base), b, v);
+    else
+        load16_f32(static_cast<const float*>(base), b, v);
+}
+
+__device__ __forceinline__ void store16(float* base, int64_t b, const float v[16]) {
+    v4f* p = reinterpret_cast<v4f*>(base) + 4 * b;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const v4f r = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+        __builtin_nontemporal_store(r, p + q);
+    }
+}
+
+__device__ __forceinline__ bool all_finite16(const float v[16]) {
+    bool ok = true;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) ok = ok && (__builtin_fabsf(v[q]) <= 3.402823466e38f);
+    return ok;
+}
+
+// ---------------------------------------------------------------------------
+// Forward
+// ---------------------------------------------------------------------------
+
+// Row-softmax evaluation at the trial point U + t d (log2 units), eq. tij_stable:
+// X = re-centred trial (new U if accepted), T = softmax rows, mrow = row maxima,
+// lsum = log2 of the row sums of 2^X, g = column sums - 1 (eq. c_g, all four).
+__device__ __forceinline__ void evaluate(const float U[16], float td0, float td1, float td2,
+                                         float X[16], float T[16], float mrow[4], float lsum[4],
+                                         float g[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float u0 = U[4 * i + 0] + td0;
+        const float u1 = U[4 * i + 1] + td1;
+        const float u2 = U[4 * i + 2] + td2;
+        const float u3 = U[4 * i + 3];
+        const float m = __builtin_fmaxf(__builtin_fmaxf(u0, u1), __builtin_fmaxf(u2, u3));
+        X[4 * i + 0] = u0 - m;
+        X[4 * i + 1] = u1 - m;
+        X[4 * i + 2] = u2 - m;
+        X[4 * i + 3] = u3 - m;
+        const float e0 = ex2(X[4 * i + 0]);
+        const float e1 = ex2(X[4 * i + 1]);
+        const float e2 = ex2(X[4 * i + 2]);
+        const float e3 = ex2(X[4 * i + 3]);
+        const float s = (e0 + e1) + (e2 + e3);
+        const float r = rcp(s);
+        T[4 * i + 0] = e0 * r;
+        T[4 * i + 1] = e1 * r;
+        T[4 * i + 2] = e2 * r;
+        T[4 * i + 3] = e3 * r;
+        mrow[i] = m;
+        lsum[i] = lg2(s);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        g[j] = ((T[j] + T[4 + j]) + (T[8 + j] + T[12 + j])) - 1.0f;
+}
+
+// Column-graph weights W_jk = sum_i T_ij T_ik (the p_jk of Sec. 3.2 extended to
+// column 4). With unit row sums the Hessian of the reduced dual is the Laplacian
+// of this graph grounded at column 4: h_jk = -W_jk, h_jj = sum_{k != j} W_jk.
+struct Weights {
+    float w01, w02, w03, w12, w13, w23;
+};
+
+__device__ __forceinline__ Weights column_weights(const float T[16]) {
+    Weights W = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float t0 = T[4 * i], t1 = T[4 * i + 1], t2 = T[4 * i + 2], t3 = T[4 * i + 3];
+        W.w01 = __builtin_fmaf(t0, t1, W.w01);
+        W.w02 = __builtin_fmaf(t0, t2, W.w02);
+        W.w03 = __builtin_fmaf(t0, t3, W.w03);
+        W.w12 = __builtin_fmaf(t1, t2, W.w12);
+        W.w13 = __builtin_fmaf(t1, t3, W.w13);
+        W.w23 = __builtin_fmaf(t2, t3, W.w23);
+    }
+    return W;
+}
+
+// Newton direction in log2 units: d = -log2(e) (Lap(W) + lam I)^{-1} g.
+// Elimination of nodes 0, 1, 2 in turn; every pivot is a sum of non-negative
+// conductances (lam acts as an extra conductance to the ground).
+__device__ __forceinline__ void newton_solve(const Weights& W, float g0, float g1, float g2, float lam,
+                                             float& d0, float& d1, float& d2) {
+    float r0 = -kLog2e * g0, r1 = -kLog2e * g1, r2 = -kLog2e * g2;
+    float q0 = W.w03 + lam, q1 = W.w13 + lam, q2 = W.w23 + lam;  // conductance to ground
+    const float i0 = rcp(__builtin_fmaxf(W.w01 + W.w02 + q0, kTiny));
+    const float f1 = W.w01 * i0, f2 = W.w02 * i0;
+    const float a12 = __builtin_fmaf(f1, W.w02, W.w12);
+    q1 = __builtin_fmaf(f1, q0, q1);
+    q2 = __builtin_fmaf(f2, q0, q2);
+    r1 = __builtin_fmaf(f1, r0, r1);
+    r2 = __builtin_fmaf(f2, r0, r2);
+    const float i1 = rcp(__builtin_fmaxf(a12 + q1, kTiny));
+    const float f2b = a12 * i1;
+    q2 = __builtin_fmaf(f2b, q1, q2);
+    r2 = __builtin_fmaf(f2b, r1, r2);
+    d2 = r2 * rcp(__builtin_fmaxf(q2, kTiny));
+    d1 = __builtin_fmaf(a12, d2, r1) * i1;
+    d0 = __builtin_fmaf(W.w01, d1, __builtin_fmaf(W.w02, d2, r0)) * i0;
+}
+
+template <int DT, bool WRITE_DUAL, bool WRITE_ITERS>
+__global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict__ H,
+                                                          float* __restrict__ P,
+                                                          float* __restrict__ dual,
+                                                          int32_t* __restrict__ iters, int64_t B,
+                                                          int64_t chunk, float tol, int max_iter) {
+    const int lane = threadIdx.x & 63;
+    const int64_t wave = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
+    const int64_t lo = wave * chunk;
+    if (lo >= B) return;  // uniform across the wave
+    const int64_t hi = (lo + chunk < B) ? lo + chunk : B;
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+
+    int64_t next = lo + 64;  // first unclaimed problem of this wave's range
+    int64_t idx = lo + lane;
+    bool active = idx < hi;
+    bool fresh = true;
+
+    float U[16];
+    float beta0 = 0.f, beta1 = 0.f, beta2 = 0.f;
+    float aoff[4], ls[4];
+    float d0 = 0.f, d1 = 0.f, d2 = 0.f;
+    float t = 0.f, tscale = 1.f, slope = 0.f, gn2 = 0.f;
+    float ga0 = 0.f, ga1 = 0.f, ga2 = 0.f, gamax = 0.f, lm_mult = 1.f;  // accepted gradient
+    Weights Wa = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};                       // accepted weights
+    int evals = 0;
+    bool first = true, nonfinite = false;
+
+    for (;;) {
+        bool fin = false;
+        if (active) {
+            if (fresh) {
+                // new problem: L = H log2(e); x^(0) = column-centring beta
+                float h[16];
+                load16<DT>(H, idx, h);
+                nonfinite = !all_finite16(h);
+                float cm[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    cm[j] = 0.25f * kLog2e * ((h[j] + h[4 + j]) + (h[8 + j] + h[12 + j]));
+                beta0 = cm[3] - cm[0];
+                beta1 = cm[3] - cm[1];
+                beta2 = cm[3] - cm[2];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    U[4 * i + 0] = nonfinite ? 0.f : __builtin_fmaf(h[4 * i + 0], kLog2e, beta0);
+                    U[4 * i + 1] = nonfinite ? 0.f : __builtin_fmaf(h[4 * i + 1], kLog2e, beta1);
+                    U[4 * i + 2] = nonfinite ? 0.f : __builtin_fmaf(h[4 * i + 2], kLog2e, beta2);
+                    U[4 * i + 3] = nonfinite ? 0.f : h[4 * i + 3] * kLog2e;
+                    aoff[i] = 0.f;
+                    ls[i] = 0.f;
+                }
+                if (nonfinite) beta0 = beta1 = beta2 = 0.f;
+                d0 = d1 = d2 = 0.f;
+                t = 0.f;
+                tscale = 1.f;
+                slope = 0.f;
+                gn2 = 0.f;
+                evals = 0;
+                first = true;
+                fresh = false;
+            }
+
+            const float td0 = t * d0, td1 = t * d1, td2 = t * d2;
+            float X[16], T[16], mrow[4], lsum[4], g[4];
+            evaluate(U, td0, td1, td2, X, T, mrow, lsum, g);
+            const float gmax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(g[0]), __builtin_fabsf(g[1])),
+                                               __builtin_fmaxf(__builtin_fabsf(g[2]), __builtin_fabsf(g[3])));
+            const float gn2t = g[0] * g[0] + g[1] * g[1] + g[2] * g[2] + g[3] * g[3];
+            // change of the reduced dual f (log2 units) from the accepted point
+            const float df = ((mrow[0] + lsum[0] - ls[0]) + (mrow[1] + lsum[1] - ls[1])) +
+                             ((mrow[2] + lsum[2] - ls[2]) + (mrow[3] + lsum[3] - ls[3])) -
+                             (td0 + td1 + td2);
+            const bool accept = first || (df <= kArmijo * t * slope) ||
+                                (__builtin_fabsf(df) < kFNoise && gn2t < gn2);
+            if (!first) ++evals;
+            bool conv = false;
+            if (accept) {
+                if (!first) {
+                    const float dd = g[0] * d0 + g[1] * d1 + g[2] * d2;
+                    tscale = (t >= 0.999f * tscale && dd < 0.25f * slope)
+                                 ? __builtin_fminf(2.f * tscale, kMaxExpand)
+                                 : 1.f;
+                }
+#pragma unroll
+                for (int q = 0; q < 16; ++q) U[q] = X[q];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    aoff[i] += mrow[i];
+                    ls[i] = lsum[i];
+                }
+                beta0 += td0;
+                beta1 += td1;
+                beta2 += td2;
+                gn2 = gn2t;
+                conv = gmax <= tol;
+            }
+            fin = conv || evals >= max_iter;
+            if (!fin) {
+                if (accept) {
+                    Wa = column_weights(T);
+                    ga0 = g[0];
+                    ga1 = g[1];
+                    ga2 = g[2];
+                    gamax = gmax;
+                    lm_mult = 1.f;
+                    t = tscale;
+                } else {
+                    // backtrack: halve the step and raise the Levenberg-Marquardt shift, so a
+                    // direction spoiled by rounding in weakly coupled modes is replaced
+                    t *= 0.5f;
+                    tscale = 1.f;
+                    lm_mult = __builtin_fminf(16.f * lm_mult, kMaxLMMult);
+                }
+                newton_solve(Wa, ga0, ga1, ga2, kLM * gamax * lm_mult, d0, d1, d2);
+                slope = ga0 * d0 + ga1 * d1 + ga2 * d2;
+                const float dm = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(d0), __builtin_fabsf(d1)),
+                                                 __builtin_fabsf(d2));
+                t = __builtin_fminf(t, kCap2 * rcp(__builtin_fmaxf(dm, kTiny)));
+                first = false;
+            } else {
+                if (!accept) {
+                    // the last trial was rejected: report the accepted point
+                    evaluate(U, 0.f, 0.f, 0.f, X, T, mrow, lsum, g);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        aoff[i] += mrow[i];
+                        ls[i] = lsum[i];
+                    }
+                }
+                if (nonfinite) {
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) T[q] = __builtin_nanf("");
+                }
+                store16(P, idx, T);
+                if constexpr (WRITE_DUAL) {
+                    const float nan = __builtin_nanf("");
+                    v4f* dp = reinterpret_cast<v4f*>(dual) + 2 * idx;
+                    const float a0 = nonfinite ? nan : -(aoff[0] + ls[0]) * kLn2;
+                    const float a1 = nonfinite ? nan : -(aoff[1] + ls[1]) * kLn2;
+                    const float a2 = nonfinite ? nan : -(aoff[2] + ls[2]) * kLn2;
+                    const float a3 = nonfinite ? nan : -(aoff[3] + ls[3]) * kLn2;
+                    const v4f va = {a0, a1, a2, a3};
+                    const v4f vb = {nonfinite ? nan : beta0 * kLn2, nonfinite ? nan : beta1 * kLn2,
+                                    nonfinite ? nan : beta2 * kLn2, nonfinite ? nan : 0.f};
+                    __builtin_nontemporal_store(va, dp);
+                    __builtin_nontemporal_store(vb, dp + 1);
+                }
+                if constexpr (WRITE_ITERS) {
+                    iters[idx] = nonfinite ? BIRKHOFF4_NON_FINITE
+                                           : (conv ? evals : BIRKHOFF4_NOT_CONVERGED);
+                }
+            }
+        }
+        // refill: finished lanes claim the next problems of the wave's range in lane order
+        const uint64_t fm = __ballot(fin);
+        if (fm) {
+            if (fin) {
+                idx = next + __popcll(fm & below);
+                active = idx < hi;
+                fresh = true;
+            }
+            next += __popcll(fm);
+        }
+        if (__ballot(active) == 0) break;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Backward (Sec. 4.2)
+// ---------------------------------------------------------------------------
+template <int DT>
+__global__ __launch_bounds__(256) void implicit_bwd_kernel(const float* __restrict__ P,
+                                                            const void* __restrict__ dP,
+                                                            float* __restrict__ dH, int64_t B) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t b = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; b < B; b += stride) {
+        float T[16], G[16];
+        load16_f32(P, b, T);
+        load16<DT>(dP, b, G);
+        // W_jk = sum_i T_ij T_ik; F_jk = sum_i T_ij T_ik (G_ij - G_ik): the right-hand
+        // side mu_c,j - sum_i T_ij mu_r,i of eq. derivative is sum_{k != j} F_jk.
+        float W01 = 0.f, W02 = 0.f, W03 = 0.f, W12 = 0.f, W13 = 0.f, W23 = 0.f;
+        float F01 = 0.f, F02 = 0.f, F03 = 0.f, F12 = 0.f, F13 = 0.f, F23 = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float t0 = T[4 * i], t1 = T[4 * i + 1], t2 = T[4 * i + 2], t3 = T[4 * i + 3];
+            const float g0 = G[4 * i], g1 = G[4 * i + 1], g2 = G[4 * i + 2], g3 = G[4 * i + 3];
+            float p;
+            p = t0 * t1; W01 += p; F01 = __builtin_fmaf(p, g0 - g1, F01);
+            p = t0 * t2; W02 += p; F02 = __builtin_fmaf(p, g0 - g2, F02);
+            p = t0 * t3; W03 += p; F03 = __builtin_fmaf(p, g0 - g3, F03);
+            p = t1 * t2; W12 += p; F12 = __builtin_fmaf(p, g1 - g2, F12);
+            p = t1 * t3; W13 += p; F13 = __builtin_fmaf(p, g1 - g3, F13);
+            p = t2 * t3; W23 += p; F23 = __builtin_fmaf(p, g2 - g3, F23);
+        }
+        // Delta w = rhs, Delta = Hessian at T (Laplacian of W grounded at column 4).
+        // Eliminating a node joins its neighbours j,k by W_jp W_pk / piv and moves its
+        // flows onto the same edges, F_jk += (W_pk F_jp + W_jp F_pk) / piv, so every
+        // right-hand side stays a sum of antisymmetric edge flows.
+        const float piv0 = W01 + W02 + W03;
+        const float i0 = piv0 > 0.f ? rcp(piv0) : 0.f;
+        const float W12b = __builtin_fmaf(W01 * W02, i0, W12);
+        const float W13b = __builtin_fmaf(W01 * W03, i0, W13);
+        const float W23b = __builtin_fmaf(W02 * W03, i0, W23);
+        const float F12b = __builtin_fmaf(W01 * F02 - W02 * F01, i0, F12);
+        const float F13b = __builtin_fmaf(W01 * F03 - W03 * F01, i0, F13);
+        const float F23b = __builtin_fmaf(W02 * F03 - W03 * F02, i0, F23);
+        const float piv1 = W12b + W13b;
+        const float i1 = piv1 > 0.f ? rcp(piv1) : 0.f;
+        const float W23c = __builtin_fmaf(W12b * W13b, i1, W23b);
+        const float F23c = __builtin_fmaf(W12b * F13b - W13b * F12b, i1, F23b);
+        const float w2 = W23c > 0.f ? F23c * rcp(W23c) : 0.f;
+        const float w1 = __builtin_fmaf(W12b, w2, F12b + F13b) * i1;
+        const float w0 = __builtin_fmaf(W01, w1, __builtin_fmaf(W02, w2, (F01 + F02) + F03)) * i0;
+        // dH = -D: dH_ij = T_ij (psi_ij - sum_k T_ik psi_ik), psi = G - 1 w^T, w_4 = 0
+        float out[16];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float s0 = G[4 * i] - w0, s1 = G[4 * i + 1] - w1, s2 = G[4 * i + 2] - w2,
+                        s3 = G[4 * i + 3];
+            const float avg = __builtin_fmaf(T[4 * i], s0,
+                              __builtin_fmaf(T[4 * i + 1], s1,
+                              __builtin_fmaf(T[4 * i + 2], s2, T[4 * i + 3] * s3)));
+            out[4 * i + 0] = T[4 * i + 0] * (s0 - avg);
+            out[4 * i + 1] = T[4 * i + 1] * (s1 - avg);
+            out[4 * i + 2] = T[4 * i + 2] * (s2 - avg);
+            out[4 * i + 3] = T[4 * i + 3] * (s3 - avg);
+        }
+        store16(dH, b, out);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Sinkhorn-Knopp baseline (eq. sinkhorn_knopp), one problem per lane
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void sk_kernel_matrix(const float h[16], float A[16]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float m = __builtin_fmaxf(__builtin_fmaxf(h[4 * i], h[4 * i + 1]),
+                                        __builtin_fmaxf(h[4 * i + 2], h[4 * i + 3]));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) A[4 * i + j] = ex2((h[4 * i + j] - m) * kLog2e);
+    }
+}
+
+// u = 1 / max(A v, FLT_MIN), v = 1 / max(A^T u, FLT_MIN)
+__device__ __forceinline__ void sk_u(const float A[16], const float v[4], float u[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        u[i] = rcp(__builtin_fmaxf(__builtin_fmaf(A[4 * i], v[0], __builtin_fmaf(A[4 * i + 1], v[1],
+                   __builtin_fmaf(A[4 * i + 2], v[2], A[4 * i + 3] * v[3]))), kFltMin));
+}
+__device__ __forceinline__ void sk_v(const float A[16], const float u[4], float v[4]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        v[j] = rcp(__builtin_fmaxf(__builtin_fmaf(A[j], u[0], __builtin_fmaf(A[4 + j], u[1],
+                   __builtin_fmaf(A[8 + j], u[2], A[12 + j] * u[3]))), kFltMin));
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void sk_fwd_kernel(const void* __restrict__ H, float* __restrict__ P,
+                                                      int64_t B, int n_steps) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t b = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; b < B; b += stride) {
+        float h[16], A[16], u[4], v[4] = {1.f, 1.f, 1.f, 1.f};
+        load16<DT>(H, b, h);
+        sk_kernel_matrix(h, A);
+        for (int k = 0; k < n_steps; ++k) {
+            sk_u(A, v, u);
+            sk_v(A, u, v);
+        }
+        float out[16];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) out[4 * i + j] = u[i] * A[4 * i + j] * v[j];
+        store16(P, b, out);
+    }
+}
+
+// Reverse mode through the n-step map. The iterates v^(k) are kept in LDS (one
+// 64-lane block, [k][component][lane] so that lanes hit distinct banks); u^(k) is
+// recomputed from v^(k-1). A clamped denominator contributes no gradient.
+template <int DT, int DG>
+__global__ __launch_bounds__(64) void sk_bwd_kernel(const void* __restrict__ H,
+                                                     const void* __restrict__ dP,
+                                                     float* __restrict__ dH, int64_t B, int n_steps) {
+    extern __shared__ float vbuf[];  // [(n_steps + 1) * 4][64]
+    const int lane = threadIdx.x;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t b = static_cast<int64_t>(blockIdx.x) * blockDim.x + lane; b < B; b += stride) {
+        float h[16], G[16], A[16], u[4], v[4] = {1.f, 1.f, 1.f, 1.f};
+        load16<DT>(H, b, h);
+        load16<DG>(dP, b, G);
+        sk_kernel_matrix(h, A);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) vbuf[j * 64 + lane] = 1.f;
+        for (int k = 1; k <= n_steps; ++k) {
+            sk_u(A, v, u);
+            sk_v(A, u, v);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) vbuf[(4 * k + j) * 64 + lane] = v[j];
+        }
+        float Ab[16], ub[4], vb[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ub[i] = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) vb[j] = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float gg = G[4 * i + j];
+                Ab[4 * i + j] = gg * u[i] * v[j];
+                ub[i] = __builtin_fmaf(gg * A[4 * i + j], v[j], ub[i]);
+                vb[j] = __builtin_fmaf(gg * u[i], A[4 * i + j], vb[j]);
+            }
+        for (int k = n_steps; k >= 1; --k) {
+            float vk[4], vp[4], uk[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                vk[j] = vbuf[(4 * k + j) * 64 + lane];
+                vp[j] = vbuf[(4 * (k - 1) + j) * 64 + lane];
+            }
+            sk_u(A, vp, uk);
+            // v^(k) = 1 / max(A^T u^(k), FLT_MIN)
+            float bb[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float den = __builtin_fmaf(A[j], uk[0], __builtin_fmaf(A[4 + j], uk[1],
+                                  __builtin_fmaf(A[8 + j], uk[2], A[12 + j] * uk[3])));
+                bb[j] = den >= kFltMin ? -vb[j] * vk[j] * vk[j] : 0.f;
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    ub[i] = __builtin_fmaf(A[4 * i + j], bb[j], ub[i]);
+                    Ab[4 * i + j] = __builtin_fmaf(uk[i], bb[j], Ab[4 * i + j]);
+                }
+            // u^(k) = 1 / max(A v^(k-1), FLT_MIN)
+            float ab[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float den = __builtin_fmaf(A[4 * i], vp[0], __builtin_fmaf(A[4 * i + 1], vp[1],
+                                  __builtin_fmaf(A[4 * i + 2], vp[2], A[4 * i + 3] * vp[3])));
+                ab[i] = den >= kFltMin ? -ub[i] * uk[i] * uk[i] : 0.f;
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) vb[j] = 0.f;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    vb[j] = __builtin_fmaf(A[4 * i + j], ab[i], vb[j]);
+                    Ab[4 * i + j] = __builtin_fmaf(ab[i], vp[j], Ab[4 * i + j]);
+                }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) ub[i] = 0.f;
+        }
+        float out[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) out[q] = Ab[q] * A[q];
+        store16(dH, b, out);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------
+constexpr int kMaxDevices = 64;
+int g_cus[kMaxDevices];  // cached compute-unit counts (0 = not queried yet)
+
+int device_cus(int* cus) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return BIRKHOFF4_ERR_DEVICE;
+    if (g_cus[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            return BIRKHOFF4_ERR_DEVICE;
+        g_cus[dev] = n;
+    }
+    *cus = g_cus[dev];
+    return BIRKHOFF4_OK;
+}
+
+bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+    if (!a || !b || na == 0 || nb == 0) return false;
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + nb && y < x + na;
+}
+
+size_t dtype_bytes(int dt) { return dt == BIRKHOFF4_BF16 ? 2 : 4; }
+bool dtype_ok(int dt) { return dt == BIRKHOFF4_F32 || dt == BIRKHOFF4_BF16; }
+
+int launch_status() {
+    return hipGetLastError() == hipSuccess ? BIRKHOFF4_OK : BIRKHOFF4_ERR_LAUNCH;
+}
+
+constexpr int kFwdBlock = 256;
+
+// Blocks of the forward kernel resident at once on one CU (VGPR-limited),
+// from the occupancy calculator; queried once per instantiation.
+template <int DT, bool WD, bool WI>
+int fwd_blocks_per_cu() {
+    static int cached = 0;
+    if (cached == 0) {
+        int nb = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, newton_fwd_kernel<DT, WD, WI>, kFwdBlock, 0) !=
+                hipSuccess || nb <= 0)
+            nb = 4;
+        cached = nb;
+    }
+    return cached;
+}
+
+// Launch exactly as many waves as can be resident, each owning a contiguous
+// range of problems (lane-level refill inside the range).
+template <int DT, bool WD, bool WI>
+int launch_fwd(const void* H, float* P, float* dual, int32_t* iters, int64_t B, float tol,
+               int max_iter, hipStream_t stream, int cus) {
+    const int64_t waves_needed = (B + 63) / 64;
+    int64_t waves = static_cast<int64_t>(cus) * fwd_blocks_per_cu<DT, WD, WI>() * (kFwdBlock / 64);
+    if (waves > waves_needed) waves = waves_needed;
+    const int64_t chunk = (B + waves - 1) / waves;
+    waves = (B + chunk - 1) / chunk;
+    const int64_t blocks = (waves * 64 + kFwdBlock - 1) / kFwdBlock;
+    hipLaunchKernelGGL((newton_fwd_kernel<DT, WD, WI>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(kFwdBlock), 0, stream, H, P, dual, iters, B, chunk, tol, max_iter);
+    return launch_status();
+}
+
+template <int DT>
+int dispatch_fwd(const void* H, float* P, float* dual, int32_t* iters, int64_t B, float tol,
+                 int max_iter, hipStream_t stream, int cus) {
+    if (dual && iters) return launch_fwd<DT, true, true>(H, P, dual, iters, B, tol, max_iter, stream, cus);
+    if (dual) return launch_fwd<DT, true, false>(H, P, dual, iters, B, tol, max_iter, stream, cus);
+    if (iters) return launch_fwd<DT, false, true>(H, P, dual, iters, B, tol, max_iter, stream, cus);
+    return launch_fwd<DT, false, false>(H, P, dual, iters, B, tol, max_iter, stream, cus);
+}
+
+int64_t grid_for(int64_t B, int block, int cus, int per_cu) {
+    int64_t blocks = (B + block - 1) / block;
+    const int64_t cap = static_cast<int64_t>(cus) * per_cu;
+    return blocks < cap ? blocks : cap;
+}
+
+}  // namespace
+
+extern "C" {
+
+int birkhoff4_fwd_ex(const void* H, int h_dtype, float* P, float* dual, int32_t* iters, int64_t B,
+                     float tol, int max_iter, hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 64)) return BIRKHOFF4_ERR_SIZE;
+    if (!dtype_ok(h_dtype)) return BIRKHOFF4_ERR_DTYPE;
+    if (!(tol >= 0.f)) return BIRKHOFF4_ERR_TOL;
+    if (max_iter < 0 || max_iter > kMaxIterCap) return BIRKHOFF4_ERR_MAX_ITER;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!H || !P) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(H) || misaligned(P) || misaligned(dual) || misaligned(iters)) return BIRKHOFF4_ERR_ALIGN;
+    const size_t nh = static_cast<size_t>(B) * 16 * dtype_bytes(h_dtype);
+    const size_t np = static_cast<size_t>(B) * 64, nd = dual ? static_cast<size_t>(B) * 32 : 0,
+                 ni = iters ? static_cast<size_t>(B) * 4 : 0;
+    if (overlaps(H, nh, P, np) || overlaps(H, nh, dual, nd) || overlaps(H, nh, iters, ni) ||
+        overlaps(P, np, dual, nd) || overlaps(P, np, iters, ni) || overlaps(dual, nd, iters, ni))
+        return BIRKHOFF4_ERR_OVERLAP;
+    int cus = 0;
+    if (int e = device_cus(&cus)) return e;
+    if (h_dtype == BIRKHOFF4_BF16)
+        return dispatch_fwd<BIRKHOFF4_BF16>(H, P, dual, iters, B, tol, max_iter, stream, cus);
+    return dispatch_fwd<BIRKHOFF4_F32>(H, P, dual, iters, B, tol, max_iter, stream, cus);
+}
+
+int birkhoff4_fwd(const float* H, float* P, float* dual, int64_t B, float tol, int max_iter,
+                  hipStream_t stream) {
+    return birkhoff4_fwd_ex(H, BIRKHOFF4_F32, P, dual, nullptr, B, tol, max_iter, stream);
+}
+
+int birkhoff4_bwd_ex(const float* P, const void* dP, int dp_dtype, float* dH, int64_t B,
+                     hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 64)) return BIRKHOFF4_ERR_SIZE;
+    if (!dtype_ok(dp_dtype)) return BIRKHOFF4_ERR_DTYPE;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!P || !dP || !dH) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(P) || misaligned(dP) || misaligned(dH)) return BIRKHOFF4_ERR_ALIGN;
+    const size_t n = static_cast<size_t>(B) * 64, ng = static_cast<size_t>(B) * 16 * dtype_bytes(dp_dtype);
+    if (overlaps(dH, n, P, n) || overlaps(dH, n, dP, ng)) return BIRKHOFF4_ERR_OVERLAP;
+    int cus = 0;
+    if (int e = device_cus(&cus)) return e;
+    const int64_t grid = grid_for(B, 256, cus, 64);
+    if (dp_dtype == BIRKHOFF4_BF16)
+        hipLaunchKernelGGL(implicit_bwd_kernel<BIRKHOFF4_BF16>, dim3(static_cast<unsigned>(grid)), dim3(256),
+                           0, stream, P, dP, dH, B);
+    else
+        hipLaunchKernelGGL(implicit_bwd_kernel<BIRKHOFF4_F32>, dim3(static_cast<unsigned>(grid)), dim3(256),
+                           0, stream, P, dP, dH, B);
+    return launch_status();
+}
+
+int birkhoff4_bwd(const float* P, const float* dual, const float* dP, float* dH, int64_t B,
+                  hipStream_t stream) {
+    (void)dual;  // the 4x4 backward needs only T* and G (Sec. 4.2)
+    return birkhoff4_bwd_ex(P, dP, BIRKHOFF4_F32, dH, B, stream);
+}
+
+int birkhoff4_sk_fwd(const void* H, int h_dtype, float* P, int64_t B, int n_steps, hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 64)) return BIRKHOFF4_ERR_SIZE;
+    if (!dtype_ok(h_dtype)) return BIRKHOFF4_ERR_DTYPE;
+    if (n_steps < 1 || n_steps > kMaxSkSteps) return BIRKHOFF4_ERR_STEPS;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!H || !P) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(H) || misaligned(P)) return BIRKHOFF4_ERR_ALIGN;
+    if (overlaps(H, static_cast<size_t>(B) * 16 * dtype_bytes(h_dtype), P, static_cast<size_t>(B) * 64))
+        return BIRKHOFF4_ERR_OVERLAP;
+    int cus = 0;
+    if (int e = device_cus(&cus)) return e;
+    const int64_t grid = grid_for(B, 256, cus, 64);
+    if (h_dtype == BIRKHOFF4_BF16)
+        hipLaunchKernelGGL(sk_fwd_kernel<BIRKHOFF4_BF16>, dim3(static_cast<unsigned>(grid)), dim3(256), 0,
+                           stream, H, P, B, n_steps);
+    else
+        hipLaunchKernelGGL(sk_fwd_kernel<BIRKHOFF4_F32>, dim3(static_cast<unsigned>(grid)), dim3(256), 0,
+                           stream, H, P, B, n_steps);
+    return launch_status();
+}
+
+int birkhoff4_sk_bwd(const void* H, int h_dtype, const void* dP, int dp_dtype, float* dH, int64_t B,
+                     int n_steps, hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 64)) return BIRKHOFF4_ERR_SIZE;
+    if (!dtype_ok(h_dtype) || !dtype_ok(dp_dtype)) return BIRKHOFF4_ERR_DTYPE;
+    if (n_steps < 1 || n_steps > kMaxSkSteps) return BIRKHOFF4_ERR_STEPS;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!H || !dP || !dH) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(H) || misaligned(dP) || misaligned(dH)) return BIRKHOFF4_ERR_ALIGN;
+    const size_t n = static_cast<size_t>(B) * 64;
+    if (overlaps(dH, n, H, static_cast<size_t>(B) * 16 * dtype_bytes(h_dtype)) ||
+        overlaps(dH, n, dP, static_cast<size_t>(B) * 16 * dtype_bytes(dp_dtype)))
+        return BIRKHOFF4_ERR_OVERLAP;
+    int cus = 0;
+    if (int e = device_cus(&cus)) return e;
+    const int64_t grid = grid_for(B, 64, cus, 64);
+    const size_t lds = static_cast<size_t>(n_steps + 1) * 4 * 64 * sizeof(float);
+    const dim3 g(static_cast<unsigned>(grid)), blk(64);
+    if (h_dtype == BIRKHOFF4_BF16) {
+        if (dp_dtype == BIRKHOFF4_BF16)
+            hipLaunchKernelGGL((sk_bwd_kernel<BIRKHOFF4_BF16, BIRKHOFF4_BF16>), g, blk, lds, stream, H, dP, dH, B, n_steps);
+        else
+            hipLaunchKernelGGL((sk_bwd_kernel<BIRKHOFF4_BF16, BIRKHOFF4_F32>), g, blk, lds, stream, H, dP, dH, B, n_steps);
+    } else {
+        if (dp_dtype == BIRKHOFF4_BF16)
+            hipLaunchKernelGGL((sk_bwd_kernel<BIRKHOFF4_F32, BIRKHOFF4_BF16>), g, blk, lds, stream, H, dP, dH, B, n_steps);
+        else
+            hipLaunchKernelGGL((sk_bwd_kernel<BIRKHOFF4_F32, BIRKHOFF4_F32>), g, blk, lds, stream, H, dP, dH, B, n_steps);
+    }
+    return launch_status();
+}
+
+const char* birkhoff4_strerror(int code) {
+    switch (code) {
+        case BIRKHOFF4_OK: return "ok";
+        case BIRKHOFF4_ERR_NULL: return "a required pointer is NULL";
+        case BIRKHOFF4_ERR_SIZE: return "batch size out of range";
+        case BIRKHOFF4_ERR_TOL: return "tol must be >= 0";
+        case BIRKHOFF4_ERR_MAX_ITER: return "max_iter must be in [0, 10000]";
+        case BIRKHOFF4_ERR_DTYPE: return "unknown dtype code";
+        case BIRKHOFF4_ERR_ALIGN: return "arrays must be 16-byte aligned";
+        case BIRKHOFF4_ERR_OVERLAP: return "an output overlaps another argument";
+        case BIRKHOFF4_ERR_STEPS: return "Sinkhorn step count must be in [1, 48]";
+        case BIRKHOFF4_ERR_DEVICE: return "HIP device query failed";
+        case BIRKHOFF4_ERR_LAUNCH: return "kernel launch failed";
+        default: return "unknown error";
+    }
+}
+
+int birkhoff4_version(void) { return 100; }
+
+}  // extern "C"

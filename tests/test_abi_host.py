@@ -1,0 +1,103 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+The library must load, export every entry point that include/birkhoff4.h
+declares, and reject bad arguments on the host before touching the device.
+The calls below use fake device addresses: every one of them fails validation
+and returns before any HIP call, so nothing is dereferenced.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_07574_amd as b4
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "birkhoff4.h")
+
+OK, ERR_NULL, ERR_SIZE, ERR_TOL, ERR_MAX_ITER, ERR_DTYPE, ERR_ALIGN, ERR_OVERLAP, ERR_STEPS = (
+    0, -1, -2, -3, -4, -5, -6, -7, -8)
+
+A = 0x10000000        # fake, 16-byte aligned device addresses far apart
+Bp = 0x20000000
+C = 0x30000000
+D = 0x40000000
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(birkhoff4_\w+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    lib = ctypes.CDLL(b4.LIB_PATH)
+    names = declared_functions()
+    assert {"birkhoff4_fwd", "birkhoff4_bwd", "birkhoff4_fwd_ex", "birkhoff4_bwd_ex",
+            "birkhoff4_sk_fwd", "birkhoff4_sk_bwd"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_strerror():
+    lib = b4.lib()
+    assert lib.birkhoff4_version() >= 100
+    for code in range(-10, 1):
+        assert lib.birkhoff4_strerror(code)
+    assert lib.birkhoff4_strerror(-999) == b"unknown error"
+
+
+def test_forward_argument_errors():
+    lib = b4.lib()
+    f = lib.birkhoff4_fwd
+    assert f(A, Bp, C, 0, 1e-6, 20, None) == OK              # B = 0 is a no-op
+    assert f(None, None, None, 0, 1e-6, 20, None) == OK
+    assert f(A, Bp, C, -1, 1e-6, 20, None) == ERR_SIZE
+    assert f(None, Bp, C, 10, 1e-6, 20, None) == ERR_NULL
+    assert f(A, None, C, 10, 1e-6, 20, None) == ERR_NULL
+    assert f(A, Bp, C, 10, -1.0, 20, None) == ERR_TOL
+    assert f(A, Bp, C, 10, float("nan"), 20, None) == ERR_TOL
+    assert f(A, Bp, C, 10, 1e-6, -1, None) == ERR_MAX_ITER
+    assert f(A, Bp, C, 10, 1e-6, 10001, None) == ERR_MAX_ITER
+    assert f(A + 4, Bp, C, 10, 1e-6, 20, None) == ERR_ALIGN
+    assert f(A, Bp + 8, C, 10, 1e-6, 20, None) == ERR_ALIGN
+    assert f(A, A + 64 * 5, C, 10, 1e-6, 20, None) == ERR_OVERLAP   # P inside H
+    assert f(A, Bp, Bp + 64 * 9, 10, 1e-6, 20, None) == ERR_OVERLAP  # dual inside P
+    fx = lib.birkhoff4_fwd_ex
+    assert fx(A, 7, Bp, C, None, 10, 1e-6, 20, None) == ERR_DTYPE
+    assert fx(A, 1, Bp, C, D + 4, 10, 1e-6, 20, None) == ERR_ALIGN
+    assert fx(A, 1, Bp, C, C + 32 * 3, 10, 1e-6, 20, None) == ERR_OVERLAP  # iters inside dual
+    # bf16 H occupies 32 B per matrix: P 32 B too early does overlap
+    assert fx(A, 1, A + 32 * 9, None, None, 10, 1e-6, 20, None) == ERR_OVERLAP
+
+
+def test_backward_and_baseline_argument_errors():
+    lib = b4.lib()
+    g = lib.birkhoff4_bwd
+    assert g(A, None, Bp, C, 0, None) == OK
+    assert g(A, None, Bp, C, -5, None) == ERR_SIZE
+    assert g(None, None, Bp, C, 5, None) == ERR_NULL
+    assert g(A, None, None, C, 5, None) == ERR_NULL
+    assert g(A, None, Bp, None, 5, None) == ERR_NULL
+    assert g(A, None, Bp, A + 16, 5, None) in (ERR_ALIGN, ERR_OVERLAP)
+    assert g(A, None, Bp, Bp + 64, 5, None) == ERR_OVERLAP
+    assert lib.birkhoff4_bwd_ex(A, Bp, 3, C, 5, None) == ERR_DTYPE
+    s = lib.birkhoff4_sk_fwd
+    assert s(A, 0, Bp, 5, 0, None) == ERR_STEPS
+    assert s(A, 0, Bp, 5, 49, None) == ERR_STEPS
+    assert s(A, 0, Bp, 0, 20, None) == OK
+    assert s(A, 5, Bp, 5, 20, None) == ERR_DTYPE
+    sb = lib.birkhoff4_sk_bwd
+    assert sb(A, 0, Bp, 0, C, 5, 0, None) == ERR_STEPS
+    assert sb(A, 0, Bp, 9, C, 5, 20, None) == ERR_DTYPE
+    assert sb(A, 0, Bp, 0, A + 64, 5, 20, None) == ERR_OVERLAP
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    H = torch.zeros(3, 4, 4)
+    with pytest.raises(b4.Birkhoff4Error):
+        b4.fwd(H)
+    with pytest.raises(b4.Birkhoff4Error):
+        b4.bwd(H, H)
