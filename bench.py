@@ -65,12 +65,14 @@ def main() -> int:
     ap.add_argument("--workload", default="mix_bf16_b2e24")
     ap.add_argument("--tol", type=float, default=1e-6)
     ap.add_argument("--max-iter", type=int, default=64)
-    ap.add_argument("--cpu-sample", type=int, default=1 << 20,
+    ap.add_argument("--cpu-sample", type=int, default=1 << 24,
                     help="matrices in the oracle's CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sk", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="time only the path (for profiler runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB device copy 5 times (scale for HBM byte counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -90,6 +92,15 @@ def main() -> int:
         return 2
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration:
+        X = torch.ones(1 << 28, device=dev)
+        Y = torch.empty_like(X)
+        for _ in range(5):
+            Y.copy_(X)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration": {"bytes_read": X.numel() * 4, "bytes_written": Y.numel() * 4,
+                                               "launches": 5}}), flush=True)
+        return 0
     w = workloads.WORKLOADS[args.workload]
     B = w.B
     bf16 = w.storage == "bf16"

@@ -8,7 +8,9 @@
 //
 // Mapping: one 4x4 problem per lane; all per-problem state lives in VGPRs. No
 // MFMA (the only products are six 4-long dot products per matrix), no LDS in
-// the Newton and implicit kernels, no atomics.
+// the Newton and implicit kernels, no atomics. Loads and stores are plain 16-byte
+// vector accesses (non-temporal hints measured slower on gfx950: the stores
+// lose write combining).
 //
 // Forward numerics (fp32, log2 domain so that v_exp_f32 applies directly):
 //  * state is U = H*log2(e) + beta - a 1^T with every row re-centred to max 0
@@ -18,10 +20,11 @@
 //  * Hessian of the reduced dual = Laplacian of the column graph with weights
 //    W_jk = sum_i T_ij T_ik (rows of T sum to one), grounded at column 4; the
 //    Newton system is solved by elimination with pivots formed as sums of these
-//    positive weights, plus a Levenberg-Marquardt shift 1e-3 * max_j |g_j| that
-//    vanishes at the solution and keeps directions finite when weights
-//    underflow;
-//  * step: capped at |d|_inf <= 8 (natural-log units), Armijo backtracking on the
+//    positive weights, plus a Levenberg-Marquardt shift max(1e-3 max_j |g_j|, 5e-8)
+//    that keeps directions finite when weights underflow and keeps gradient
+//    components at the fp32 rounding floor from driving huge steps;
+//  * step: spread of the column shifts max_j d_j - min_j d_j (with d_4 = 0) capped at 8
+//    (natural-log units), Armijo backtracking on the
 //    reduced dual f, with a gradient-norm test once f no longer resolves the
 //    decrease; each backtrack halves the step and multiplies the shift by 16
 //    (re-solving with the saved weights), and the trial step doubles while full
@@ -32,7 +35,9 @@
 // Lane-level work refill: each wave owns a contiguous range of problems; a
 // lane whose problem is finished writes it out and takes the next unclaimed
 // problem of its wave's range at once, so a wave pays the mean number of
-// Newton steps, not the maximum over its 64 lanes.
+// Newton steps, not the maximum over its 64 lanes. The next 64 problems of the
+// range are prefetched into a register ring spread over the wave's lanes and
+// handed to finishing lanes with ds_bpermute, so a refill never waits on HBM.
 
 #include <hip/hip_runtime.h>
 
@@ -48,11 +53,19 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kCap2 = 8.0f * kLog2e;  // step cap in log2 units
 constexpr float kLM = 1e-3f;            // Levenberg-Marquardt coefficient
+// Floor of the shift: column sums are rounded to ~2e-7 in fp32, so a gradient at that
+// level is noise; with the floor it can move a weakly coupled column by a few nats at
+// most instead of swamping the step that the real residual needs.
+constexpr float kLMFloor = 5e-8f;
 constexpr float kArmijo = 1e-4f;
 constexpr float kFNoise = 4e-6f;        // |delta f| below this is rounding noise
 constexpr float kMaxExpand = 16.0f;
 constexpr float kMaxLMMult = 1e20f;     // keeps the shift finite (|g| <= 4)
 constexpr float kTiny = 1e-30f;
+// Backward pivots at or below this are treated as disconnected nodes (potential 0):
+// v_rcp_f32 of a denormal is infinite, and such a node's entries of dH carry
+// factors of T that are far below fp32 resolution anyway.
+constexpr float kPivMin = 1e-30f;
 constexpr float kFltMin = 1.17549435e-38f;
 constexpr int kMaxSkSteps = 48;   // sk_bwd keeps (n+1) x 4 floats per lane in LDS
 constexpr int kMaxIterCap = 10000;
@@ -71,7 +84,7 @@ __device__ __forceinline__ void load16_f32(const float* base, int64_t b, float v
     const v4f* p = reinterpret_cast<const v4f*>(base) + 4 * b;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-        const v4f r = __builtin_nontemporal_load(p + q);
+        const v4f r = *(p + q);
         v[4 * q + 0] = r.x;
         v[4 * q + 1] = r.y;
         v[4 * q + 2] = r.z;
@@ -83,7 +96,7 @@ __device__ __forceinline__ void load16_bf16(const uint16_t* base, int64_t b, flo
     const v4u* p = reinterpret_cast<const v4u*>(base) + 2 * b;
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-        const v4u r = __builtin_nontemporal_load(p + q);
+        const v4u r = *(p + q);
         const uint32_t w[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -101,55 +114,82 @@ __device__ __forceinline__ void load16(const void* base, int64_t b, float v[16])
         load16_f32(static_cast<const float*>(base), b, v);
 }
 
+// Raw storage words of one problem (8 for bf16, 16 for fp32), kept undecoded in the
+// prefetch ring and moved between lanes with ds_bpermute.
+template <int DT>
+struct RawWords {
+    static constexpr int n = (DT == BIRKHOFF4_BF16) ? 8 : 16;
+};
+
+template <int DT>
+__device__ __forceinline__ void load_raw(const void* base, int64_t b, uint32_t w[RawWords<DT>::n]) {
+    const v4u* p = reinterpret_cast<const v4u*>(base) + (RawWords<DT>::n / 4) * b;
+#pragma unroll
+    for (int q = 0; q < RawWords<DT>::n / 4; ++q) {
+        const v4u r = p[q];
+        w[4 * q + 0] = r.x;
+        w[4 * q + 1] = r.y;
+        w[4 * q + 2] = r.z;
+        w[4 * q + 3] = r.w;
+    }
+}
+
+template <int DT>
+__device__ __forceinline__ void decode_raw(const uint32_t w[RawWords<DT>::n], float h[16]) {
+    if constexpr (DT == BIRKHOFF4_BF16) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            h[2 * k + 0] = __uint_as_float(w[k] << 16);
+            h[2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) h[k] = __uint_as_float(w[k]);
+    }
+}
+
 __device__ __forceinline__ void store16(float* base, int64_t b, const float v[16]) {
     v4f* p = reinterpret_cast<v4f*>(base) + 4 * b;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         const v4f r = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
-        __builtin_nontemporal_store(r, p + q);
+        *(p + q) = r;
     }
-}
-
-__device__ __forceinline__ bool all_finite16(const float v[16]) {
-    bool ok = true;
-#pragma unroll
-    for (int q = 0; q < 16; ++q) ok = ok && (__builtin_fabsf(v[q]) <= 3.402823466e38f);
-    return ok;
 }
 
 // ---------------------------------------------------------------------------
 // Forward
 // ---------------------------------------------------------------------------
 
-// Row-softmax evaluation at the trial point U + t d (log2 units), eq. tij_stable:
-// X = re-centred trial (new U if accepted), T = softmax rows, mrow = row maxima,
-// lsum = log2 of the row sums of 2^X, g = column sums - 1 (eq. c_g, all four).
-__device__ __forceinline__ void evaluate(const float U[16], float td0, float td1, float td2,
-                                         float X[16], float T[16], float mrow[4], float lsum[4],
-                                         float g[4]) {
+// Row-softmax evaluation at the trial point U + s (log2 units, s_4 = 0), eq. tij_stable.
+// U is replaced by the trial re-centred per row (the new current point); T = the row
+// softmax; mrow = row maxima removed; lsum = log2 of the row sums of 2^U; g = column
+// sums - 1 (eq. c_g, all four columns).
+__device__ __forceinline__ void evaluate_inplace(float U[16], float s0, float s1, float s2, float T[16],
+                                                 float mrow[4], float lsum[4], float g[4]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const float u0 = U[4 * i + 0] + td0;
-        const float u1 = U[4 * i + 1] + td1;
-        const float u2 = U[4 * i + 2] + td2;
+        const float u0 = U[4 * i + 0] + s0;
+        const float u1 = U[4 * i + 1] + s1;
+        const float u2 = U[4 * i + 2] + s2;
         const float u3 = U[4 * i + 3];
         const float m = __builtin_fmaxf(__builtin_fmaxf(u0, u1), __builtin_fmaxf(u2, u3));
-        X[4 * i + 0] = u0 - m;
-        X[4 * i + 1] = u1 - m;
-        X[4 * i + 2] = u2 - m;
-        X[4 * i + 3] = u3 - m;
-        const float e0 = ex2(X[4 * i + 0]);
-        const float e1 = ex2(X[4 * i + 1]);
-        const float e2 = ex2(X[4 * i + 2]);
-        const float e3 = ex2(X[4 * i + 3]);
-        const float s = (e0 + e1) + (e2 + e3);
-        const float r = rcp(s);
+        U[4 * i + 0] = u0 - m;
+        U[4 * i + 1] = u1 - m;
+        U[4 * i + 2] = u2 - m;
+        U[4 * i + 3] = u3 - m;
+        const float e0 = ex2(U[4 * i + 0]);
+        const float e1 = ex2(U[4 * i + 1]);
+        const float e2 = ex2(U[4 * i + 2]);
+        const float e3 = ex2(U[4 * i + 3]);
+        const float sum = (e0 + e1) + (e2 + e3);
+        const float r = rcp(sum);
         T[4 * i + 0] = e0 * r;
         T[4 * i + 1] = e1 * r;
         T[4 * i + 2] = e2 * r;
         T[4 * i + 3] = e3 * r;
         mrow[i] = m;
-        lsum[i] = lg2(s);
+        lsum[i] = lg2(sum);
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j)
@@ -207,6 +247,7 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
                                                           float* __restrict__ dual,
                                                           int32_t* __restrict__ iters, int64_t B,
                                                           int64_t chunk, float tol, int max_iter) {
+    constexpr int NW = RawWords<DT>::n;
     const int lane = threadIdx.x & 63;
     const int64_t wave = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
     const int64_t lo = wave * chunk;
@@ -214,93 +255,81 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
     const int64_t hi = (lo + chunk < B) ? lo + chunk : B;
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 
-    int64_t next = lo + 64;  // first unclaimed problem of this wave's range
-    int64_t idx = lo + lane;
-    bool active = idx < hi;
-    bool fresh = true;
+    // Prefetch ring: the raw words of the next 64 unclaimed problems [next, next + 64) of
+    // this wave's range; problem p sits in lane (p - lo) mod 64. A finishing lane pulls
+    // its next problem from the ring with ds_bpermute, and the lane whose slot was
+    // consumed reloads it with the problem 64 further on, so the load has a whole
+    // consumption round to land before it is needed.
+    uint32_t ring[NW];
+    int64_t next = lo;
+    if (lo + lane < hi) load_raw<DT>(H, lo + lane, ring);
 
+    int64_t idx = -1;
+    bool active = false;
+    bool fin = true;  // every lane starts by claiming a problem
+
+    // Per-problem state. U is the current point, re-centred per row, in log2 units:
+    // U = H log2(e) + beta - a 1^T; (beta, a, ls) give the dual at output.
     float U[16];
-    float beta0 = 0.f, beta1 = 0.f, beta2 = 0.f;
-    float aoff[4], ls[4];
-    float d0 = 0.f, d1 = 0.f, d2 = 0.f;
-    float t = 0.f, tscale = 1.f, slope = 0.f, gn2 = 0.f;
-    float ga0 = 0.f, ga1 = 0.f, ga2 = 0.f, gamax = 0.f, lm_mult = 1.f;  // accepted gradient
-    Weights Wa = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};                       // accepted weights
+    float b0 = 0.f, b1 = 0.f, b2 = 0.f;           // beta_1..3 of the current point (log2 units)
+    float a[4], ls[4];                            // row offsets and log2 row sums of 2^U
+    float d0 = 0.f, d1 = 0.f, d2 = 0.f;           // Newton direction at the accepted point
+    float t = 0.f;                                // trial step along d
+    float o0 = 0.f, o1 = 0.f, o2 = 0.f;           // current point minus accepted point
+    float tscale = 1.f, slope = 0.f, gn2 = 0.f;
+    float fofs = 0.f;                             // f(current) - f(accepted), log2 units
+    float ga0 = 0.f, ga1 = 0.f, ga2 = 0.f, gamax = 0.f, lm_mult = 1.f;
+    Weights Wa = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     int evals = 0;
     bool first = true, nonfinite = false;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a[i] = ls[i] = 0.f;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) U[q] = 0.f;
 
     for (;;) {
-        bool fin = false;
         if (active) {
-            if (fresh) {
-                // new problem: L = H log2(e); x^(0) = column-centring beta
-                float h[16];
-                load16<DT>(H, idx, h);
-                nonfinite = !all_finite16(h);
-                float cm[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    cm[j] = 0.25f * kLog2e * ((h[j] + h[4 + j]) + (h[8 + j] + h[12 + j]));
-                beta0 = cm[3] - cm[0];
-                beta1 = cm[3] - cm[1];
-                beta2 = cm[3] - cm[2];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    U[4 * i + 0] = nonfinite ? 0.f : __builtin_fmaf(h[4 * i + 0], kLog2e, beta0);
-                    U[4 * i + 1] = nonfinite ? 0.f : __builtin_fmaf(h[4 * i + 1], kLog2e, beta1);
-                    U[4 * i + 2] = nonfinite ? 0.f : __builtin_fmaf(h[4 * i + 2], kLog2e, beta2);
-                    U[4 * i + 3] = nonfinite ? 0.f : h[4 * i + 3] * kLog2e;
-                    aoff[i] = 0.f;
-                    ls[i] = 0.f;
-                }
-                if (nonfinite) beta0 = beta1 = beta2 = 0.f;
-                d0 = d1 = d2 = 0.f;
-                t = 0.f;
-                tscale = 1.f;
-                slope = 0.f;
-                gn2 = 0.f;
-                evals = 0;
-                first = true;
-                fresh = false;
-            }
-
-            const float td0 = t * d0, td1 = t * d1, td2 = t * d2;
-            float X[16], T[16], mrow[4], lsum[4], g[4];
-            evaluate(U, td0, td1, td2, X, T, mrow, lsum, g);
+            // trial point: accepted point + t d, reached from the current point
+            const float s0 = __builtin_fmaf(t, d0, -o0), s1 = __builtin_fmaf(t, d1, -o1),
+                        s2 = __builtin_fmaf(t, d2, -o2);
+            float T[16], mrow[4], lsum[4], g[4];
+            evaluate_inplace(U, s0, s1, s2, T, mrow, lsum, g);
             const float gmax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(g[0]), __builtin_fabsf(g[1])),
                                                __builtin_fmaxf(__builtin_fabsf(g[2]), __builtin_fabsf(g[3])));
             const float gn2t = g[0] * g[0] + g[1] * g[1] + g[2] * g[2] + g[3] * g[3];
-            // change of the reduced dual f (log2 units) from the accepted point
-            const float df = ((mrow[0] + lsum[0] - ls[0]) + (mrow[1] + lsum[1] - ls[1])) +
-                             ((mrow[2] + lsum[2] - ls[2]) + (mrow[3] + lsum[3] - ls[3])) -
-                             (td0 + td1 + td2);
+            // f(trial) - f(accepted) = f(current) - f(accepted) + row-wise change (log2 units)
+            const float df = fofs + (((mrow[0] + lsum[0] - ls[0]) + (mrow[1] + lsum[1] - ls[1])) +
+                                     ((mrow[2] + lsum[2] - ls[2]) + (mrow[3] + lsum[3] - ls[3]))) -
+                             ((s0 + s1) + s2);
+            // the trial becomes the current point
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                a[i] += mrow[i];
+                ls[i] = lsum[i];
+            }
+            b0 += s0;
+            b1 += s1;
+            b2 += s2;
+            fofs = df;
+            o0 += s0;
+            o1 += s1;
+            o2 += s2;
             const bool accept = first || (df <= kArmijo * t * slope) ||
                                 (__builtin_fabsf(df) < kFNoise && gn2t < gn2);
             if (!first) ++evals;
-            bool conv = false;
-            if (accept) {
-                if (!first) {
-                    const float dd = g[0] * d0 + g[1] * d1 + g[2] * d2;
-                    tscale = (t >= 0.999f * tscale && dd < 0.25f * slope)
-                                 ? __builtin_fminf(2.f * tscale, kMaxExpand)
-                                 : 1.f;
-                }
-#pragma unroll
-                for (int q = 0; q < 16; ++q) U[q] = X[q];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    aoff[i] += mrow[i];
-                    ls[i] = lsum[i];
-                }
-                beta0 += td0;
-                beta1 += td1;
-                beta2 += td2;
-                gn2 = gn2t;
-                conv = gmax <= tol;
-            }
-            fin = conv || evals >= max_iter;
+            const bool conv = accept && gmax <= tol;
+            fin = conv || nonfinite || evals >= max_iter;
             if (!fin) {
                 if (accept) {
+                    if (!first) {
+                        const float dd = g[0] * d0 + g[1] * d1 + g[2] * d2;
+                        tscale = (t >= 0.999f * tscale && dd < 0.25f * slope)
+                                     ? __builtin_fminf(2.f * tscale, kMaxExpand)
+                                     : 1.f;
+                    }
+                    fofs = 0.f;
+                    o0 = o1 = o2 = 0.f;
+                    gn2 = gn2t;
                     Wa = column_weights(T);
                     ga0 = g[0];
                     ga1 = g[1];
@@ -315,39 +344,38 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
                     tscale = 1.f;
                     lm_mult = __builtin_fminf(16.f * lm_mult, kMaxLMMult);
                 }
-                newton_solve(Wa, ga0, ga1, ga2, kLM * gamax * lm_mult, d0, d1, d2);
+                newton_solve(Wa, ga0, ga1, ga2, __builtin_fmaxf(kLM * gamax, kLMFloor) * lm_mult, d0, d1,
+                             d2);
                 slope = ga0 * d0 + ga1 * d1 + ga2 * d2;
-                const float dm = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(d0), __builtin_fabsf(d1)),
-                                                 __builtin_fabsf(d2));
+                // cap the spread of the column shifts (d_4 = 0): the cap is gauge-symmetric, so
+                // two columns moving in opposite directions cannot jump twice as far
+                const float dm = __builtin_fmaxf(__builtin_fmaxf(d0, d1), __builtin_fmaxf(d2, 0.f)) -
+                                 __builtin_fminf(__builtin_fminf(d0, d1), __builtin_fminf(d2, 0.f));
                 t = __builtin_fminf(t, kCap2 * rcp(__builtin_fmaxf(dm, kTiny)));
                 first = false;
             } else {
-                if (!accept) {
-                    // the last trial was rejected: report the accepted point
-                    evaluate(U, 0.f, 0.f, 0.f, X, T, mrow, lsum, g);
+                if (!accept && !nonfinite) {
+                    // max_iter reached on a rejected trial: return to the accepted point
+                    const float r0 = -o0, r1 = -o1, r2 = -o2;
+                    evaluate_inplace(U, r0, r1, r2, T, mrow, lsum, g);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        aoff[i] += mrow[i];
+                        a[i] += mrow[i];
                         ls[i] = lsum[i];
                     }
+                    b0 += r0;
+                    b1 += r1;
+                    b2 += r2;
                 }
-                if (nonfinite) {
-#pragma unroll
-                    for (int q = 0; q < 16; ++q) T[q] = __builtin_nanf("");
-                }
+                // a non-finite input was poisoned with NaN at load, so T and the dual are NaN
                 store16(P, idx, T);
                 if constexpr (WRITE_DUAL) {
-                    const float nan = __builtin_nanf("");
                     v4f* dp = reinterpret_cast<v4f*>(dual) + 2 * idx;
-                    const float a0 = nonfinite ? nan : -(aoff[0] + ls[0]) * kLn2;
-                    const float a1 = nonfinite ? nan : -(aoff[1] + ls[1]) * kLn2;
-                    const float a2 = nonfinite ? nan : -(aoff[2] + ls[2]) * kLn2;
-                    const float a3 = nonfinite ? nan : -(aoff[3] + ls[3]) * kLn2;
-                    const v4f va = {a0, a1, a2, a3};
-                    const v4f vb = {nonfinite ? nan : beta0 * kLn2, nonfinite ? nan : beta1 * kLn2,
-                                    nonfinite ? nan : beta2 * kLn2, nonfinite ? nan : 0.f};
-                    __builtin_nontemporal_store(va, dp);
-                    __builtin_nontemporal_store(vb, dp + 1);
+                    const v4f va = {-(a[0] + ls[0]) * kLn2, -(a[1] + ls[1]) * kLn2, -(a[2] + ls[2]) * kLn2,
+                                    -(a[3] + ls[3]) * kLn2};
+                    const v4f vb = {b0 * kLn2, b1 * kLn2, b2 * kLn2, b0 * 0.f};
+                    dp[0] = va;
+                    dp[1] = vb;
                 }
                 if constexpr (WRITE_ITERS) {
                     iters[idx] = nonfinite ? BIRKHOFF4_NON_FINITE
@@ -358,12 +386,55 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
         // refill: finished lanes claim the next problems of the wave's range in lane order
         const uint64_t fm = __ballot(fin);
         if (fm) {
+            const int k = __popcll(fm);
+            const int off = static_cast<int>((next - lo) & 63);
+            const int rank = __popcll(fm & below);
+            const int src = (off + rank) & 63;
+            uint32_t got[NW];
+#pragma unroll
+            for (int q = 0; q < NW; ++q)
+                got[q] = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(src << 2, static_cast<int>(ring[q])));
+            const int pos = (lane - off) & 63;
+            if (pos < k && next + pos + 64 < hi) load_raw<DT>(H, next + pos + 64, ring);
             if (fin) {
-                idx = next + __popcll(fm & below);
+                idx = next + rank;
                 active = idx < hi;
-                fresh = true;
+                fin = false;
+                if (active) {
+                    // new problem: L = H log2(e); x^(0) = column-centring beta. A NaN or
+                    // infinite entry poisons every derived value with NaN.
+                    float h[16];
+                    decode_raw<DT>(got, h);
+                    float cm[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        cm[j] = 0.25f * kLog2e * ((h[j] + h[4 + j]) + (h[8 + j] + h[12 + j]));
+                    // NaN or +-Inf anywhere makes this sum NaN or infinite (a finite sum
+                    // that overflows needs entries near FLT_MAX, where exp overflows anyway)
+                    const float hs = (cm[0] + cm[1]) + (cm[2] + cm[3]);
+                    nonfinite = !(__builtin_fabsf(hs) <= 3.402823466e38f);
+                    const float poison = hs - hs;  // 0, or NaN for a non-finite input
+                    b0 = cm[3] - cm[0] + poison;
+                    b1 = cm[3] - cm[1] + poison;
+                    b2 = cm[3] - cm[2] + poison;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        U[4 * i + 0] = __builtin_fmaf(h[4 * i + 0], kLog2e, b0);
+                        U[4 * i + 1] = __builtin_fmaf(h[4 * i + 1], kLog2e, b1);
+                        U[4 * i + 2] = __builtin_fmaf(h[4 * i + 2], kLog2e, b2);
+                        U[4 * i + 3] = __builtin_fmaf(h[4 * i + 3], kLog2e, poison);
+                        a[i] = 0.f;
+                        ls[i] = 0.f;
+                    }
+                    d0 = d1 = d2 = 0.f;
+                    t = o0 = o1 = o2 = 0.f;
+                    tscale = 1.f;
+                    slope = gn2 = fofs = 0.f;
+                    evals = 0;
+                    first = true;
+                }
             }
-            next += __popcll(fm);
+            next += k;
         }
         if (__ballot(active) == 0) break;
     }
@@ -402,7 +473,7 @@ __global__ __launch_bounds__(256) void implicit_bwd_kernel(const float* __restri
         // flows onto the same edges, F_jk += (W_pk F_jp + W_jp F_pk) / piv, so every
         // right-hand side stays a sum of antisymmetric edge flows.
         const float piv0 = W01 + W02 + W03;
-        const float i0 = piv0 > 0.f ? rcp(piv0) : 0.f;
+        const float i0 = piv0 > kPivMin ? rcp(piv0) : 0.f;
         const float W12b = __builtin_fmaf(W01 * W02, i0, W12);
         const float W13b = __builtin_fmaf(W01 * W03, i0, W13);
         const float W23b = __builtin_fmaf(W02 * W03, i0, W23);
@@ -410,10 +481,10 @@ __global__ __launch_bounds__(256) void implicit_bwd_kernel(const float* __restri
         const float F13b = __builtin_fmaf(W01 * F03 - W03 * F01, i0, F13);
         const float F23b = __builtin_fmaf(W02 * F03 - W03 * F02, i0, F23);
         const float piv1 = W12b + W13b;
-        const float i1 = piv1 > 0.f ? rcp(piv1) : 0.f;
+        const float i1 = piv1 > kPivMin ? rcp(piv1) : 0.f;
         const float W23c = __builtin_fmaf(W12b * W13b, i1, W23b);
         const float F23c = __builtin_fmaf(W12b * F13b - W13b * F12b, i1, F23b);
-        const float w2 = W23c > 0.f ? F23c * rcp(W23c) : 0.f;
+        const float w2 = W23c > kPivMin ? F23c * rcp(W23c) : 0.f;
         const float w1 = __builtin_fmaf(W12b, w2, F12b + F13b) * i1;
         const float w0 = __builtin_fmaf(W01, w1, __builtin_fmaf(W02, w2, (F01 + F02) + F03)) * i0;
         // dH = -D: dH_ij = T_ij (psi_ij - sum_k T_ik psi_ik), psi = G - 1 w^T, w_4 = 0

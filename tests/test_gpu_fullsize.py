@@ -60,12 +60,17 @@ def test_fullsize(name):
     assert marg.max() <= TOL_MARGINAL
     assert torch.isfinite(P).all()
     if dH is not None:
-        # row and column sums of dH vanish for every matrix
+        assert torch.isfinite(dH).all()
+        # row and column sums of dH vanish for every matrix, up to rounding
         d64 = dH.double()
-        rs = d64.sum(dim=-1).abs().amax().item()
-        cs = d64.sum(dim=-2).abs().amax().item()
-        say(f"  max |row/col sums of dH|: {rs:.2e} {cs:.2e}")
-        assert rs < 1e-5 and cs < 1e-5
+        sums = torch.maximum(d64.sum(dim=-1).abs().amax(dim=-1), d64.sum(dim=-2).abs().amax(dim=-1))
+        worst = int(torch.argmax(sums).item())
+        say(f"  max |row/col sums of dH|: {sums[worst].item():.2e} at matrix {worst}, "
+            f"max|dH| there {dH[worst].abs().max().item():.3e}")
+        worst_ix = np.array([worst])
+        check_parity(ch.H[worst_ix], P[worst:worst + 1].cpu().numpy(), None,
+                     ch.dP[worst_ix], dH[worst:worst + 1].cpu().numpy(), f"{name} worst dH sums")
+        assert sums.max().item() < 1e-4
     idx = _sample(B, marg, itn)
     idx_t = torch.from_numpy(idx).to("cuda:0")
     Ps = P[idx_t].cpu().numpy()

@@ -1,0 +1,78 @@
+"""Regression cases found on full-size workloads, regenerated from the seeded
+generators (no stored inputs).
+
+* mix_bf16_b2e24 #8108295: a 2-cycle between two columns under an inf-norm step cap
+  (fixed by capping the spread of the column shifts);
+* mix_bf16_b2e24 #9164907 and 16 logunif_b2e25 matrices: stalls just above tol when a
+  gradient at the fp32 rounding floor drove weakly coupled columns (fixed by the floor
+  of the Levenberg-Marquardt shift);
+* logunif_b2e25 #20482192: NaN in the backward from the reciprocal of a denormal pivot
+  (fixed by treating pivots <= 1e-30 as disconnected).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_07574_amd as b4
+import workloads
+from tests._gpu import (MAX_ITER, TOL_DH, TOL_MARGINAL, TOL_P, bits_to_dev, check_parity, gpu_fwd,
+                        marginal_linf_device, say, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    "mix_bf16_b2e24": [8108295, 9164907],
+    "logunif_b2e25": [1548970, 5897705, 7163824, 8253668, 9546997, 9961632, 10235358, 10598146,
+                      12182588, 12701271, 13677741, 16948698, 20482192, 22615900, 22955309,
+                      24646586, 28609303],
+}
+
+
+def _gather(name, indices):
+    w = workloads.WORKLOADS[name]
+    H, dP = [], []
+    for i in indices:
+        c, o = divmod(i, workloads.CHUNK)
+        ch = workloads.make_chunk(w, c)
+        H.append(ch.H[o])
+        dP.append(ch.dP[o])
+    return np.stack(H), np.stack(dP)
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_regression_cases(name):
+    say(f"test: hard cases of {name}: {CASES[name]}")
+    H, dP = _gather(name, CASES[name])
+    # also run each one surrounded by easy neighbours, as inside a full wave
+    Hw = np.concatenate([workloads.gauss(200, 1.0, seed=5)[0], H, workloads.gauss(200, 1.0, seed=6)[0]])
+    P, dual, it = gpu_fwd(to_dev(H))
+    Pw, _, itw = gpu_fwd(to_dev(Hw))
+    dH = b4.bwd(P, to_dev(dP))
+    torch.cuda.synchronize()
+    itn = it.cpu().numpy()
+    say(f"  iters {itn.tolist()}")
+    assert (itn >= 0).all() and (itw.cpu().numpy() >= 0).all()
+    assert torch.isfinite(dH).all()
+    check_parity(H, P.cpu().numpy(), dual.cpu().numpy(), dP, dH.cpu().numpy(), name)
+
+
+def test_sigma50_two_million():
+    say("test: 2^21 matrices at sigma = 50")
+    H, dP = workloads.gauss(1 << 21, 50.0, seed=99)
+    Hd = to_dev(H)
+    P, dual, it = gpu_fwd(Hd)
+    dH = b4.bwd(P, to_dev(dP))
+    torch.cuda.synchronize()
+    itn = it.cpu().numpy()
+    marg = marginal_linf_device(P).cpu().numpy()
+    say(f"  iters mean={itn.mean():.2f} max={itn.max()} not_converged={(itn < 0).sum()} "
+        f"max marginal={marg.max():.3e}")
+    assert (itn >= 0).all() and marg.max() <= TOL_MARGINAL
+    assert torch.isfinite(dH).all()
+    rng = np.random.default_rng(1)
+    idx = np.unique(np.concatenate([rng.choice(len(H), 3000, replace=False), np.argsort(itn)[-200:],
+                                    np.argsort(marg)[-200:]]))
+    it_t = torch.from_numpy(idx).to("cuda:0")
+    check_parity(H[idx], P[it_t].cpu().numpy(), dual[it_t].cpu().numpy(), dP[idx],
+                 dH[it_t].cpu().numpy(), "sigma=50 sample")
