@@ -249,7 +249,9 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
                                                           int64_t chunk, float tol, int max_iter) {
     constexpr int NW = RawWords<DT>::n;
     const int lane = threadIdx.x & 63;
-    const int64_t wave = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
+    // the wave index is uniform across the wave: keep the range bookkeeping in SGPRs
+    const int64_t wave = static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) +
+                         __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
     const int64_t lo = wave * chunk;
     if (lo >= B) return;  // uniform across the wave
     const int64_t hi = (lo + chunk < B) ? lo + chunk : B;
