@@ -7,10 +7,10 @@
 // (eq. sinkhorn_knopp) and its reverse-mode gradient.
 //
 // Mapping: one 4x4 problem per lane; all per-problem state lives in VGPRs. No
-// MFMA (the only products are six 4-long dot products per matrix), no LDS in
-// the Newton and implicit kernels, no atomics. Loads and stores are plain 16-byte
-// vector accesses (non-temporal hints measured slower on gfx950: the stores
-// lose write combining).
+// MFMA (the only products are six 4-long dot products per matrix), no atomics.
+// Loads and stores are plain 16-byte vector accesses (non-temporal hints
+// measured slower on gfx950: the stores lose write combining). The implicit
+// kernel uses no LDS; the Newton kernel uses LDS only to stage its outputs.
 //
 // Forward numerics (fp32, log2 domain so that v_exp_f32 applies directly):
 //  * state is U = H*log2(e) + beta - a 1^T with every row re-centred to max 0
@@ -38,6 +38,11 @@
 // Newton steps, not the maximum over its 64 lanes. The next 64 problems of the
 // range are prefetched into a register ring spread over the wave's lanes and
 // handed to finishing lanes with ds_bpermute, so a refill never waits on HBM.
+// Finished outputs are staged in a per-wave LDS ring and written 16 problems
+// at a time by the whole wave (4 lanes per 64-byte P block, 2 per dual), so a
+// store instruction writes whole 64-byte pieces instead of one 16-byte piece
+// per finishing lane; the flush is issued after the ring loads, so the wait that
+// the next refill needs never covers stores issued in the same iteration.
 
 #include <hip/hip_runtime.h>
 
@@ -69,6 +74,10 @@ constexpr float kPivMin = 1e-30f;
 constexpr float kFltMin = 1.17549435e-38f;
 constexpr int kMaxSkSteps = 48;   // sk_bwd keeps (n+1) x 4 floats per lane in LDS
 constexpr int kMaxIterCap = 10000;
+constexpr int kFwdBlock = 256;
+constexpr int kFwdWaves = kFwdBlock / 64;
+// Per-wave ring of finished outputs: at most 15 left after a flush plus 64 new ones.
+constexpr int kStageCap = 80;
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
@@ -250,8 +259,14 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
     constexpr int NW = RawWords<DT>::n;
     const int lane = threadIdx.x & 63;
     // the wave index is uniform across the wave: keep the range bookkeeping in SGPRs
-    const int64_t wave = static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) +
-                         __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+    const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+    const int64_t wave = static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + wv;
+    constexpr int SC = kStageCap, SD = WRITE_DUAL ? kStageCap : 1, SI = WRITE_ITERS ? kStageCap : 1;
+    __shared__ v4f sP[kFwdWaves][4 * SC];
+    __shared__ v4f sD[kFwdWaves][2 * SD];
+    __shared__ int32_t sIdx[kFwdWaves][SC];  // problem index - lo
+    __shared__ int32_t sIt[kFwdWaves][SI];
+    int head = 0, count = 0;  // staged outputs: slots head .. head + count - 1 (mod SC)
     const int64_t lo = wave * chunk;
     if (lo >= B) return;  // uniform across the wave
     const int64_t hi = (lo + chunk < B) ? lo + chunk : B;
@@ -289,7 +304,44 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
 #pragma unroll
     for (int q = 0; q < 16; ++q) U[q] = 0.f;
 
+    // Write out n <= 16 staged outputs from slot head on: 4 lanes per P (one 64-byte
+    // row block each), 2 per dual, 1 per iteration count, so every store instruction
+    // writes whole 64-byte pieces of up to 16 problems.
+    auto flush = [&](int n) {
+        __builtin_amdgcn_wave_barrier();
+        {
+            int e = lane >> 2;
+            if (e < n) {
+                e += head;
+                if (e >= SC) e -= SC;
+                const v4f v = sP[wv][4 * e + (lane & 3)];
+                reinterpret_cast<v4f*>(P)[4 * (lo + sIdx[wv][e]) + (lane & 3)] = v;
+            }
+        }
+        if constexpr (WRITE_DUAL) {
+            int e = lane >> 1;
+            if (e < n) {
+                e += head;
+                if (e >= SC) e -= SC;
+                const v4f v = sD[wv][2 * e + (lane & 1)];
+                reinterpret_cast<v4f*>(dual)[2 * (lo + sIdx[wv][e]) + (lane & 1)] = v;
+            }
+        }
+        if constexpr (WRITE_ITERS) {
+            if (lane < n) {
+                int e = head + lane;
+                if (e >= SC) e -= SC;
+                iters[lo + sIdx[wv][e]] = sIt[wv][e];
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        head += n;
+        if (head >= SC) head -= SC;
+        count -= n;
+    };
+
     for (;;) {
+        bool staged = false;
         if (active) {
             // trial point: accepted point + t d, reached from the current point
             const float s0 = __builtin_fmaf(t, d0, -o0), s1 = __builtin_fmaf(t, d1, -o1),
@@ -369,20 +421,26 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
                     b1 += r1;
                     b2 += r2;
                 }
-                // a non-finite input was poisoned with NaN at load, so T and the dual are NaN
-                store16(P, idx, T);
+                // a non-finite input was poisoned with NaN at load, so T and the dual are NaN.
+                // Stage the outputs in this wave's LDS ring, in lane order after the
+                // outputs already staged.
+                int slot = head + count + __popcll(__ballot(1) & below);
+                if (slot >= SC) slot -= SC;
+                sP[wv][4 * slot + 0] = v4f{T[0], T[1], T[2], T[3]};
+                sP[wv][4 * slot + 1] = v4f{T[4], T[5], T[6], T[7]};
+                sP[wv][4 * slot + 2] = v4f{T[8], T[9], T[10], T[11]};
+                sP[wv][4 * slot + 3] = v4f{T[12], T[13], T[14], T[15]};
+                sIdx[wv][slot] = static_cast<int32_t>(idx - lo);
                 if constexpr (WRITE_DUAL) {
-                    v4f* dp = reinterpret_cast<v4f*>(dual) + 2 * idx;
-                    const v4f va = {-(a[0] + ls[0]) * kLn2, -(a[1] + ls[1]) * kLn2, -(a[2] + ls[2]) * kLn2,
-                                    -(a[3] + ls[3]) * kLn2};
-                    const v4f vb = {b0 * kLn2, b1 * kLn2, b2 * kLn2, b0 * 0.f};
-                    dp[0] = va;
-                    dp[1] = vb;
+                    sD[wv][2 * slot] = v4f{-(a[0] + ls[0]) * kLn2, -(a[1] + ls[1]) * kLn2,
+                                           -(a[2] + ls[2]) * kLn2, -(a[3] + ls[3]) * kLn2};
+                    sD[wv][2 * slot + 1] = v4f{b0 * kLn2, b1 * kLn2, b2 * kLn2, b0 * 0.f};
                 }
                 if constexpr (WRITE_ITERS) {
-                    iters[idx] = nonfinite ? BIRKHOFF4_NON_FINITE
-                                           : (conv ? evals : BIRKHOFF4_NOT_CONVERGED);
+                    sIt[wv][slot] = nonfinite ? BIRKHOFF4_NON_FINITE
+                                              : (conv ? evals : BIRKHOFF4_NOT_CONVERGED);
                 }
+                staged = true;
             }
         }
         // refill: finished lanes claim the next problems of the wave's range in lane order
@@ -438,7 +496,14 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
             }
             next += k;
         }
-        if (__ballot(active) == 0) break;
+        // outputs staged this iteration are written after the ring loads are issued, so
+        // the wait of the next refill covers stores one iteration old
+        count += __popcll(__ballot(staged));
+        while (count >= 16) flush(16);
+        if (__ballot(active) == 0) {
+            if (count > 0) flush(count);
+            break;
+        }
     }
 }
 
@@ -676,8 +741,6 @@ int launch_status() {
     return hipGetLastError() == hipSuccess ? BIRKHOFF4_OK : BIRKHOFF4_ERR_LAUNCH;
 }
 
-constexpr int kFwdBlock = 256;
-
 // Blocks of the forward kernel resident at once on one CU (VGPR-limited),
 // from the occupancy calculator; queried once per instantiation.
 template <int DT, bool WD, bool WI>
@@ -702,6 +765,7 @@ int launch_fwd(const void* H, float* P, float* dual, int32_t* iters, int64_t B, 
     int64_t waves = static_cast<int64_t>(cus) * fwd_blocks_per_cu<DT, WD, WI>() * (kFwdBlock / 64);
     if (waves > waves_needed) waves = waves_needed;
     const int64_t chunk = (B + waves - 1) / waves;
+    if (chunk > INT32_MAX) return BIRKHOFF4_ERR_SIZE;  // staged outputs keep 32-bit offsets
     waves = (B + chunk - 1) / chunk;
     const int64_t blocks = (waves * 64 + kFwdBlock - 1) / kFwdBlock;
     hipLaunchKernelGGL((newton_fwd_kernel<DT, WD, WI>), dim3(static_cast<unsigned>(blocks)),
