@@ -64,8 +64,8 @@ constexpr float kLM = 1e-3f;            // Levenberg-Marquardt coefficient
 constexpr float kLMFloor = 5e-8f;
 constexpr float kArmijo = 1e-4f;
 constexpr float kFNoise = 4e-6f;        // |delta f| below this is rounding noise
-constexpr float kMaxExpand = 16.0f;
-constexpr float kMaxLMMult = 1e20f;     // keeps the shift finite (|g| <= 4)
+constexpr int kMaxExpandLog2 = 4;      // initial trial step <= 16
+constexpr float kMaxShift = 1e18f;      // keeps the escalated shift finite
 constexpr float kTiny = 1e-30f;
 // Backward pivots at or below this are treated as disconnected nodes (potential 0):
 // v_rcp_f32 of a denormal is infinite, and such a node's entries of dH carry
@@ -171,34 +171,35 @@ __device__ __forceinline__ void store16(float* base, int64_t b, const float v[16
 // ---------------------------------------------------------------------------
 
 // Row-softmax evaluation at the trial point U + s (log2 units, s_4 = 0), eq. tij_stable.
-// U is replaced by the trial re-centred per row (the new current point); T = the row
-// softmax; mrow = row maxima removed; lsum = log2 of the row sums of 2^U; g = column
-// sums - 1 (eq. c_g, all four columns).
+// Every row of U has log-sum-exp 0 (U = log2 of the current T), and each column shift
+// of a trial is bounded by the step cap, so 2^(U + s) needs no max subtraction: it
+// neither overflows nor loses a row's dominant entry. U is replaced by the trial
+// re-normalised per row (the new current point); T = the row softmax; lsum = log2 of
+// the row sums of 2^(U + s); g = column sums - 1 (eq. c_g, all four columns).
 __device__ __forceinline__ void evaluate_inplace(float U[16], float s0, float s1, float s2, float T[16],
-                                                 float mrow[4], float lsum[4], float g[4]) {
+                                                 float lsum[4], float g[4]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const float u0 = U[4 * i + 0] + s0;
         const float u1 = U[4 * i + 1] + s1;
         const float u2 = U[4 * i + 2] + s2;
         const float u3 = U[4 * i + 3];
-        const float m = __builtin_fmaxf(__builtin_fmaxf(u0, u1), __builtin_fmaxf(u2, u3));
-        U[4 * i + 0] = u0 - m;
-        U[4 * i + 1] = u1 - m;
-        U[4 * i + 2] = u2 - m;
-        U[4 * i + 3] = u3 - m;
-        const float e0 = ex2(U[4 * i + 0]);
-        const float e1 = ex2(U[4 * i + 1]);
-        const float e2 = ex2(U[4 * i + 2]);
-        const float e3 = ex2(U[4 * i + 3]);
+        const float e0 = ex2(u0);
+        const float e1 = ex2(u1);
+        const float e2 = ex2(u2);
+        const float e3 = ex2(u3);
         const float sum = (e0 + e1) + (e2 + e3);
         const float r = rcp(sum);
+        const float l = lg2(sum);
         T[4 * i + 0] = e0 * r;
         T[4 * i + 1] = e1 * r;
         T[4 * i + 2] = e2 * r;
         T[4 * i + 3] = e3 * r;
-        mrow[i] = m;
-        lsum[i] = lg2(sum);
+        U[4 * i + 0] = u0 - l;
+        U[4 * i + 1] = u1 - l;
+        U[4 * i + 2] = u2 - l;
+        U[4 * i + 3] = u3 - l;
+        lsum[i] = l;
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j)
@@ -250,6 +251,39 @@ __device__ __forceinline__ void newton_solve(const Weights& W, float g0, float g
     d0 = __builtin_fmaf(W.w01, d1, __builtin_fmaf(W.w02, d2, r0)) * i0;
 }
 
+// Initial state of one problem from its raw words: x^(0) = column-centring beta
+// (beta_j = mean_i H_i4 - mean_i H_ij), U = H log2(e) + beta - a 1^T with a = the row
+// maxima, so every row of U starts at max 0. A NaN or infinite entry makes the column
+// mean sum NaN or infinite and poisons U, a and beta with NaN (a finite sum that
+// overflows needs entries near FLT_MAX, where exp overflows anyway).
+template <int DT>
+__device__ __forceinline__ void init_problem(const uint32_t w[RawWords<DT>::n], float U[16], float a[4],
+                                             float& b0, float& b1, float& b2) {
+    float h[16];
+    decode_raw<DT>(w, h);
+    float cm[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cm[j] = 0.25f * kLog2e * ((h[j] + h[4 + j]) + (h[8 + j] + h[12 + j]));
+    const float hs = (cm[0] + cm[1]) + (cm[2] + cm[3]);
+    const float poison = hs - hs;  // 0, or NaN for a non-finite input
+    b0 = cm[3] - cm[0] + poison;
+    b1 = cm[3] - cm[1] + poison;
+    b2 = cm[3] - cm[2] + poison;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float u0 = __builtin_fmaf(h[4 * i + 0], kLog2e, b0);
+        const float u1 = __builtin_fmaf(h[4 * i + 1], kLog2e, b1);
+        const float u2 = __builtin_fmaf(h[4 * i + 2], kLog2e, b2);
+        const float u3 = __builtin_fmaf(h[4 * i + 3], kLog2e, poison);
+        const float m = __builtin_fmaxf(__builtin_fmaxf(u0, u1), __builtin_fmaxf(u2, u3)) + poison;
+        U[4 * i + 0] = u0 - m;
+        U[4 * i + 1] = u1 - m;
+        U[4 * i + 2] = u2 - m;
+        U[4 * i + 3] = u3 - m;
+        a[i] = m;
+    }
+}
+
 template <int DT, bool WRITE_DUAL, bool WRITE_ITERS>
 __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict__ H,
                                                           float* __restrict__ P,
@@ -272,35 +306,42 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
     const int64_t hi = (lo + chunk < B) ? lo + chunk : B;
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 
-    // Prefetch ring: the raw words of the next 64 unclaimed problems [next, next + 64) of
-    // this wave's range; problem p sits in lane (p - lo) mod 64. A finishing lane pulls
-    // its next problem from the ring with ds_bpermute, and the lane whose slot was
-    // consumed reloads it with the problem 64 further on, so the load has a whole
-    // consumption round to land before it is needed.
-    uint32_t ring[NW];
-    int64_t next = lo;
-    if (lo + lane < hi) load_raw<DT>(H, lo + lane, ring);
-
-    int64_t idx = -1;
+    const int32_t nrel = static_cast<int32_t>(hi - lo);
+    // Problem supply: the range is taken in batches of 64 consecutive problems, one per
+    // lane. The raw words of the next batch are loaded one batch ahead with whole-wave
+    // loads; when the current batch runs out the whole wave initialises the next one at
+    // once (full EXEC), and finishing lanes take initialised problems with ds_bpermute.
+    uint32_t raw[NW];
+#pragma unroll
+    for (int q = 0; q < NW; ++q) raw[q] = 0u;
+    if (lane < nrel) load_raw<DT>(H, lo + lane, raw);
+    float iU[16], ia[4], ib0, ib1, ib2;  // initial state of problem ibase + lane
+    init_problem<DT>(raw, iU, ia, ib0, ib1, ib2);
+    if (64 + lane < nrel) load_raw<DT>(H, lo + 64 + lane, raw);
+    int32_t ibase = 0;  // first problem of the initialised batch (offset from lo)
+    int icur = 0;       // problems of that batch already taken
+    int32_t rel = -1;  // this lane's problem, as an offset from lo
     bool active = false;
     bool fin = true;  // every lane starts by claiming a problem
 
-    // Per-problem state. U is the current point, re-centred per row, in log2 units:
-    // U = H log2(e) + beta - a 1^T; (beta, a, ls) give the dual at output.
+    // Per-problem state. U is the current point, normalised per row, in log2 units:
+    // U = H log2(e) + beta - a 1^T = log2 T; (beta, a) give the dual at output.
     float U[16];
     float b0 = 0.f, b1 = 0.f, b2 = 0.f;           // beta_1..3 of the current point (log2 units)
-    float a[4], ls[4];                            // row offsets and log2 row sums of 2^U
+    float a[4];                                   // row log-sum-exp of H log2(e) + beta
     float d0 = 0.f, d1 = 0.f, d2 = 0.f;           // Newton direction at the accepted point
     float t = 0.f;                                // trial step along d
     float o0 = 0.f, o1 = 0.f, o2 = 0.f;           // current point minus accepted point
-    float tscale = 1.f, slope = 0.f, gn2 = 0.f;
+    float gn2 = 0.f;
     float fofs = 0.f;                             // f(current) - f(accepted), log2 units
-    float ga0 = 0.f, ga1 = 0.f, ga2 = 0.f, gamax = 0.f, lm_mult = 1.f;
+    float ga0 = 0.f, ga1 = 0.f, ga2 = 0.f;       // gradient at the accepted point
+    float lam = 0.f;                              // Levenberg-Marquardt shift
     Weights Wa = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    int evals = 0;
+    // bits 0-15: trial steps taken; bits 16-18: log2 of the initial trial step
+    int cnt = 0;
     bool first = true, nonfinite = false;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = ls[i] = 0.f;
+    for (int i = 0; i < 4; ++i) a[i] = 0.f;
 #pragma unroll
     for (int q = 0; q < 16; ++q) U[q] = 0.f;
 
@@ -346,20 +387,18 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
             // trial point: accepted point + t d, reached from the current point
             const float s0 = __builtin_fmaf(t, d0, -o0), s1 = __builtin_fmaf(t, d1, -o1),
                         s2 = __builtin_fmaf(t, d2, -o2);
-            float T[16], mrow[4], lsum[4], g[4];
-            evaluate_inplace(U, s0, s1, s2, T, mrow, lsum, g);
+            float T[16], lsum[4], g[4];
+            evaluate_inplace(U, s0, s1, s2, T, lsum, g);
             const float gmax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(g[0]), __builtin_fabsf(g[1])),
                                                __builtin_fmaxf(__builtin_fabsf(g[2]), __builtin_fabsf(g[3])));
             const float gn2t = g[0] * g[0] + g[1] * g[1] + g[2] * g[2] + g[3] * g[3];
             // f(trial) - f(accepted) = f(current) - f(accepted) + row-wise change (log2 units)
-            const float df = fofs + (((mrow[0] + lsum[0] - ls[0]) + (mrow[1] + lsum[1] - ls[1])) +
-                                     ((mrow[2] + lsum[2] - ls[2]) + (mrow[3] + lsum[3] - ls[3]))) -
+            const float df = fofs + ((lsum[0] + lsum[1]) + (lsum[2] + lsum[3])) -
                              ((s0 + s1) + s2);
             // the trial becomes the current point
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                a[i] += mrow[i];
-                ls[i] = lsum[i];
+                a[i] += lsum[i];
             }
             b0 += s0;
             b1 += s1;
@@ -368,18 +407,21 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
             o0 += s0;
             o1 += s1;
             o2 += s2;
+            // directional derivative of f along d at the accepted point (log2 units)
+            const float slope = ga0 * d0 + ga1 * d1 + ga2 * d2;
             const bool accept = first || (df <= kArmijo * t * slope) ||
                                 (__builtin_fabsf(df) < kFNoise && gn2t < gn2);
-            if (!first) ++evals;
+            if (!first) ++cnt;
+            const int evals = cnt & 0xffff;
             const bool conv = accept && gmax <= tol;
             fin = conv || nonfinite || evals >= max_iter;
             if (!fin) {
                 if (accept) {
                     if (!first) {
                         const float dd = g[0] * d0 + g[1] * d1 + g[2] * d2;
-                        tscale = (t >= 0.999f * tscale && dd < 0.25f * slope)
-                                     ? __builtin_fminf(2.f * tscale, kMaxExpand)
-                                     : 1.f;
+                        const int ts = cnt >> 16;  // the trial step doubles while full steps
+                        const bool grow = t >= 0.999f * __builtin_ldexpf(1.f, ts) && dd < 0.25f * slope;
+                        cnt = evals | ((grow ? (ts < kMaxExpandLog2 ? ts + 1 : ts) : 0) << 16);
                     }
                     fofs = 0.f;
                     o0 = o1 = o2 = 0.f;
@@ -388,19 +430,16 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
                     ga0 = g[0];
                     ga1 = g[1];
                     ga2 = g[2];
-                    gamax = gmax;
-                    lm_mult = 1.f;
-                    t = tscale;
+                    lam = __builtin_fmaxf(kLM * gmax, kLMFloor);
+                    t = __builtin_ldexpf(1.f, cnt >> 16);
                 } else {
                     // backtrack: halve the step and raise the Levenberg-Marquardt shift, so a
                     // direction spoiled by rounding in weakly coupled modes is replaced
                     t *= 0.5f;
-                    tscale = 1.f;
-                    lm_mult = __builtin_fminf(16.f * lm_mult, kMaxLMMult);
+                    cnt = evals;
+                    lam = __builtin_fminf(16.f * lam, kMaxShift);
                 }
-                newton_solve(Wa, ga0, ga1, ga2, __builtin_fmaxf(kLM * gamax, kLMFloor) * lm_mult, d0, d1,
-                             d2);
-                slope = ga0 * d0 + ga1 * d1 + ga2 * d2;
+                newton_solve(Wa, ga0, ga1, ga2, lam, d0, d1, d2);
                 // cap the spread of the column shifts (d_4 = 0): the cap is gauge-symmetric, so
                 // two columns moving in opposite directions cannot jump twice as far
                 const float dm = __builtin_fmaxf(__builtin_fmaxf(d0, d1), __builtin_fmaxf(d2, 0.f)) -
@@ -411,11 +450,10 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
                 if (!accept && !nonfinite) {
                     // max_iter reached on a rejected trial: return to the accepted point
                     const float r0 = -o0, r1 = -o1, r2 = -o2;
-                    evaluate_inplace(U, r0, r1, r2, T, mrow, lsum, g);
+                    evaluate_inplace(U, r0, r1, r2, T, lsum, g);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        a[i] += mrow[i];
-                        ls[i] = lsum[i];
+                        a[i] += lsum[i];
                     }
                     b0 += r0;
                     b1 += r1;
@@ -430,10 +468,9 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
                 sP[wv][4 * slot + 1] = v4f{T[4], T[5], T[6], T[7]};
                 sP[wv][4 * slot + 2] = v4f{T[8], T[9], T[10], T[11]};
                 sP[wv][4 * slot + 3] = v4f{T[12], T[13], T[14], T[15]};
-                sIdx[wv][slot] = static_cast<int32_t>(idx - lo);
+                sIdx[wv][slot] = rel;
                 if constexpr (WRITE_DUAL) {
-                    sD[wv][2 * slot] = v4f{-(a[0] + ls[0]) * kLn2, -(a[1] + ls[1]) * kLn2,
-                                           -(a[2] + ls[2]) * kLn2, -(a[3] + ls[3]) * kLn2};
+                    sD[wv][2 * slot] = v4f{-a[0] * kLn2, -a[1] * kLn2, -a[2] * kLn2, -a[3] * kLn2};
                     sD[wv][2 * slot + 1] = v4f{b0 * kLn2, b1 * kLn2, b2 * kLn2, b0 * 0.f};
                 }
                 if constexpr (WRITE_ITERS) {
@@ -443,61 +480,61 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
                 staged = true;
             }
         }
-        // refill: finished lanes claim the next problems of the wave's range in lane order
+        // refill: finished lanes take the next problems of the wave's range in lane order
         const uint64_t fm = __ballot(fin);
         if (fm) {
             const int k = __popcll(fm);
-            const int off = static_cast<int>((next - lo) & 63);
             const int rank = __popcll(fm & below);
-            const int src = (off + rank) & 63;
-            uint32_t got[NW];
+            // lanes with take set receive problem ibase + src (src < 64) of the batch held
+            // in iU, ia, ib (uniform ds_bpermute: every lane supplies its slot)
+            auto take = [&](bool take_it, int src) {
+                const int addr = (src & 63) << 2;
+                float gU[16], ga[4];
 #pragma unroll
-            for (int q = 0; q < NW; ++q)
-                got[q] = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(src << 2, static_cast<int>(ring[q])));
-            const int pos = (lane - off) & 63;
-            if (pos < k && next + pos + 64 < hi) load_raw<DT>(H, next + pos + 64, ring);
-            if (fin) {
-                idx = next + rank;
-                active = idx < hi;
-                fin = false;
-                if (active) {
-                    // new problem: L = H log2(e); x^(0) = column-centring beta. A NaN or
-                    // infinite entry poisons every derived value with NaN.
-                    float h[16];
-                    decode_raw<DT>(got, h);
-                    float cm[4];
+                for (int q = 0; q < 16; ++q)
+                    gU[q] = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(iU[q])));
 #pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        cm[j] = 0.25f * kLog2e * ((h[j] + h[4 + j]) + (h[8 + j] + h[12 + j]));
-                    // NaN or +-Inf anywhere makes this sum NaN or infinite (a finite sum
-                    // that overflows needs entries near FLT_MAX, where exp overflows anyway)
-                    const float hs = (cm[0] + cm[1]) + (cm[2] + cm[3]);
-                    nonfinite = !(__builtin_fabsf(hs) <= 3.402823466e38f);
-                    const float poison = hs - hs;  // 0, or NaN for a non-finite input
-                    b0 = cm[3] - cm[0] + poison;
-                    b1 = cm[3] - cm[1] + poison;
-                    b2 = cm[3] - cm[2] + poison;
+                for (int i = 0; i < 4; ++i)
+                    ga[i] = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(ia[i])));
+                const float g0 = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(ib0)));
+                const float g1 = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(ib1)));
+                const float g2 = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(ib2)));
+                if (take_it) {
+                    rel = ibase + (src & 63);
+                    active = rel < nrel;
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        U[4 * i + 0] = __builtin_fmaf(h[4 * i + 0], kLog2e, b0);
-                        U[4 * i + 1] = __builtin_fmaf(h[4 * i + 1], kLog2e, b1);
-                        U[4 * i + 2] = __builtin_fmaf(h[4 * i + 2], kLog2e, b2);
-                        U[4 * i + 3] = __builtin_fmaf(h[4 * i + 3], kLog2e, poison);
-                        a[i] = 0.f;
-                        ls[i] = 0.f;
-                    }
+                    for (int q = 0; q < 16; ++q) U[q] = gU[q];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) a[i] = ga[i];
+                    b0 = g0;
+                    b1 = g1;
+                    b2 = g2;
+                    nonfinite = __builtin_isnan(g0);  // beta is NaN exactly for poisoned inputs
                     d0 = d1 = d2 = 0.f;
                     t = o0 = o1 = o2 = 0.f;
-                    tscale = 1.f;
-                    slope = gn2 = fofs = 0.f;
-                    evals = 0;
+                    gn2 = fofs = 0.f;
+                    cnt = 0;
                     first = true;
                 }
+            };
+            const int avail = 64 - icur;
+            if (avail > 0) take(fin && rank < avail, icur + rank);
+            if (k > avail) {
+                // the batch ran out: initialise the next one (its raw words were loaded a
+                // batch ago) and start loading the one after it
+                ibase += 64;
+                init_problem<DT>(raw, iU, ia, ib0, ib1, ib2);
+                if (ibase + 64 + lane < nrel) load_raw<DT>(H, lo + ibase + 64 + lane, raw);
+                take(fin && rank >= avail, rank - avail);
+                icur = k - avail;
+            } else {
+                icur += k;
             }
-            next += k;
+            fin = false;
         }
-        // outputs staged this iteration are written after the ring loads are issued, so
-        // the wait of the next refill covers stores one iteration old
+        // outputs staged this iteration are written after the batch loads are issued, so
+        // the wait before the next batch initialisation covers stores at least one
+        // iteration old
         count += __popcll(__ballot(staged));
         while (count >= 16) flush(16);
         if (__ballot(active) == 0) {
@@ -765,7 +802,7 @@ int launch_fwd(const void* H, float* P, float* dual, int32_t* iters, int64_t B, 
     int64_t waves = static_cast<int64_t>(cus) * fwd_blocks_per_cu<DT, WD, WI>() * (kFwdBlock / 64);
     if (waves > waves_needed) waves = waves_needed;
     const int64_t chunk = (B + waves - 1) / waves;
-    if (chunk > INT32_MAX) return BIRKHOFF4_ERR_SIZE;  // staged outputs keep 32-bit offsets
+    if (chunk > INT32_MAX - 128) return BIRKHOFF4_ERR_SIZE;  // problems are 32-bit offsets in a range
     waves = (B + chunk - 1) / chunk;
     const int64_t blocks = (waves * 64 + kFwdBlock - 1) / kFwdBlock;
     hipLaunchKernelGGL((newton_fwd_kernel<DT, WD, WI>), dim3(static_cast<unsigned>(blocks)),
