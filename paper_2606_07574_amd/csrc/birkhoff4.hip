@@ -74,10 +74,10 @@ constexpr float kPivMin = 1e-30f;
 constexpr float kFltMin = 1.17549435e-38f;
 constexpr int kMaxSkSteps = 48;   // sk_bwd keeps (n+1) x 4 floats per lane in LDS
 constexpr int kMaxIterCap = 10000;
-constexpr int kFwdBlock = 256;
+constexpr int kFwdBlock = 1024;  // one workgroup per CU: 16 waves, 4 per SIMD
 constexpr int kFwdWaves = kFwdBlock / 64;
-// Per-wave ring of finished outputs: at most 15 left after a flush plus 64 new ones.
-constexpr int kStageCap = 80;
+// Ring slot of the forward kernel, in v4f: a problem's initial state (6 v4f) or its output (7).
+constexpr int kSlot = 7;
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
@@ -284,51 +284,79 @@ __device__ __forceinline__ void init_problem(const uint32_t w[RawWords<DT>::n], 
     }
 }
 
+// Initial state of the batch member held by this lane, written to its ring slot:
+// U rows in v4f 0..3, the row offsets a in v4f 4, (beta_1..3, unused) in v4f 5.
+template <int DT>
+__device__ __forceinline__ void init_to_slot(const uint32_t w[RawWords<DT>::n], v4f* slot) {
+    float U[16], a[4], b0, b1, b2;
+    init_problem<DT>(w, U, a, b0, b1, b2);
+    slot[0] = v4f{U[0], U[1], U[2], U[3]};
+    slot[1] = v4f{U[4], U[5], U[6], U[7]};
+    slot[2] = v4f{U[8], U[9], U[10], U[11]};
+    slot[3] = v4f{U[12], U[13], U[14], U[15]};
+    slot[4] = v4f{a[0], a[1], a[2], a[3]};
+    slot[5] = v4f{b0, b1, b2, 0.f};
+}
+
 template <int DT, bool WRITE_DUAL, bool WRITE_ITERS>
-__global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict__ H,
-                                                          float* __restrict__ P,
-                                                          float* __restrict__ dual,
-                                                          int32_t* __restrict__ iters, int64_t B,
-                                                          int64_t chunk, float tol, int max_iter) {
+__global__ __launch_bounds__(kFwdBlock) void newton_fwd_kernel(const void* __restrict__ H,
+                                                                float* __restrict__ P,
+                                                                float* __restrict__ dual,
+                                                                int32_t* __restrict__ iters, int64_t B,
+                                                                int64_t chunk, float tol, int max_iter) {
     constexpr int NW = RawWords<DT>::n;
     const int lane = threadIdx.x & 63;
     // the wave index is uniform across the wave: keep the range bookkeeping in SGPRs
     const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
-    const int64_t wave = static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + wv;
-    constexpr int SC = kStageCap, SD = WRITE_DUAL ? kStageCap : 1, SI = WRITE_ITERS ? kStageCap : 1;
-    __shared__ v4f sP[kFwdWaves][4 * SC];
-    __shared__ v4f sD[kFwdWaves][2 * SD];
-    __shared__ int32_t sIdx[kFwdWaves][SC];  // problem index - lo
-    __shared__ int32_t sIt[kFwdWaves][SI];
-    int head = 0, count = 0;  // staged outputs: slots head .. head + count - 1 (mod SC)
-    const int64_t lo = wave * chunk;
-    if (lo >= B) return;  // uniform across the wave
+    // Per-wave ring of 64 slots of kSlot v4f. A slot first holds the initial state of
+    // one problem of the wave's current batch; the lane that takes it leaves its
+    // finished output there (P rows in v4f 0..3, dual in 4..5, (index, status) in 6),
+    // and the outputs are written to HBM from the ring 16 problems at a time.
+    __shared__ v4f ring_all[kFwdWaves][64 * kSlot];
+    __shared__ int32_t next_batch;  // next unclaimed batch of the block's range
+    v4f* const ring = ring_all[wv];
+    // The block owns problems lo .. hi - 1, in batches of 64 consecutive problems. Its
+    // waves share them through an LDS counter: a wave that the SIMD arbiter favours
+    // simply takes more batches, so all waves of a CU finish within about one batch.
+    const int64_t lo = static_cast<int64_t>(blockIdx.x) * chunk;
+    if (lo >= B) return;  // uniform across the block
     const int64_t hi = (lo + chunk < B) ? lo + chunk : B;
+    const int32_t nrel = static_cast<int32_t>(hi - lo);
+    const int32_t nbatch = (nrel + 63) >> 6;
+    if (threadIdx.x == 0) next_batch = kFwdWaves;  // wave w starts on batch w
+    __syncthreads();
+    if (wv >= nbatch) return;  // uniform across the wave
+    auto claim = [&]() -> int32_t {
+        int32_t v = 0;
+        if (lane == 0) v = atomicAdd(&next_batch, 1);
+        return __builtin_amdgcn_readfirstlane(v);
+    };
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 
-    const int32_t nrel = static_cast<int32_t>(hi - lo);
-    // Problem supply: the range is taken in batches of 64 consecutive problems, one per
-    // lane. The raw words of the next batch are loaded one batch ahead with whole-wave
-    // loads; when the current batch runs out the whole wave initialises the next one at
-    // once (full EXEC), and finishing lanes take initialised problems with ds_bpermute.
+    // Problem supply: the raw words of the wave's next batch are loaded one batch ahead
+    // with whole-wave loads; when a batch runs out the whole wave initialises the next
+    // one at once (full EXEC, one problem per lane) into the ring, where finishing lanes
+    // pick them up. Every lane starts on its own member of the first batch, straight
+    // from registers.
     uint32_t raw[NW];
 #pragma unroll
     for (int q = 0; q < NW; ++q) raw[q] = 0u;
-    if (lane < nrel) load_raw<DT>(H, lo + lane, raw);
-    float iU[16], ia[4], ib0, ib1, ib2;  // initial state of problem ibase + lane
-    init_problem<DT>(raw, iU, ia, ib0, ib1, ib2);
-    if (64 + lane < nrel) load_raw<DT>(H, lo + 64 + lane, raw);
-    int32_t ibase = 0;  // first problem of the initialised batch (offset from lo)
-    int icur = 0;       // problems of that batch already taken
-    int32_t rel = -1;  // this lane's problem, as an offset from lo
-    bool active = false;
-    bool fin = true;  // every lane starts by claiming a problem
-
+    const int32_t first_rel = (wv << 6) + lane;
+    if (first_rel < nrel) load_raw<DT>(H, lo + first_rel, raw);
     // Per-problem state. U is the current point, normalised per row, in log2 units:
     // U = H log2(e) + beta - a 1^T = log2 T; (beta, a) give the dual at output.
     float U[16];
-    float b0 = 0.f, b1 = 0.f, b2 = 0.f;           // beta_1..3 of the current point (log2 units)
+    float b0, b1, b2;                             // beta_1..3 of the current point (log2 units)
     float a[4];                                   // row log-sum-exp of H log2(e) + beta
+    init_problem<DT>(raw, U, a, b0, b1, b2);
+    int32_t nxt = claim();  // batch whose raw words are loading into raw
+    if ((nxt << 6) + lane < nrel) load_raw<DT>(H, lo + (nxt << 6) + lane, raw);
+    int32_t ibase = 0;    // first problem of the batch in the ring (offset from lo)
+    int icur = 64;        // ring slots already taken (the first batch lives in registers)
+    int head = 64;        // outputs waiting in the ring occupy slots head .. icur - 1
+    int32_t rel = first_rel;  // this lane's problem, as an offset from lo
+    bool active = rel < nrel;
+    bool nonfinite = __builtin_isnan(b0);  // beta is NaN exactly for poisoned inputs
     float d0 = 0.f, d1 = 0.f, d2 = 0.f;           // Newton direction at the accepted point
     float t = 0.f;                                // trial step along d
     float o0 = 0.f, o1 = 0.f, o2 = 0.f;           // current point minus accepted point
@@ -339,55 +367,47 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
     Weights Wa = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     // bits 0-15: trial steps taken; bits 16-18: log2 of the initial trial step
     int cnt = 0;
-    bool first = true, nonfinite = false;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = 0.f;
-#pragma unroll
-    for (int q = 0; q < 16; ++q) U[q] = 0.f;
+    bool first = true;
 
-    // Write out n <= 16 staged outputs from slot head on: 4 lanes per P (one 64-byte
-    // row block each), 2 per dual, 1 per iteration count, so every store instruction
-    // writes whole 64-byte pieces of up to 16 problems.
-    auto flush = [&](int n) {
+    // Write out n <= 16 finished outputs from ring slot h on: 4 lanes per P (one 64-byte
+    // row block each), 2 per dual, 1 per status, so every store instruction writes
+    // whole 64-byte pieces of up to 16 problems.
+    auto flush = [&](int h, int n) {
         __builtin_amdgcn_wave_barrier();
         {
-            int e = lane >> 2;
+            const int e = lane >> 2;
             if (e < n) {
-                e += head;
-                if (e >= SC) e -= SC;
-                const v4f v = sP[wv][4 * e + (lane & 3)];
-                reinterpret_cast<v4f*>(P)[4 * (lo + sIdx[wv][e]) + (lane & 3)] = v;
+                const v4f* sl = ring + (h + e) * kSlot;
+                const int32_t idx = __float_as_int(sl[6].x);
+                reinterpret_cast<v4f*>(P)[4 * (lo + idx) + (lane & 3)] = sl[lane & 3];
             }
         }
         if constexpr (WRITE_DUAL) {
-            int e = lane >> 1;
+            const int e = lane >> 1;
             if (e < n) {
-                e += head;
-                if (e >= SC) e -= SC;
-                const v4f v = sD[wv][2 * e + (lane & 1)];
-                reinterpret_cast<v4f*>(dual)[2 * (lo + sIdx[wv][e]) + (lane & 1)] = v;
+                const v4f* sl = ring + (h + e) * kSlot;
+                const int32_t idx = __float_as_int(sl[6].x);
+                reinterpret_cast<v4f*>(dual)[2 * (lo + idx) + (lane & 1)] = sl[4 + (lane & 1)];
             }
         }
         if constexpr (WRITE_ITERS) {
             if (lane < n) {
-                int e = head + lane;
-                if (e >= SC) e -= SC;
-                iters[lo + sIdx[wv][e]] = sIt[wv][e];
+                const v4f* sl = ring + (h + lane) * kSlot;
+                iters[lo + __float_as_int(sl[6].x)] = __float_as_int(sl[6].y);
             }
         }
         __builtin_amdgcn_wave_barrier();
-        head += n;
-        if (head >= SC) head -= SC;
-        count -= n;
     };
 
     for (;;) {
-        bool staged = false;
+        bool fin = false;
+        float T[16];
+        int status = 0;
         if (active) {
             // trial point: accepted point + t d, reached from the current point
             const float s0 = __builtin_fmaf(t, d0, -o0), s1 = __builtin_fmaf(t, d1, -o1),
                         s2 = __builtin_fmaf(t, d2, -o2);
-            float T[16], lsum[4], g[4];
+            float lsum[4], g[4];
             evaluate_inplace(U, s0, s1, s2, T, lsum, g);
             const float gmax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(g[0]), __builtin_fabsf(g[1])),
                                                __builtin_fmaxf(__builtin_fabsf(g[2]), __builtin_fabsf(g[3])));
@@ -459,86 +479,71 @@ __global__ __launch_bounds__(256) void newton_fwd_kernel(const void* __restrict_
                     b1 += r1;
                     b2 += r2;
                 }
-                // a non-finite input was poisoned with NaN at load, so T and the dual are NaN.
-                // Stage the outputs in this wave's LDS ring, in lane order after the
-                // outputs already staged.
-                int slot = head + count + __popcll(__ballot(1) & below);
-                if (slot >= SC) slot -= SC;
-                sP[wv][4 * slot + 0] = v4f{T[0], T[1], T[2], T[3]};
-                sP[wv][4 * slot + 1] = v4f{T[4], T[5], T[6], T[7]};
-                sP[wv][4 * slot + 2] = v4f{T[8], T[9], T[10], T[11]};
-                sP[wv][4 * slot + 3] = v4f{T[12], T[13], T[14], T[15]};
-                sIdx[wv][slot] = rel;
-                if constexpr (WRITE_DUAL) {
-                    sD[wv][2 * slot] = v4f{-a[0] * kLn2, -a[1] * kLn2, -a[2] * kLn2, -a[3] * kLn2};
-                    sD[wv][2 * slot + 1] = v4f{b0 * kLn2, b1 * kLn2, b2 * kLn2, b0 * 0.f};
-                }
-                if constexpr (WRITE_ITERS) {
-                    sIt[wv][slot] = nonfinite ? BIRKHOFF4_NON_FINITE
-                                              : (conv ? evals : BIRKHOFF4_NOT_CONVERGED);
-                }
-                staged = true;
+                // a non-finite input was poisoned with NaN at load, so T and the dual are NaN
+                status = nonfinite ? BIRKHOFF4_NON_FINITE : (conv ? evals : BIRKHOFF4_NOT_CONVERGED);
             }
         }
-        // refill: finished lanes take the next problems of the wave's range in lane order
+        // refill: finished lanes take the next problems of the wave's range in lane order,
+        // each from one ring slot, and leave their outputs in that slot
         const uint64_t fm = __ballot(fin);
         if (fm) {
             const int k = __popcll(fm);
             const int rank = __popcll(fm & below);
-            // lanes with take set receive problem ibase + src (src < 64) of the batch held
-            // in iU, ia, ib (uniform ds_bpermute: every lane supplies its slot)
-            auto take = [&](bool take_it, int src) {
-                const int addr = (src & 63) << 2;
-                float gU[16], ga[4];
-#pragma unroll
-                for (int q = 0; q < 16; ++q)
-                    gU[q] = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(iU[q])));
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    ga[i] = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(ia[i])));
-                const float g0 = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(ib0)));
-                const float g1 = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(ib1)));
-                const float g2 = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(ib2)));
-                if (take_it) {
-                    rel = ibase + (src & 63);
-                    active = rel < nrel;
-#pragma unroll
-                    for (int q = 0; q < 16; ++q) U[q] = gU[q];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) a[i] = ga[i];
-                    b0 = g0;
-                    b1 = g1;
-                    b2 = g2;
-                    nonfinite = __builtin_isnan(g0);  // beta is NaN exactly for poisoned inputs
-                    d0 = d1 = d2 = 0.f;
-                    t = o0 = o1 = o2 = 0.f;
-                    gn2 = fofs = 0.f;
-                    cnt = 0;
-                    first = true;
+            auto swap = [&](int sidx) {
+                v4f* sl = ring + sidx * kSlot;
+                const v4f u0 = sl[0], u1 = sl[1], u2 = sl[2], u3 = sl[3], av = sl[4], bv = sl[5];
+                sl[0] = v4f{T[0], T[1], T[2], T[3]};
+                sl[1] = v4f{T[4], T[5], T[6], T[7]};
+                sl[2] = v4f{T[8], T[9], T[10], T[11]};
+                sl[3] = v4f{T[12], T[13], T[14], T[15]};
+                if constexpr (WRITE_DUAL) {
+                    sl[4] = v4f{-a[0] * kLn2, -a[1] * kLn2, -a[2] * kLn2, -a[3] * kLn2};
+                    sl[5] = v4f{b0 * kLn2, b1 * kLn2, b2 * kLn2, b0 * 0.f};  // beta_4 = 0, NaN if poisoned
                 }
+                sl[6] = v4f{__int_as_float(rel), __int_as_float(status), 0.f, 0.f};
+                U[0] = u0.x; U[1] = u0.y; U[2] = u0.z; U[3] = u0.w;
+                U[4] = u1.x; U[5] = u1.y; U[6] = u1.z; U[7] = u1.w;
+                U[8] = u2.x; U[9] = u2.y; U[10] = u2.z; U[11] = u2.w;
+                U[12] = u3.x; U[13] = u3.y; U[14] = u3.z; U[15] = u3.w;
+                a[0] = av.x; a[1] = av.y; a[2] = av.z; a[3] = av.w;
+                b0 = bv.x;
+                b1 = bv.y;
+                b2 = bv.z;
+                rel = ibase + sidx;
+                active = rel < nrel;
+                nonfinite = __builtin_isnan(b0);
+                d0 = d1 = d2 = 0.f;
+                t = o0 = o1 = o2 = 0.f;
+                gn2 = fofs = 0.f;
+                cnt = 0;
+                first = true;
             };
             const int avail = 64 - icur;
-            if (avail > 0) take(fin && rank < avail, icur + rank);
+            if (fin && rank < avail) swap(icur + rank);
             if (k > avail) {
-                // the batch ran out: initialise the next one (its raw words were loaded a
-                // batch ago) and start loading the one after it
-                ibase += 64;
-                init_problem<DT>(raw, iU, ia, ib0, ib1, ib2);
-                if (ibase + 64 + lane < nrel) load_raw<DT>(H, lo + ibase + 64 + lane, raw);
-                take(fin && rank >= avail, rank - avail);
+                // the batch ran out: write out every output still in the ring, then
+                // initialise the next batch (its raw words were loaded a batch ago) into
+                // the ring and start loading the one after it
+                for (int h = head; h < 64; h += 16) flush(h, (64 - h < 16) ? 64 - h : 16);
+                ibase = nxt << 6;  // past the range once the block's batches are all claimed
+                init_to_slot<DT>(raw, ring + lane * kSlot);
+                if (nxt < nbatch) {
+                    nxt = claim();
+                    if ((nxt << 6) + lane < nrel) load_raw<DT>(H, lo + (nxt << 6) + lane, raw);
+                }
+                if (fin && rank >= avail) swap(rank - avail);
                 icur = k - avail;
+                head = 0;
             } else {
                 icur += k;
             }
-            fin = false;
+            while (icur - head >= 16) {
+                flush(head, 16);
+                head += 16;
+            }
         }
-        // outputs staged this iteration are written after the batch loads are issued, so
-        // the wait before the next batch initialisation covers stores at least one
-        // iteration old
-        count += __popcll(__ballot(staged));
-        while (count >= 16) flush(16);
         if (__ballot(active) == 0) {
-            if (count > 0) flush(count);
+            if (icur > head) flush(head, icur - head);
             break;
         }
     }
@@ -787,24 +792,23 @@ int fwd_blocks_per_cu() {
         int nb = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, newton_fwd_kernel<DT, WD, WI>, kFwdBlock, 0) !=
                 hipSuccess || nb <= 0)
-            nb = 4;
+            nb = 1;
         cached = nb;
     }
     return cached;
 }
 
-// Launch exactly as many waves as can be resident, each owning a contiguous
-// range of problems (lane-level refill inside the range).
+// Launch one resident workgroup per CU (as many as the occupancy calculator allows),
+// each owning a contiguous range of whole 64-problem batches that its waves share.
 template <int DT, bool WD, bool WI>
 int launch_fwd(const void* H, float* P, float* dual, int32_t* iters, int64_t B, float tol,
                int max_iter, hipStream_t stream, int cus) {
-    const int64_t waves_needed = (B + 63) / 64;
-    int64_t waves = static_cast<int64_t>(cus) * fwd_blocks_per_cu<DT, WD, WI>() * (kFwdBlock / 64);
-    if (waves > waves_needed) waves = waves_needed;
-    const int64_t chunk = (B + waves - 1) / waves;
-    if (chunk > INT32_MAX - 128) return BIRKHOFF4_ERR_SIZE;  // problems are 32-bit offsets in a range
-    waves = (B + chunk - 1) / chunk;
-    const int64_t blocks = (waves * 64 + kFwdBlock - 1) / kFwdBlock;
+    const int64_t batches = (B + 63) / 64;
+    int64_t blocks = static_cast<int64_t>(cus) * fwd_blocks_per_cu<DT, WD, WI>();
+    if (blocks > batches) blocks = batches;
+    const int64_t chunk = ((batches + blocks - 1) / blocks) * 64;
+    if (chunk > INT32_MAX / 2) return BIRKHOFF4_ERR_SIZE;  // problems are 32-bit offsets in a range
+    blocks = (B + chunk - 1) / chunk;
     hipLaunchKernelGGL((newton_fwd_kernel<DT, WD, WI>), dim3(static_cast<unsigned>(blocks)),
                        dim3(kFwdBlock), 0, stream, H, P, dual, iters, B, chunk, tol, max_iter);
     return launch_status();
