@@ -19,6 +19,8 @@ FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "-shared", f"--offload-arch={ARCH}",
     # keep packed-fp32 instructions out of the generated code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # fp32 denormals flush to zero (the forward kernel relies on it, see csrc)
+    "-fgpu-flush-denormals-to-zero",
     "-Wall", "-Wno-unused-function",
 ]
 

@@ -7,16 +7,22 @@
 // (eq. sinkhorn_knopp) and its reverse-mode gradient.
 //
 // Mapping: one 4x4 problem per lane; all per-problem state lives in VGPRs. No
-// MFMA (the only products are six 4-long dot products per matrix), no atomics.
-// Loads and stores are plain 16-byte vector accesses (non-temporal hints
+// MFMA (the only products are six 4-long dot products per matrix), no global
+// atomics. Loads and stores are plain 16-byte vector accesses (non-temporal hints
 // measured slower on gfx950: the stores lose write combining). The implicit
-// kernel uses no LDS; the Newton kernel uses LDS only to stage its outputs.
+// kernel uses no LDS; the Newton kernel uses LDS for its ring of initialised
+// problems and for the batch counter its waves share.
 //
-// Forward numerics (fp32, log2 domain so that v_exp_f32 applies directly):
-//  * state is U = H*log2(e) + beta - a 1^T with every row re-centred to max 0
-//    after each accepted step, so entries that carry mass are near 0 and keep
-//    full fp32 resolution even when |beta| is in the hundreds (a beta-only state
-//    cannot tune the column sums below ~1e-5 there);
+// Forward numerics (fp32; exponents in log2 units so that v_exp_f32 applies directly;
+// the library is compiled with fp32 denormals flushed to zero):
+//  * state is the row softmax T at the current point, with the row normalisers a and
+//    column potentials beta (log2 T = H log2(e) + beta - a 1^T). A trial that moves the
+//    potentials by s multiplies column j by 2^(s_j) and renormalises the rows: three
+//    exponentials per trial instead of sixteen, and entries keep full relative precision
+//    whatever |beta| is (a beta-only state recomputed from H cannot tune the column sums
+//    below ~1e-5 once |beta| reaches hundreds). Entries that fall below the smallest
+//    normal float flush to zero and are re-derived from H once the accumulated column
+//    shifts could have brought them within reach of fp32 resolution;
 //  * Hessian of the reduced dual = Laplacian of the column graph with weights
 //    W_jk = sum_i T_ij T_ik (rows of T sum to one), grounded at column 4; the
 //    Newton system is solved by elimination with pivots formed as sums of these
@@ -29,20 +35,18 @@
 //    decrease; each backtrack halves the step and multiplies the shift by 16
 //    (re-solving with the saved weights), and the trial step doubles while full
 //    steps keep descending strongly;
-//  * initial point beta_j = mean_i H_i4 - mean_i H_ij (column centring);
+//  * initial point beta_j = mean_i H_i4 - mean_i H_ij (column centring), evaluated in the
+//    log domain;
 //  * stop when max over the four columns of |c_j - 1| <= tol.
 //
-// Lane-level work refill: each wave owns a contiguous range of problems; a
-// lane whose problem is finished writes it out and takes the next unclaimed
-// problem of its wave's range at once, so a wave pays the mean number of
-// Newton steps, not the maximum over its 64 lanes. The next 64 problems of the
-// range are prefetched into a register ring spread over the wave's lanes and
-// handed to finishing lanes with ds_bpermute, so a refill never waits on HBM.
-// Finished outputs are staged in a per-wave LDS ring and written 16 problems
-// at a time by the whole wave (4 lanes per 64-byte P block, 2 per dual), so a
-// store instruction writes whole 64-byte pieces instead of one 16-byte piece
-// per finishing lane; the flush is issued after the ring loads, so the wait that
-// the next refill needs never covers stores issued in the same iteration.
+// Work distribution: each workgroup owns a contiguous range of problems, cut into
+// batches of 64 that its waves claim through an LDS counter. A wave initialises a batch
+// with one problem per lane at full width: the initial point, its column sums and, for
+// problems not already converged there, the column weights and gradient. Problems that
+// are finished at the initial point are written out at once; the others are compacted
+// into a per-wave LDS ring. Every lane then runs Newton trials on its own problem, and a
+// lane whose problem finishes writes it out and takes the next problem from the ring at
+// once, so a wave pays the mean number of trials, not the maximum over its 64 lanes.
 
 #include <hip/hip_runtime.h>
 
@@ -77,8 +81,13 @@ constexpr int kMaxIterCap = 10000;
 constexpr int64_t kMaxGrid = int64_t(1) << 24;  // blocks of a streaming launch
 constexpr int kFwdBlock = 1024;  // one workgroup per CU: 16 waves, 4 per SIMD
 constexpr int kFwdWaves = kFwdBlock / 64;
-// Ring slot of the forward kernel, in v4f: a problem's initial state (6 v4f) or its output (7).
-constexpr int kSlot = 7;
+// Ring slot of the forward kernel, in v4f: a problem's state at its initial point.
+constexpr int kSlot = 9;
+// Accumulated spread of column shifts (log2 units) after which entries that flushed to
+// zero are re-derived from H: such an entry was below 2^-126 when it flushed and has grown
+// by at most this much (plus one trial's spread, <= 2 step caps) since, so it is still
+// below 2^-43 when it is re-derived.
+constexpr float kReviveBits = 60.0f;
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
@@ -171,42 +180,6 @@ __device__ __forceinline__ void store16(float* base, int64_t b, const float v[16
 // Forward
 // ---------------------------------------------------------------------------
 
-// Row-softmax evaluation at the trial point U + s (log2 units, s_4 = 0), eq. tij_stable.
-// Every row of U has log-sum-exp 0 (U = log2 of the current T), and each column shift
-// of a trial is bounded by the step cap, so 2^(U + s) needs no max subtraction: it
-// neither overflows nor loses a row's dominant entry. U is replaced by the trial
-// re-normalised per row (the new current point); T = the row softmax; lsum = log2 of
-// the row sums of 2^(U + s); g = column sums - 1 (eq. c_g, all four columns).
-__device__ __forceinline__ void evaluate_inplace(float U[16], float s0, float s1, float s2, float T[16],
-                                                 float lsum[4], float g[4]) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const float u0 = U[4 * i + 0] + s0;
-        const float u1 = U[4 * i + 1] + s1;
-        const float u2 = U[4 * i + 2] + s2;
-        const float u3 = U[4 * i + 3];
-        const float e0 = ex2(u0);
-        const float e1 = ex2(u1);
-        const float e2 = ex2(u2);
-        const float e3 = ex2(u3);
-        const float sum = (e0 + e1) + (e2 + e3);
-        const float r = rcp(sum);
-        const float l = lg2(sum);
-        T[4 * i + 0] = e0 * r;
-        T[4 * i + 1] = e1 * r;
-        T[4 * i + 2] = e2 * r;
-        T[4 * i + 3] = e3 * r;
-        U[4 * i + 0] = u0 - l;
-        U[4 * i + 1] = u1 - l;
-        U[4 * i + 2] = u2 - l;
-        U[4 * i + 3] = u3 - l;
-        lsum[i] = l;
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-        g[j] = ((T[j] + T[4 + j]) + (T[8 + j] + T[12 + j])) - 1.0f;
-}
-
 // Column-graph weights W_jk = sum_i T_ij T_ik (the p_jk of Sec. 3.2 extended to
 // column 4). With unit row sums the Hessian of the reduced dual is the Laplacian
 // of this graph grounded at column 4: h_jk = -W_jk, h_jj = sum_{k != j} W_jk.
@@ -252,14 +225,49 @@ __device__ __forceinline__ void newton_solve(const Weights& W, float g0, float g
     d0 = __builtin_fmaf(W.w01, d1, __builtin_fmaf(W.w02, d2, r0)) * i0;
 }
 
-// Initial state of one problem from its raw words: x^(0) = column-centring beta
-// (beta_j = mean_i H_i4 - mean_i H_ij), U = H log2(e) + beta - a 1^T with a = the row
-// maxima, so every row of U starts at max 0. A NaN or infinite entry makes the column
-// mean sum NaN or infinite and poisons U, a and beta with NaN (a finite sum that
-// overflows needs entries near FLT_MAX, where exp overflows anyway).
+// Spread max_j v_j - min_j v_j of a column shift (v_4 = 0). It bounds how far any entry
+// of the row-normalised T can move, in log2 units, when the column potentials move by v.
+__device__ __forceinline__ float spread(float v0, float v1, float v2) {
+    return __builtin_fmaxf(__builtin_fmaxf(v0, v1), __builtin_fmaxf(v2, 0.f)) -
+           __builtin_fminf(__builtin_fminf(v0, v1), __builtin_fminf(v2, 0.f));
+}
+
+// Trial evaluation, eq. tij_stable in product form. T is the row softmax at the current
+// point; moving the column potentials by s (log2 units, s_4 = 0) multiplies column j by
+// 2^(s_j), and each row is renormalised. T becomes the trial's row softmax, l the log2 of
+// the row sums (the change of the row normalisers) and g the column sums minus one
+// (eq. c_g, all four columns). Products that fall below the smallest normal float flush
+// to zero; such entries are re-derived from H when they could matter again.
+__device__ __forceinline__ void evaluate(float T[16], float s0, float s1, float s2, float l[4], float g[4]) {
+    const float S0 = ex2(s0), S1 = ex2(s1), S2 = ex2(s2);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float e0 = T[4 * i + 0] * S0;
+        const float e1 = T[4 * i + 1] * S1;
+        const float e2 = T[4 * i + 2] * S2;
+        const float e3 = T[4 * i + 3];
+        const float sum = (e0 + e1) + (e2 + e3);
+        const float r = rcp(sum);
+        l[i] = lg2(sum);
+        T[4 * i + 0] = e0 * r;
+        T[4 * i + 1] = e1 * r;
+        T[4 * i + 2] = e2 * r;
+        T[4 * i + 3] = e3 * r;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        g[j] = ((T[j] + T[4 + j]) + (T[8 + j] + T[12 + j])) - 1.0f;
+}
+
+// Initial point of one problem from its raw words: beta^(0)_j = mean_i H_i4 - mean_i H_ij
+// (column centring), T = row softmax of H + 1 beta^T evaluated in the log domain with the
+// row maxima subtracted (eq. tij_stable), a = log2 of the row normalisers of
+// H log2(e) + beta, g = column sums - 1. A NaN or infinite entry makes the column-mean
+// sum NaN or infinite and poisons T, a and beta with NaN (a finite sum that overflows
+// needs entries near FLT_MAX, where exp overflows anyway).
 template <int DT>
-__device__ __forceinline__ void init_problem(const uint32_t w[RawWords<DT>::n], float U[16], float a[4],
-                                             float& b0, float& b1, float& b2) {
+__device__ __forceinline__ void init_problem(const uint32_t w[RawWords<DT>::n], float T[16], float a[4],
+                                             float& b0, float& b1, float& b2, float g[4]) {
     float h[16];
     decode_raw<DT>(w, h);
     float cm[4];
@@ -277,26 +285,33 @@ __device__ __forceinline__ void init_problem(const uint32_t w[RawWords<DT>::n], 
         const float u2 = __builtin_fmaf(h[4 * i + 2], kLog2e, b2);
         const float u3 = __builtin_fmaf(h[4 * i + 3], kLog2e, poison);
         const float m = __builtin_fmaxf(__builtin_fmaxf(u0, u1), __builtin_fmaxf(u2, u3)) + poison;
-        U[4 * i + 0] = u0 - m;
-        U[4 * i + 1] = u1 - m;
-        U[4 * i + 2] = u2 - m;
-        U[4 * i + 3] = u3 - m;
-        a[i] = m;
+        const float e0 = ex2(u0 - m), e1 = ex2(u1 - m), e2 = ex2(u2 - m), e3 = ex2(u3 - m);
+        const float sum = (e0 + e1) + (e2 + e3);
+        const float r = rcp(sum);
+        T[4 * i + 0] = e0 * r;
+        T[4 * i + 1] = e1 * r;
+        T[4 * i + 2] = e2 * r;
+        T[4 * i + 3] = e3 * r;
+        a[i] = m + lg2(sum);
     }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        g[j] = ((T[j] + T[4 + j]) + (T[8 + j] + T[12 + j])) - 1.0f;
 }
 
-// Initial state of the batch member held by this lane, written to its ring slot:
-// U rows in v4f 0..3, the row offsets a in v4f 4, (beta_1..3, unused) in v4f 5.
-template <int DT>
-__device__ __forceinline__ void init_to_slot(const uint32_t w[RawWords<DT>::n], v4f* slot) {
-    float U[16], a[4], b0, b1, b2;
-    init_problem<DT>(w, U, a, b0, b1, b2);
-    slot[0] = v4f{U[0], U[1], U[2], U[3]};
-    slot[1] = v4f{U[4], U[5], U[6], U[7]};
-    slot[2] = v4f{U[8], U[9], U[10], U[11]};
-    slot[3] = v4f{U[12], U[13], U[14], U[15]};
-    slot[4] = v4f{a[0], a[1], a[2], a[3]};
-    slot[5] = v4f{b0, b1, b2, 0.f};
+// Output of one problem: P = T, dual = (alpha*(beta), beta) in natural-log units with
+// beta_4 = 0 (NaN for a poisoned input), and the status word.
+template <bool WRITE_DUAL, bool WRITE_ITERS>
+__device__ __forceinline__ void store_output(float* __restrict__ P, float* __restrict__ dual,
+                                             int32_t* __restrict__ iters, int64_t gi, const float T[16],
+                                             const float a[4], float b0, float b1, float b2, int status) {
+    store16(P, gi, T);
+    if constexpr (WRITE_DUAL) {
+        v4f* dp = reinterpret_cast<v4f*>(dual) + 2 * gi;
+        dp[0] = v4f{-a[0] * kLn2, -a[1] * kLn2, -a[2] * kLn2, -a[3] * kLn2};
+        dp[1] = v4f{b0 * kLn2, b1 * kLn2, b2 * kLn2, b0 * 0.f};
+    }
+    if constexpr (WRITE_ITERS) iters[gi] = status;
 }
 
 template <int DT, bool WRITE_DUAL, bool WRITE_ITERS>
@@ -309,10 +324,11 @@ __global__ __launch_bounds__(kFwdBlock) void newton_fwd_kernel(const void* __res
     const int lane = threadIdx.x & 63;
     // the wave index is uniform across the wave: keep the range bookkeeping in SGPRs
     const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
-    // Per-wave ring of 64 slots of kSlot v4f. A slot first holds the initial state of
-    // one problem of the wave's current batch; the lane that takes it leaves its
-    // finished output there (P rows in v4f 0..3, dual in 4..5, (index, status) in 6),
-    // and the outputs are written to HBM from the ring 16 problems at a time.
+    // Per-wave ring of 64 slots of kSlot v4f. A slot first holds a problem that is
+    // initialised and not finished at its initial point: T rows (v4f 0..3), a (4),
+    // beta_1..3 and the problem's offset (5), the column weights and gradient at the
+    // initial point (6..8). The lane that takes it leaves the output of its previous
+    // problem in its place: P rows (0..3), dual (4..5), (offset or -1, status) (6).
     __shared__ v4f ring_all[kFwdWaves][64 * kSlot];
     __shared__ int32_t next_batch;  // next unclaimed batch of the block's range
     v4f* const ring = ring_all[wv];
@@ -334,116 +350,197 @@ __global__ __launch_bounds__(kFwdBlock) void newton_fwd_kernel(const void* __res
     };
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 
-    // Problem supply: the raw words of the wave's next batch are loaded one batch ahead
-    // with whole-wave loads; when a batch runs out the whole wave initialises the next
-    // one at once (full EXEC, one problem per lane) into the ring, where finishing lanes
-    // pick them up. Every lane starts on its own member of the first batch, straight
-    // from registers.
+    // Raw words of the batch to initialise next (one problem per lane), loaded one batch
+    // ahead with whole-wave loads.
     uint32_t raw[NW];
 #pragma unroll
     for (int q = 0; q < NW; ++q) raw[q] = 0u;
-    const int32_t first_rel = (wv << 6) + lane;
-    if (first_rel < nrel) load_raw<DT>(H, lo + first_rel, raw);
-    // Per-problem state. U is the current point, normalised per row, in log2 units:
-    // U = H log2(e) + beta - a 1^T = log2 T; (beta, a) give the dual at output.
-    float U[16];
-    float b0, b1, b2;                             // beta_1..3 of the current point (log2 units)
-    float a[4];                                   // row log-sum-exp of H log2(e) + beta
-    init_problem<DT>(raw, U, a, b0, b1, b2);
-    int32_t nxt = claim();  // batch whose raw words are loading into raw
+    int32_t nxt = wv;
     if ((nxt << 6) + lane < nrel) load_raw<DT>(H, lo + (nxt << 6) + lane, raw);
-    int32_t ibase = 0;    // first problem of the batch in the ring (offset from lo)
-    int icur = 64;        // ring slots already taken (the first batch lives in registers)
-    int head = 64;        // outputs waiting in the ring occupy slots head .. icur - 1
-    int32_t rel = first_rel;  // this lane's problem, as an offset from lo
-    bool active = rel < nrel;
-    bool nonfinite = __builtin_isnan(b0);  // beta is NaN exactly for poisoned inputs
-    float d0 = 0.f, d1 = 0.f, d2 = 0.f;           // Newton direction at the accepted point
-    float t = 0.f;                                // trial step along d
-    float o0 = 0.f, o1 = 0.f, o2 = 0.f;           // current point minus accepted point
-    float gn2 = 0.f;
-    float fofs = 0.f;                             // f(current) - f(accepted), log2 units
-    float ga0 = 0.f, ga1 = 0.f, ga2 = 0.f;       // gradient at the accepted point
+    int nfresh = 0;  // ring slots [icur, nfresh) hold problems not yet taken
+    int icur = 0;
+
+    // Per-problem state of this lane. T is the current point (row softmax); a, beta its
+    // row normalisers and column potentials (log2 units, so log2 T = H log2(e) + beta - a).
+    bool active = false;   // working on a problem
+    bool want = true;      // needs a problem
+    bool has_out = false;  // holds the finished output of its last problem
+    int status = 0;        // status word of that output
+    int32_t rel = 0;       // problem offset from lo
+    float T[16], a[4], b0 = 0.f, b1 = 0.f, b2 = 0.f;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) T[q] = 0.f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) a[q] = 0.f;
+    Weights Wa = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};  // column weights at the accepted point
+    float ga0 = 0.f, ga1 = 0.f, ga2 = 0.f;        // gradient at the accepted point
     float lam = 0.f;                              // Levenberg-Marquardt shift
-    Weights Wa = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    float gn2 = 0.f;                              // |g|^2 at the accepted point
+    float t = 1.f;                                // trial step along the Newton direction
+    float o0 = 0.f, o1 = 0.f, o2 = 0.f;           // current point minus accepted point
+    float fofs = 0.f;                             // f(current) - f(accepted), log2 units
+    float gsum = 0.f;                             // column-shift spreads since the last re-derivation
     // bits 0-15: trial steps taken; bits 16-18: log2 of the initial trial step
     int cnt = 0;
-    bool first = true;
 
-    // Write out n <= 16 finished outputs from ring slot h on: 4 lanes per P (one 64-byte
-    // row block each), 2 per dual, 1 per status, so every store instruction writes
-    // whole 64-byte pieces of up to 16 problems.
-    auto flush = [&](int h, int n) {
-        __builtin_amdgcn_wave_barrier();
-        {
-            const int e = lane >> 2;
-            if (e < n) {
-                const v4f* sl = ring + (h + e) * kSlot;
-                const int32_t idx = __float_as_int(sl[6].x);
-                reinterpret_cast<v4f*>(P)[4 * (lo + idx) + (lane & 3)] = sl[lane & 3];
+    // Write out the outputs left in ring slots h0 .. h0 + n - 1, 16 problems at a time: 4
+    // lanes per P (one 64-byte row block each), 2 per dual, 1 per status, so that a store
+    // instruction writes whole 64-byte pieces. A slot whose offset is negative holds no
+    // output. Each pass reads its slots' offsets and data before it branches on them.
+    auto flush = [&](int h0, int n) {
+        for (int h = 0; h < n; h += 16) {
+            const int m = (n - h < 16) ? n - h : 16;
+            const int ep = lane >> 2, ed = lane >> 1;
+            const v4f* sp = ring + (h0 + h + (ep < m ? ep : 0)) * kSlot;
+            const v4f* sd = ring + (h0 + h + (ed < m ? ed : 0)) * kSlot;
+            const v4f* si = ring + (h0 + h + (lane < m ? lane : 0)) * kSlot;
+            const int32_t ip = __float_as_int(sp[6].x);
+            const v4f pv = sp[lane & 3];
+            int32_t id = -1;
+            v4f dv = {0.f, 0.f, 0.f, 0.f};
+            if constexpr (WRITE_DUAL) {
+                id = __float_as_int(sd[6].x);
+                dv = sd[4 + (lane & 1)];
             }
+            int32_t ii = -1, st = 0;
+            if constexpr (WRITE_ITERS) {
+                const v4f sv = si[6];
+                ii = __float_as_int(sv.x);
+                st = __float_as_int(sv.y);
+            }
+            if (ep < m && ip >= 0) reinterpret_cast<v4f*>(P)[4 * (lo + ip) + (lane & 3)] = pv;
+            if constexpr (WRITE_DUAL)
+                if (ed < m && id >= 0) reinterpret_cast<v4f*>(dual)[2 * (lo + id) + (lane & 1)] = dv;
+            if constexpr (WRITE_ITERS)
+                if (lane < m && ii >= 0) iters[lo + ii] = st;
         }
+    };
+
+    // Leave the output of this lane's finished problem in ring slot `slot`.
+    auto stage_output = [&](int slot, const float To[16], const float ao[4], float c0, float c1, float c2,
+                            int32_t idx, int st) {
+        v4f* sl = ring + slot * kSlot;
+        sl[0] = v4f{To[0], To[1], To[2], To[3]};
+        sl[1] = v4f{To[4], To[5], To[6], To[7]};
+        sl[2] = v4f{To[8], To[9], To[10], To[11]};
+        sl[3] = v4f{To[12], To[13], To[14], To[15]};
         if constexpr (WRITE_DUAL) {
-            const int e = lane >> 1;
-            if (e < n) {
-                const v4f* sl = ring + (h + e) * kSlot;
-                const int32_t idx = __float_as_int(sl[6].x);
-                reinterpret_cast<v4f*>(dual)[2 * (lo + idx) + (lane & 1)] = sl[4 + (lane & 1)];
-            }
+            sl[4] = v4f{-ao[0] * kLn2, -ao[1] * kLn2, -ao[2] * kLn2, -ao[3] * kLn2};
+            sl[5] = v4f{c0 * kLn2, c1 * kLn2, c2 * kLn2, c0 * 0.f};  // beta_4 = 0, NaN if poisoned
         }
-        if constexpr (WRITE_ITERS) {
-            if (lane < n) {
-                const v4f* sl = ring + (h + lane) * kSlot;
-                iters[lo + __float_as_int(sl[6].x)] = __float_as_int(sl[6].y);
-            }
+        sl[6] = v4f{__int_as_float(idx), __int_as_float(st), 0.f, 0.f};
+    };
+
+    // Initialise the batch whose raw words are loaded, one problem per lane with the whole
+    // wave. Every global store of the kernel is issued here (or after the last batch), right
+    // after the wait for the batch's words and before the next batch's words are requested:
+    // memory operations retire in order, so that wait never covers a store younger than one
+    // batch period. The outputs left in the ring are written out first. Then the problems
+    // that are not finished at their initial point are compacted into ring slots
+    // 0 .. nfresh - 1 with their column weights and gradient, and those that are (converged,
+    // non-finite, or max_iter = 0) are staged right after them and written out.
+    auto init_batch = [&]() {
+        // Take the batch's words into use here (the compiler waits for them before these
+        // empty statements), and keep every store below after them.
+#pragma unroll
+        for (int q = 0; q < NW; ++q) asm volatile("" : "+v"(raw[q])::"memory");
+        const int32_t r = (nxt << 6) + lane;
+        float Ti[16], ai[4], c0, c1, c2, g[4];
+        init_problem<DT>(raw, Ti, ai, c0, c1, c2, g);
+        flush(0, nfresh);
+        const float gmax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(g[0]), __builtin_fabsf(g[1])),
+                                           __builtin_fmaxf(__builtin_fabsf(g[2]), __builtin_fabsf(g[3])));
+        const bool nonfinite = __builtin_isnan(c0);  // beta is NaN exactly for poisoned inputs
+        const bool conv = gmax <= tol;
+        const bool valid = r < nrel;
+        const bool done = valid && (conv || nonfinite || max_iter == 0);
+        const bool fresh = valid && !done;
+        const uint64_t fm = __ballot(fresh), dm = __ballot(done);
+        const int nf = __popcll(fm);
+        if (fresh) {
+            v4f* sl = ring + __popcll(fm & below) * kSlot;
+            const Weights W = column_weights(Ti);
+            sl[0] = v4f{Ti[0], Ti[1], Ti[2], Ti[3]};
+            sl[1] = v4f{Ti[4], Ti[5], Ti[6], Ti[7]};
+            sl[2] = v4f{Ti[8], Ti[9], Ti[10], Ti[11]};
+            sl[3] = v4f{Ti[12], Ti[13], Ti[14], Ti[15]};
+            sl[4] = v4f{ai[0], ai[1], ai[2], ai[3]};
+            sl[5] = v4f{c0, c1, c2, __int_as_float(r)};
+            sl[6] = v4f{W.w01, W.w02, W.w03, W.w12};
+            sl[7] = v4f{W.w13, W.w23, g[0], g[1]};
+            sl[8] = v4f{g[2], __builtin_fmaxf(kLM * gmax, kLMFloor),
+                        g[0] * g[0] + g[1] * g[1] + g[2] * g[2] + g[3] * g[3], 0.f};
         }
-        __builtin_amdgcn_wave_barrier();
+        if (done)
+            stage_output(nf + __popcll(dm & below), Ti, ai, c0, c1, c2, r,
+                         nonfinite ? BIRKHOFF4_NON_FINITE : (conv ? 0 : BIRKHOFF4_NOT_CONVERGED));
+        flush(nf, __popcll(dm));
+        nfresh = nf;
+        icur = 0;
+        nxt = claim();
+        if (nxt < nbatch && (nxt << 6) + lane < nrel) load_raw<DT>(H, lo + (nxt << 6) + lane, raw);
     };
 
     for (;;) {
-        bool fin = false;
-        float T[16];
-        int status = 0;
         if (active) {
+            // Newton direction at the accepted point, with the step capped so that no two
+            // columns move apart by more than the cap (gauge-symmetric)
+            float d0, d1, d2;
+            newton_solve(Wa, ga0, ga1, ga2, lam, d0, d1, d2);
+            t = __builtin_fminf(t, kCap2 * rcp(__builtin_fmaxf(spread(d0, d1, d2), kTiny)));
             // trial point: accepted point + t d, reached from the current point
             const float s0 = __builtin_fmaf(t, d0, -o0), s1 = __builtin_fmaf(t, d1, -o1),
                         s2 = __builtin_fmaf(t, d2, -o2);
-            float lsum[4], g[4];
-            evaluate_inplace(U, s0, s1, s2, T, lsum, g);
-            const float gmax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(g[0]), __builtin_fabsf(g[1])),
-                                               __builtin_fmaxf(__builtin_fabsf(g[2]), __builtin_fabsf(g[3])));
-            const float gn2t = g[0] * g[0] + g[1] * g[1] + g[2] * g[2] + g[3] * g[3];
-            // f(trial) - f(accepted) = f(current) - f(accepted) + row-wise change (log2 units)
-            const float df = fofs + ((lsum[0] + lsum[1]) + (lsum[2] + lsum[3])) -
-                             ((s0 + s1) + s2);
-            // the trial becomes the current point
+            float l[4], g[4];
+            evaluate(T, s0, s1, s2, l, g);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                a[i] += lsum[i];
-            }
+            for (int i = 0; i < 4; ++i) a[i] += l[i];
             b0 += s0;
             b1 += s1;
             b2 += s2;
-            fofs = df;
             o0 += s0;
             o1 += s1;
             o2 += s2;
+            // f(trial) - f(accepted) = f(current) - f(accepted) + row-wise change (log2 units)
+            const float df = fofs + ((l[0] + l[1]) + (l[2] + l[3])) - ((s0 + s1) + s2);
+            fofs = df;
+            gsum += spread(s0, s1, s2);
+            ++cnt;
+            const float gmax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(g[0]), __builtin_fabsf(g[1])),
+                                               __builtin_fmaxf(__builtin_fabsf(g[2]), __builtin_fabsf(g[3])));
+            const float gn2t = g[0] * g[0] + g[1] * g[1] + g[2] * g[2] + g[3] * g[3];
             // directional derivative of f along d at the accepted point (log2 units)
             const float slope = ga0 * d0 + ga1 * d1 + ga2 * d2;
-            const bool accept = first || (df <= kArmijo * t * slope) ||
-                                (__builtin_fabsf(df) < kFNoise && gn2t < gn2);
-            if (!first) ++cnt;
+            const bool accept = (df <= kArmijo * t * slope) || (__builtin_fabsf(df) < kFNoise && gn2t < gn2);
             const int evals = cnt & 0xffff;
             const bool conv = accept && gmax <= tol;
-            fin = conv || nonfinite || evals >= max_iter;
-            if (!fin) {
-                if (accept) {
-                    if (!first) {
-                        const float dd = g[0] * d0 + g[1] * d1 + g[2] * d2;
-                        const int ts = cnt >> 16;  // the trial step doubles while full steps
-                        const bool grow = t >= 0.999f * __builtin_ldexpf(1.f, ts) && dd < 0.25f * slope;
-                        cnt = evals | ((grow ? (ts < kMaxExpandLog2 ? ts + 1 : ts) : 0) << 16);
+            if (!conv && evals < max_iter) {
+                // Entries that underflowed to zero can grow by at most the accumulated spread;
+                // before that could bring one within reach of fp32 resolution, re-derive every
+                // zero entry from H at the current point (they stay zero while still tiny).
+                if (gsum >= kReviveBits) {
+                    gsum = 0.f;
+                    float tmin = T[0];
+#pragma unroll
+                    for (int q = 1; q < 16; ++q) tmin = __builtin_fminf(tmin, T[q]);
+                    if (tmin == 0.f) {
+                        float h[16];
+                        load16<DT>(H, lo + rel, h);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float bj[4] = {b0, b1, b2, 0.f};
+#pragma unroll
+                            for (int j = 0; j < 4; ++j)
+                                if (T[4 * i + j] == 0.f)
+                                    T[4 * i + j] = ex2(__builtin_fmaf(h[4 * i + j], kLog2e, bj[j]) - a[i]);
+                        }
                     }
+                }
+                if (accept) {
+                    const float dd = g[0] * d0 + g[1] * d1 + g[2] * d2;
+                    const int ts = cnt >> 16;  // the trial step doubles while full steps
+                    const bool grow = t >= 0.999f * __builtin_ldexpf(1.f, ts) && dd < 0.25f * slope;
+                    cnt = evals | ((grow ? (ts < kMaxExpandLog2 ? ts + 1 : ts) : 0) << 16);
                     fofs = 0.f;
                     o0 = o1 = o2 = 0.f;
                     gn2 = gn2t;
@@ -460,94 +557,72 @@ __global__ __launch_bounds__(kFwdBlock) void newton_fwd_kernel(const void* __res
                     cnt = evals;
                     lam = __builtin_fminf(16.f * lam, kMaxShift);
                 }
-                newton_solve(Wa, ga0, ga1, ga2, lam, d0, d1, d2);
-                // cap the spread of the column shifts (d_4 = 0): the cap is gauge-symmetric, so
-                // two columns moving in opposite directions cannot jump twice as far
-                const float dm = __builtin_fmaxf(__builtin_fmaxf(d0, d1), __builtin_fmaxf(d2, 0.f)) -
-                                 __builtin_fminf(__builtin_fminf(d0, d1), __builtin_fminf(d2, 0.f));
-                t = __builtin_fminf(t, kCap2 * rcp(__builtin_fmaxf(dm, kTiny)));
-                first = false;
             } else {
-                if (!accept && !nonfinite) {
+                if (!accept) {
                     // max_iter reached on a rejected trial: return to the accepted point
-                    const float r0 = -o0, r1 = -o1, r2 = -o2;
-                    evaluate_inplace(U, r0, r1, r2, T, lsum, g);
+                    evaluate(T, -o0, -o1, -o2, l, g);
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        a[i] += lsum[i];
-                    }
-                    b0 += r0;
-                    b1 += r1;
-                    b2 += r2;
+                    for (int i = 0; i < 4; ++i) a[i] += l[i];
+                    b0 -= o0;
+                    b1 -= o1;
+                    b2 -= o2;
                 }
-                // a non-finite input was poisoned with NaN at load, so T and the dual are NaN
-                status = nonfinite ? BIRKHOFF4_NON_FINITE : (conv ? evals : BIRKHOFF4_NOT_CONVERGED);
+                status = conv ? evals : BIRKHOFF4_NOT_CONVERGED;
+                active = false;
+                want = true;
+                has_out = true;
             }
         }
-        // refill: finished lanes take the next problems of the wave's range in lane order,
-        // each from one ring slot, and leave their outputs in that slot
-        const uint64_t fm = __ballot(fin);
-        if (fm) {
-            const int k = __popcll(fm);
-            const int rank = __popcll(fm & below);
-            auto swap = [&](int sidx) {
-                v4f* sl = ring + sidx * kSlot;
-                const v4f u0 = sl[0], u1 = sl[1], u2 = sl[2], u3 = sl[3], av = sl[4], bv = sl[5];
-                sl[0] = v4f{T[0], T[1], T[2], T[3]};
-                sl[1] = v4f{T[4], T[5], T[6], T[7]};
-                sl[2] = v4f{T[8], T[9], T[10], T[11]};
-                sl[3] = v4f{T[12], T[13], T[14], T[15]};
-                if constexpr (WRITE_DUAL) {
-                    sl[4] = v4f{-a[0] * kLn2, -a[1] * kLn2, -a[2] * kLn2, -a[3] * kLn2};
-                    sl[5] = v4f{b0 * kLn2, b1 * kLn2, b2 * kLn2, b0 * 0.f};  // beta_4 = 0, NaN if poisoned
-                }
-                sl[6] = v4f{__int_as_float(rel), __int_as_float(status), 0.f, 0.f};
-                U[0] = u0.x; U[1] = u0.y; U[2] = u0.z; U[3] = u0.w;
-                U[4] = u1.x; U[5] = u1.y; U[6] = u1.z; U[7] = u1.w;
-                U[8] = u2.x; U[9] = u2.y; U[10] = u2.z; U[11] = u2.w;
-                U[12] = u3.x; U[13] = u3.y; U[14] = u3.z; U[15] = u3.w;
+        // Hand-off: every lane that wants a problem takes the next one of the ring and
+        // leaves its finished output in the slot; batches are initialised as the ring runs out.
+        uint64_t wm = __ballot(want);
+        while (wm != 0) {
+            const int k = __popcll(wm);
+            const int rank = __popcll(wm & below);
+            const int avail = nfresh - icur;
+            if (want && rank < avail) {
+                const v4f* sl = ring + (icur + rank) * kSlot;
+                const v4f r0 = sl[0], r1 = sl[1], r2 = sl[2], r3 = sl[3], av = sl[4], bv = sl[5],
+                          w0 = sl[6], w1 = sl[7], w2 = sl[8];
+                stage_output(icur + rank, T, a, b0, b1, b2, has_out ? rel : -1, status);
+                T[0] = r0.x; T[1] = r0.y; T[2] = r0.z; T[3] = r0.w;
+                T[4] = r1.x; T[5] = r1.y; T[6] = r1.z; T[7] = r1.w;
+                T[8] = r2.x; T[9] = r2.y; T[10] = r2.z; T[11] = r2.w;
+                T[12] = r3.x; T[13] = r3.y; T[14] = r3.z; T[15] = r3.w;
                 a[0] = av.x; a[1] = av.y; a[2] = av.z; a[3] = av.w;
-                b0 = bv.x;
-                b1 = bv.y;
-                b2 = bv.z;
-                rel = ibase + sidx;
-                active = rel < nrel;
-                nonfinite = __builtin_isnan(b0);
-                d0 = d1 = d2 = 0.f;
-                t = o0 = o1 = o2 = 0.f;
-                gn2 = fofs = 0.f;
+                b0 = bv.x; b1 = bv.y; b2 = bv.z;
+                rel = __float_as_int(bv.w);
+                Wa = Weights{w0.x, w0.y, w0.z, w0.w, w1.x, w1.y};
+                ga0 = w1.z; ga1 = w1.w; ga2 = w2.x;
+                lam = w2.y;
+                gn2 = w2.z;
+                t = 1.f;
+                o0 = o1 = o2 = 0.f;
+                fofs = gsum = 0.f;
                 cnt = 0;
-                first = true;
-            };
-            const int avail = 64 - icur;
-            if (fin && rank < avail) swap(icur + rank);
-            if (k > avail) {
-                // the batch ran out: write out every output still in the ring, then
-                // initialise the next batch (its raw words were loaded a batch ago) into
-                // the ring and start loading the one after it
-                for (int h = head; h < 64; h += 16) flush(h, (64 - h < 16) ? 64 - h : 16);
-                ibase = nxt << 6;  // past the range once the block's batches are all claimed
-                init_to_slot<DT>(raw, ring + lane * kSlot);
-                if (nxt < nbatch) {
-                    nxt = claim();
-                    if ((nxt << 6) + lane < nrel) load_raw<DT>(H, lo + (nxt << 6) + lane, raw);
-                }
-                if (fin && rank >= avail) swap(rank - avail);
-                icur = k - avail;
-                head = 0;
-            } else {
+                active = true;
+                want = false;
+                has_out = false;
+            }
+            if (k <= avail) {
                 icur += k;
+                break;
             }
-            while (icur - head >= 16) {
-                flush(head, 16);
-                head += 16;
+            icur = nfresh;
+            if (nxt >= nbatch) {
+                // nothing left to initialise: lanes still holding an output write it and idle
+                if (has_out)
+                    store_output<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, lo + rel, T, a, b0, b1, b2, status);
+                has_out = false;
+                want = false;
+                break;
             }
+            init_batch();
+            wm = __ballot(want);
         }
-        if (__ballot(active) == 0) {
-            if (icur > head) flush(head, icur - head);
-            break;
-        }
+        if (__ballot(active) == 0) break;
     }
+    flush(0, icur);
 }
 
 // ---------------------------------------------------------------------------
@@ -581,19 +656,24 @@ __global__ __launch_bounds__(256) void implicit_bwd_kernel(const float* __restri
         // Delta w = rhs, Delta = Hessian at T (Laplacian of W grounded at column 4).
         // Eliminating a node joins its neighbours j,k by W_jp W_pk / piv and moves its
         // flows onto the same edges, F_jk += (W_pk F_jp + W_jp F_pk) / piv, so every
-        // right-hand side stays a sum of antisymmetric edge flows.
+        // right-hand side stays a sum of antisymmetric edge flows. Each product is formed
+        // as (W_jp / piv) times a weight or flow: the ratio is at most one, so a product
+        // underflows only when its result does (two tiny weights multiplied first could
+        // flush to zero while the flows they pair with survive).
         const float piv0 = W01 + W02 + W03;
         const float i0 = piv0 > kPivMin ? rcp(piv0) : 0.f;
-        const float W12b = __builtin_fmaf(W01 * W02, i0, W12);
-        const float W13b = __builtin_fmaf(W01 * W03, i0, W13);
-        const float W23b = __builtin_fmaf(W02 * W03, i0, W23);
-        const float F12b = __builtin_fmaf(W01 * F02 - W02 * F01, i0, F12);
-        const float F13b = __builtin_fmaf(W01 * F03 - W03 * F01, i0, F13);
-        const float F23b = __builtin_fmaf(W02 * F03 - W03 * F02, i0, F23);
+        const float f1 = W01 * i0, f2 = W02 * i0, f3 = W03 * i0;
+        const float W12b = __builtin_fmaf(f1, W02, W12);
+        const float W13b = __builtin_fmaf(f1, W03, W13);
+        const float W23b = __builtin_fmaf(f2, W03, W23);
+        const float F12b = __builtin_fmaf(f1, F02, __builtin_fmaf(-f2, F01, F12));
+        const float F13b = __builtin_fmaf(f1, F03, __builtin_fmaf(-f3, F01, F13));
+        const float F23b = __builtin_fmaf(f2, F03, __builtin_fmaf(-f3, F02, F23));
         const float piv1 = W12b + W13b;
         const float i1 = piv1 > kPivMin ? rcp(piv1) : 0.f;
-        const float W23c = __builtin_fmaf(W12b * W13b, i1, W23b);
-        const float F23c = __builtin_fmaf(W12b * F13b - W13b * F12b, i1, F23b);
+        const float g2 = W12b * i1, g3 = W13b * i1;
+        const float W23c = __builtin_fmaf(g2, W13b, W23b);
+        const float F23c = __builtin_fmaf(g2, F13b, __builtin_fmaf(-g3, F12b, F23b));
         const float w2 = W23c > kPivMin ? F23c * rcp(W23c) : 0.f;
         const float w1 = __builtin_fmaf(W12b, w2, F12b + F13b) * i1;
         const float w0 = __builtin_fmaf(W01, w1, __builtin_fmaf(W02, w2, (F01 + F02) + F03)) * i0;

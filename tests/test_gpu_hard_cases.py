@@ -7,7 +7,10 @@ generators (no stored inputs).
   gradient at the fp32 rounding floor drove weakly coupled columns (fixed by the floor
   of the Levenberg-Marquardt shift);
 * logunif_b2e25 #20482192: NaN in the backward from the reciprocal of a denormal pivot
-  (fixed by treating pivots <= 1e-30 as disconnected).
+  (fixed by treating pivots <= 1e-30 as disconnected);
+* logunif_b2e25 #21935421: with fp32 denormals flushed to zero, the backward's product of
+  two tiny weights (2e-19 x 3e-20) flushed while the matching flow term did not, and the
+  potentials blew up to 1e10 (fixed by forming the weight/pivot ratio before multiplying).
 """
 import numpy as np
 import pytest
@@ -25,7 +28,7 @@ CASES = {
     "mix_bf16_b2e24": [8108295, 9164907],
     "logunif_b2e25": [1548970, 5897705, 7163824, 8253668, 9546997, 9961632, 10235358, 10598146,
                       12182588, 12701271, 13677741, 16948698, 20482192, 22615900, 22955309,
-                      24646586, 28609303],
+                      21935421, 24646586, 28609303],
 }
 
 
@@ -70,6 +73,11 @@ def test_sigma50_two_million():
         f"max marginal={marg.max():.3e}")
     assert (itn >= 0).all() and marg.max() <= TOL_MARGINAL
     assert torch.isfinite(dH).all()
+    # rows and columns of every dH sum to zero (catches a blown-up potential anywhere)
+    d64 = dH.double()
+    sums = torch.maximum(d64.sum(dim=-1).abs().amax(dim=-1), d64.sum(dim=-2).abs().amax(dim=-1))
+    say(f"  max |row/col sums of dH| = {sums.max().item():.2e}")
+    assert sums.max().item() < 1e-4
     rng = np.random.default_rng(1)
     idx = np.unique(np.concatenate([rng.choice(len(H), 3000, replace=False), np.argsort(itn)[-200:],
                                     np.argsort(marg)[-200:]]))
