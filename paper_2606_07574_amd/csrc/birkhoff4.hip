@@ -8,10 +8,11 @@
 //
 // Mapping: one 4x4 problem per lane; all per-problem state lives in VGPRs. No
 // MFMA (the only products are six 4-long dot products per matrix), no global
-// atomics. Loads and stores are plain 16-byte vector accesses (non-temporal hints
-// measured slower on gfx950: the stores lose write combining). The implicit
-// kernel uses no LDS; the Newton kernel uses LDS for its ring of initialised
-// problems and for the batch counter its waves share.
+// atomics. Loads and stores are 16-byte vector accesses. The implicit kernel
+// streams wave-contiguous pieces with non-temporal hints and transposes them
+// through LDS; the Newton kernel uses LDS for its ring of initialised problems, for
+// staging its outputs and for the batch counter its waves share (non-temporal hints
+// measured slower there: its output writes depend on write combining in L2).
 //
 // Forward numerics (fp32; exponents in log2 units so that v_exp_f32 applies directly;
 // the library is compiled with fp32 denormals flushed to zero):
@@ -628,70 +629,149 @@ __global__ __launch_bounds__(kFwdBlock) void newton_fwd_kernel(const void* __res
 // ---------------------------------------------------------------------------
 // Backward (Sec. 4.2)
 // ---------------------------------------------------------------------------
+// dH for one problem from T (= P) and G (= dP): -D of eq. derivative, Sec. 4.2.
+__device__ __forceinline__ void implicit_vjp(const float T[16], const float G[16], float out[16]) {
+    // W_jk = sum_i T_ij T_ik; F_jk = sum_i T_ij T_ik (G_ij - G_ik): the right-hand
+    // side mu_c,j - sum_i T_ij mu_r,i of eq. derivative is sum_{k != j} F_jk.
+    float W01 = 0.f, W02 = 0.f, W03 = 0.f, W12 = 0.f, W13 = 0.f, W23 = 0.f;
+    float F01 = 0.f, F02 = 0.f, F03 = 0.f, F12 = 0.f, F13 = 0.f, F23 = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float t0 = T[4 * i], t1 = T[4 * i + 1], t2 = T[4 * i + 2], t3 = T[4 * i + 3];
+        const float g0 = G[4 * i], g1 = G[4 * i + 1], g2 = G[4 * i + 2], g3 = G[4 * i + 3];
+        float p;
+        p = t0 * t1; W01 += p; F01 = __builtin_fmaf(p, g0 - g1, F01);
+        p = t0 * t2; W02 += p; F02 = __builtin_fmaf(p, g0 - g2, F02);
+        p = t0 * t3; W03 += p; F03 = __builtin_fmaf(p, g0 - g3, F03);
+        p = t1 * t2; W12 += p; F12 = __builtin_fmaf(p, g1 - g2, F12);
+        p = t1 * t3; W13 += p; F13 = __builtin_fmaf(p, g1 - g3, F13);
+        p = t2 * t3; W23 += p; F23 = __builtin_fmaf(p, g2 - g3, F23);
+    }
+    // Delta w = rhs, Delta = Hessian at T (Laplacian of W grounded at column 4).
+    // Eliminating a node joins its neighbours j,k by W_jp W_pk / piv and moves its
+    // flows onto the same edges, F_jk += (W_pk F_jp + W_jp F_pk) / piv, so every
+    // right-hand side stays a sum of antisymmetric edge flows. Each product is formed
+    // as (W_jp / piv) times a weight or flow: the ratio is at most one, so a product
+    // underflows only when its result does (two tiny weights multiplied first could
+    // flush to zero while the flows they pair with survive).
+    const float piv0 = W01 + W02 + W03;
+    const float i0 = piv0 > kPivMin ? rcp(piv0) : 0.f;
+    const float f1 = W01 * i0, f2 = W02 * i0, f3 = W03 * i0;
+    const float W12b = __builtin_fmaf(f1, W02, W12);
+    const float W13b = __builtin_fmaf(f1, W03, W13);
+    const float W23b = __builtin_fmaf(f2, W03, W23);
+    const float F12b = __builtin_fmaf(f1, F02, __builtin_fmaf(-f2, F01, F12));
+    const float F13b = __builtin_fmaf(f1, F03, __builtin_fmaf(-f3, F01, F13));
+    const float F23b = __builtin_fmaf(f2, F03, __builtin_fmaf(-f3, F02, F23));
+    const float piv1 = W12b + W13b;
+    const float i1 = piv1 > kPivMin ? rcp(piv1) : 0.f;
+    const float g2 = W12b * i1, g3 = W13b * i1;
+    const float W23c = __builtin_fmaf(g2, W13b, W23b);
+    const float F23c = __builtin_fmaf(g2, F13b, __builtin_fmaf(-g3, F12b, F23b));
+    const float w2 = W23c > kPivMin ? F23c * rcp(W23c) : 0.f;
+    const float w1 = __builtin_fmaf(W12b, w2, F12b + F13b) * i1;
+    const float w0 = __builtin_fmaf(W01, w1, __builtin_fmaf(W02, w2, (F01 + F02) + F03)) * i0;
+    // dH = -D: dH_ij = T_ij (psi_ij - sum_k T_ik psi_ik), psi = G - 1 w^T, w_4 = 0
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float s0 = G[4 * i] - w0, s1 = G[4 * i + 1] - w1, s2 = G[4 * i + 2] - w2,
+                    s3 = G[4 * i + 3];
+        const float avg = __builtin_fmaf(T[4 * i], s0,
+                          __builtin_fmaf(T[4 * i + 1], s1,
+                          __builtin_fmaf(T[4 * i + 2], s2, T[4 * i + 3] * s3)));
+        out[4 * i + 0] = T[4 * i + 0] * (s0 - avg);
+        out[4 * i + 1] = T[4 * i + 1] * (s1 - avg);
+        out[4 * i + 2] = T[4 * i + 2] * (s2 - avg);
+        out[4 * i + 3] = T[4 * i + 3] * (s3 - avg);
+    }
+}
+
+// One 64-problem chunk per wave: P, dP and dH move between HBM and registers in
+// wave-contiguous 16-byte pieces (each load or store instruction covers 1 KB of
+// consecutive problems), transposed through a per-wave LDS buffer to one problem per
+// lane. Per-lane 64-byte records (four 16-byte accesses at a 64-byte stride) stream at
+// about half the rate. Every byte is touched once, so all accesses carry the
+// non-temporal hint (measured 11 % faster on MI355X than default caching).
+constexpr int kBwdBlock = 256;
+constexpr int kBwdWaves = kBwdBlock / 64;
+constexpr int kBwdStride = 5;  // v4f per problem in the LDS buffer (4 rows + 1 pad: no bank conflicts on reads)
+
 template <int DT>
-__global__ __launch_bounds__(256) void implicit_bwd_kernel(const float* __restrict__ P,
-                                                            const void* __restrict__ dP,
-                                                            float* __restrict__ dH, int64_t B) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
-    for (int64_t b = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; b < B; b += stride) {
+__global__ __launch_bounds__(kBwdBlock) void implicit_bwd_kernel(const float* __restrict__ P,
+                                                                  const void* __restrict__ dP,
+                                                                  float* __restrict__ dH, int64_t B) {
+    __shared__ v4f buf_all[kBwdWaves][64 * kBwdStride];
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+    v4f* const buf = buf_all[wv];
+    const v4f* P4 = reinterpret_cast<const v4f*>(P);
+    v4f* dH4 = reinterpret_cast<v4f*>(dH);
+    // slot of the 16-byte piece this lane moves in a coalesced access q: problem 16 q + lane / 4, row lane % 4
+    const int cpos = (lane >> 2) * kBwdStride + (lane & 3);
+    const int64_t nchunk = (B + 63) / 64;
+    for (int64_t c = static_cast<int64_t>(blockIdx.x) * kBwdWaves + wv; c < nchunk;
+         c += static_cast<int64_t>(gridDim.x) * kBwdWaves) {
+        const int64_t base = c * 64;
+        const int n = (B - base < 64) ? static_cast<int>(B - base) : 64;  // problems in this chunk
+        // issue every load of the chunk first
+        v4f pc[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int k = 64 * q + lane;  // 16-byte piece within the chunk
+            pc[q] = k < 4 * n ? __builtin_nontemporal_load(P4 + 4 * base + k) : v4f{0.f, 0.f, 0.f, 0.f};
+        }
+        constexpr int NG = (DT == BIRKHOFF4_BF16) ? 2 : 4;  // 16-byte pieces of dP per lane
+        constexpr int GP = (DT == BIRKHOFF4_BF16) ? 2 : 4;  // 16-byte pieces per problem
+        v4u gc[NG];
+        const v4u* G4 = reinterpret_cast<const v4u*>(dP);
+#pragma unroll
+        for (int q = 0; q < NG; ++q) {
+            const int k = 64 * q + lane;
+            gc[q] = k < GP * n ? __builtin_nontemporal_load(G4 + GP * base + k) : v4u{0u, 0u, 0u, 0u};
+        }
+        // P: pieces to one problem per lane
+#pragma unroll
+        for (int q = 0; q < 4; ++q) buf[16 * q * kBwdStride + cpos] = pc[q];
+        __builtin_amdgcn_wave_barrier();
         float T[16], G[16];
-        load16_f32(P, b, T);
-        load16<DT>(dP, b, G);
-        // W_jk = sum_i T_ij T_ik; F_jk = sum_i T_ij T_ik (G_ij - G_ik): the right-hand
-        // side mu_c,j - sum_i T_ij mu_r,i of eq. derivative is sum_{k != j} F_jk.
-        float W01 = 0.f, W02 = 0.f, W03 = 0.f, W12 = 0.f, W13 = 0.f, W23 = 0.f;
-        float F01 = 0.f, F02 = 0.f, F03 = 0.f, F12 = 0.f, F13 = 0.f, F23 = 0.f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float t0 = T[4 * i], t1 = T[4 * i + 1], t2 = T[4 * i + 2], t3 = T[4 * i + 3];
-            const float g0 = G[4 * i], g1 = G[4 * i + 1], g2 = G[4 * i + 2], g3 = G[4 * i + 3];
-            float p;
-            p = t0 * t1; W01 += p; F01 = __builtin_fmaf(p, g0 - g1, F01);
-            p = t0 * t2; W02 += p; F02 = __builtin_fmaf(p, g0 - g2, F02);
-            p = t0 * t3; W03 += p; F03 = __builtin_fmaf(p, g0 - g3, F03);
-            p = t1 * t2; W12 += p; F12 = __builtin_fmaf(p, g1 - g2, F12);
-            p = t1 * t3; W13 += p; F13 = __builtin_fmaf(p, g1 - g3, F13);
-            p = t2 * t3; W23 += p; F23 = __builtin_fmaf(p, g2 - g3, F23);
+        for (int r = 0; r < 4; ++r) {
+            const v4f t = buf[lane * kBwdStride + r];
+            T[4 * r + 0] = t.x; T[4 * r + 1] = t.y; T[4 * r + 2] = t.z; T[4 * r + 3] = t.w;
         }
-        // Delta w = rhs, Delta = Hessian at T (Laplacian of W grounded at column 4).
-        // Eliminating a node joins its neighbours j,k by W_jp W_pk / piv and moves its
-        // flows onto the same edges, F_jk += (W_pk F_jp + W_jp F_pk) / piv, so every
-        // right-hand side stays a sum of antisymmetric edge flows. Each product is formed
-        // as (W_jp / piv) times a weight or flow: the ratio is at most one, so a product
-        // underflows only when its result does (two tiny weights multiplied first could
-        // flush to zero while the flows they pair with survive).
-        const float piv0 = W01 + W02 + W03;
-        const float i0 = piv0 > kPivMin ? rcp(piv0) : 0.f;
-        const float f1 = W01 * i0, f2 = W02 * i0, f3 = W03 * i0;
-        const float W12b = __builtin_fmaf(f1, W02, W12);
-        const float W13b = __builtin_fmaf(f1, W03, W13);
-        const float W23b = __builtin_fmaf(f2, W03, W23);
-        const float F12b = __builtin_fmaf(f1, F02, __builtin_fmaf(-f2, F01, F12));
-        const float F13b = __builtin_fmaf(f1, F03, __builtin_fmaf(-f3, F01, F13));
-        const float F23b = __builtin_fmaf(f2, F03, __builtin_fmaf(-f3, F02, F23));
-        const float piv1 = W12b + W13b;
-        const float i1 = piv1 > kPivMin ? rcp(piv1) : 0.f;
-        const float g2 = W12b * i1, g3 = W13b * i1;
-        const float W23c = __builtin_fmaf(g2, W13b, W23b);
-        const float F23c = __builtin_fmaf(g2, F13b, __builtin_fmaf(-g3, F12b, F23b));
-        const float w2 = W23c > kPivMin ? F23c * rcp(W23c) : 0.f;
-        const float w1 = __builtin_fmaf(W12b, w2, F12b + F13b) * i1;
-        const float w0 = __builtin_fmaf(W01, w1, __builtin_fmaf(W02, w2, (F01 + F02) + F03)) * i0;
-        // dH = -D: dH_ij = T_ij (psi_ij - sum_k T_ik psi_ik), psi = G - 1 w^T, w_4 = 0
+        __builtin_amdgcn_wave_barrier();
+        // dP: the same, GP pieces per problem
+        v4u* bufu = reinterpret_cast<v4u*>(buf);
+#pragma unroll
+        for (int q = 0; q < NG; ++q) {
+            const int k = 64 * q + lane;
+            bufu[(k / GP) * kBwdStride + (k % GP)] = gc[q];
+        }
+        __builtin_amdgcn_wave_barrier();
+        {
+            uint32_t w[4 * GP];
+#pragma unroll
+            for (int r = 0; r < GP; ++r) {
+                const v4u u = bufu[lane * kBwdStride + r];
+                w[4 * r + 0] = u.x; w[4 * r + 1] = u.y; w[4 * r + 2] = u.z; w[4 * r + 3] = u.w;
+            }
+            decode_raw<DT>(w, G);
+        }
+        __builtin_amdgcn_wave_barrier();
         float out[16];
+        implicit_vjp(T, G, out);
+        // dH: one problem per lane to pieces
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float s0 = G[4 * i] - w0, s1 = G[4 * i + 1] - w1, s2 = G[4 * i + 2] - w2,
-                        s3 = G[4 * i + 3];
-            const float avg = __builtin_fmaf(T[4 * i], s0,
-                              __builtin_fmaf(T[4 * i + 1], s1,
-                              __builtin_fmaf(T[4 * i + 2], s2, T[4 * i + 3] * s3)));
-            out[4 * i + 0] = T[4 * i + 0] * (s0 - avg);
-            out[4 * i + 1] = T[4 * i + 1] * (s1 - avg);
-            out[4 * i + 2] = T[4 * i + 2] * (s2 - avg);
-            out[4 * i + 3] = T[4 * i + 3] * (s3 - avg);
+        for (int r = 0; r < 4; ++r)
+            buf[lane * kBwdStride + r] = v4f{out[4 * r], out[4 * r + 1], out[4 * r + 2], out[4 * r + 3]};
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int k = 64 * q + lane;
+            const v4f o = buf[16 * q * kBwdStride + cpos];
+            if (k < 4 * n) __builtin_nontemporal_store(o, dH4 + 4 * base + k);
         }
-        store16(dH, b, out);
+        __builtin_amdgcn_wave_barrier();
     }
 }
 
@@ -950,15 +1030,15 @@ int birkhoff4_bwd_ex(const float* P, const void* dP, int dp_dtype, float* dH, in
     if (misaligned(P) || misaligned(dP) || misaligned(dH)) return BIRKHOFF4_ERR_ALIGN;
     const size_t n = static_cast<size_t>(B) * 64, ng = static_cast<size_t>(B) * 16 * dtype_bytes(dp_dtype);
     if (overlaps(dH, n, P, n) || overlaps(dH, n, dP, ng)) return BIRKHOFF4_ERR_OVERLAP;
-    // One problem per thread: the resident waves then sweep one contiguous window of
-    // the arrays at a time, which streams about 12 % faster on MI355X than a
-    // grid-stride loop over a grid sized to the CUs. Larger batches loop.
-    const int64_t grid = (B + 255) / 256 < kMaxGrid ? (B + 255) / 256 : kMaxGrid;
+    // One 64-problem chunk per wave; batches beyond kMaxGrid blocks loop.
+    const int64_t chunks = (B + 63) / 64;
+    const int64_t want = (chunks + kBwdWaves - 1) / kBwdWaves;
+    const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
     if (dp_dtype == BIRKHOFF4_BF16)
-        hipLaunchKernelGGL(implicit_bwd_kernel<BIRKHOFF4_BF16>, dim3(static_cast<unsigned>(grid)), dim3(256),
+        hipLaunchKernelGGL(implicit_bwd_kernel<BIRKHOFF4_BF16>, dim3(static_cast<unsigned>(grid)), dim3(kBwdBlock),
                            0, stream, P, dP, dH, B);
     else
-        hipLaunchKernelGGL(implicit_bwd_kernel<BIRKHOFF4_F32>, dim3(static_cast<unsigned>(grid)), dim3(256),
+        hipLaunchKernelGGL(implicit_bwd_kernel<BIRKHOFF4_F32>, dim3(static_cast<unsigned>(grid)), dim3(kBwdBlock),
                            0, stream, P, dP, dH, B);
     return launch_status();
 }
