@@ -11,8 +11,9 @@
 // atomics. Loads and stores are 16-byte vector accesses. The implicit kernel
 // streams wave-contiguous pieces with non-temporal hints and transposes them
 // through LDS; the Newton kernel uses LDS for its ring of initialised problems, for
-// staging its outputs and for the batch counter its waves share (non-temporal hints
-// measured slower there: its output writes depend on write combining in L2).
+// staging its outputs and for the batch counter its waves share; it writes P
+// non-temporally and the 32-byte dual records through L2, where neighbouring records
+// that finish close in time merge into whole lines.
 //
 // Forward numerics (fp32; exponents in log2 units so that v_exp_f32 applies directly;
 // the library is compiled with fp32 denormals flushed to zero):
@@ -409,7 +410,9 @@ __global__ __launch_bounds__(kFwdBlock) void newton_fwd_kernel(const void* __res
                 ii = __float_as_int(sv.x);
                 st = __float_as_int(sv.y);
             }
-            if (ep < m && ip >= 0) reinterpret_cast<v4f*>(P)[4 * (lo + ip) + (lane & 3)] = pv;
+            // P bypasses L2 retention (non-temporal): the partial dual lines then stay in
+            // L2 long enough to merge with their neighbours' halves
+            if (ep < m && ip >= 0) __builtin_nontemporal_store(pv, reinterpret_cast<v4f*>(P) + 4 * (lo + ip) + (lane & 3));
             if constexpr (WRITE_DUAL)
                 if (ed < m && id >= 0) reinterpret_cast<v4f*>(dual)[2 * (lo + id) + (lane & 1)] = dv;
             if constexpr (WRITE_ITERS)
