@@ -47,7 +47,17 @@ enum {
     BIRKHOFF4_ERR_OVERLAP = -7,   /* an output overlaps another argument */
     BIRKHOFF4_ERR_STEPS = -8,     /* Sinkhorn step count out of range */
     BIRKHOFF4_ERR_DEVICE = -9,    /* HIP device query failed */
-    BIRKHOFF4_ERR_LAUNCH = -10    /* kernel launch failed (hipGetLastError) */
+    BIRKHOFF4_ERR_LAUNCH = -10,   /* kernel launch failed (hipGetLastError) */
+    BIRKHOFF4_ERR_VARIANT = -11   /* unknown forward variant */
+};
+
+/* Forward kernel variants (birkhoff4_fwd_ex2). Both compute the same projection to the
+ * same tolerance; they differ in how problems map to lanes, so iterates and step counts may
+ * differ at the rounding level. */
+enum {
+    BIRKHOFF4_AUTO = 0,       /* LATENCY for B <= 32768, else THROUGHPUT */
+    BIRKHOFF4_THROUGHPUT = 1, /* one problem per lane, with lane-level refill */
+    BIRKHOFF4_LATENCY = 2     /* four lanes per problem (one row each), no refill */
 };
 
 /* Storage dtypes for inputs (outputs are always fp32; compute is always fp32). */
@@ -101,6 +111,14 @@ int birkhoff4_bwd(const float* P, const float* dual, const float* dP, float* dH,
  * Other arguments as in birkhoff4_fwd. */
 int birkhoff4_fwd_ex(const void* H, int h_dtype, float* P, float* dual, int32_t* iters,
                      int64_t B, float tol, int max_iter, hipStream_t stream);
+
+/* Forward with an explicit kernel variant (BIRKHOFF4_AUTO, _THROUGHPUT or _LATENCY); other
+ * arguments as in birkhoff4_fwd_ex, which is this call with BIRKHOFF4_AUTO. The latency
+ * variant splits each problem's row-wise work over four lanes (the paper's Sec. 3.3 also
+ * spreads one matrix over several lanes), which shortens the serial chain of a Newton step
+ * for batches too small to fill the GPU; returns BIRKHOFF4_ERR_VARIANT for other values. */
+int birkhoff4_fwd_ex2(const void* H, int h_dtype, float* P, float* dual, int32_t* iters,
+                      int64_t B, float tol, int max_iter, int variant, hipStream_t stream);
 
 /* Backward with a storage dtype for dP (BIRKHOFF4_F32 or BIRKHOFF4_BF16). */
 int birkhoff4_bwd_ex(const float* P, const void* dP, int dp_dtype, float* dH, int64_t B,

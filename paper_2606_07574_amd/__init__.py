@@ -22,6 +22,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libbirkhoff4.so")
 
 F32, BF16 = 0, 1
+AUTO, THROUGHPUT, LATENCY = 0, 1, 2
 NOT_CONVERGED, NON_FINITE = -1, -2
 DEFAULT_TOL = 1e-6
 DEFAULT_MAX_ITER = 64
@@ -47,6 +48,7 @@ def _load():
         "birkhoff4_fwd": [vp, vp, vp, i64, f32, i32, st],
         "birkhoff4_bwd": [vp, vp, vp, vp, i64, st],
         "birkhoff4_fwd_ex": [vp, i32, vp, vp, vp, i64, f32, i32, st],
+        "birkhoff4_fwd_ex2": [vp, i32, vp, vp, vp, i64, f32, i32, i32, st],
         "birkhoff4_bwd_ex": [vp, vp, i32, vp, i64, st],
         "birkhoff4_sk_fwd": [vp, i32, vp, i64, i32, st],
         "birkhoff4_sk_bwd": [vp, i32, vp, i32, vp, i64, i32, st],
@@ -100,11 +102,13 @@ def _ptr(t: torch.Tensor | None) -> int | None:
 
 
 def fwd(H: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER,
-        want_dual: bool = True, want_iters: bool = False, out: torch.Tensor | None = None):
+        want_dual: bool = True, want_iters: bool = False, out: torch.Tensor | None = None,
+        variant: int = AUTO):
     """Project exp(H) onto the Birkhoff polytope, per trailing 4x4 matrix.
 
     H: float32 or bfloat16 [..., 4, 4] on the GPU. Returns (P, dual, iters):
     P float32 like H, dual float32 [..., 8] or None, iters int32 [...] or None.
+    variant: AUTO, THROUGHPUT (one problem per lane) or LATENCY (four lanes per problem).
     """
     B = _batch(H, "H")
     lead = H.shape[:-2]
@@ -112,8 +116,8 @@ def fwd(H: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_I
     dual = torch.empty(*lead, 8, dtype=torch.float32, device=H.device) if want_dual else None
     iters = torch.empty(lead, dtype=torch.int32, device=H.device) if want_iters else None
     with torch.cuda.device(H.device):
-        _check(_load().birkhoff4_fwd_ex(_ptr(H), _dtype_code(H), _ptr(P), _ptr(dual), _ptr(iters),
-                                        B, float(tol), int(max_iter), _stream(H)))
+        _check(_load().birkhoff4_fwd_ex2(_ptr(H), _dtype_code(H), _ptr(P), _ptr(dual), _ptr(iters),
+                                         B, float(tol), int(max_iter), int(variant), _stream(H)))
     return P, dual, iters
 
 

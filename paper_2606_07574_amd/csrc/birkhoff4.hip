@@ -80,6 +80,8 @@ constexpr float kPivMin = 1e-30f;
 constexpr float kFltMin = 1.17549435e-38f;
 constexpr int kMaxSkSteps = 48;   // sk_bwd keeps (n+1) x 4 floats per lane in LDS
 constexpr int kMaxIterCap = 10000;
+// Batches up to this size take the four-lanes-per-problem forward by default.
+constexpr int64_t kLatencyMaxB = int64_t(1) << 15;
 constexpr int64_t kMaxGrid = int64_t(1) << 24;  // blocks of a streaming launch
 constexpr int kFwdBlock = 1024;  // one workgroup per CU: 16 waves, 4 per SIMD
 constexpr int kFwdWaves = kFwdBlock / 64;
@@ -630,6 +632,183 @@ __global__ __launch_bounds__(kFwdBlock) void newton_fwd_kernel(const void* __res
 }
 
 // ---------------------------------------------------------------------------
+// Forward, latency variant: four lanes per problem
+// ---------------------------------------------------------------------------
+// For small batches the one-problem-per-lane kernel is bound by the serial chain of one
+// Newton trial (~300 dependent instructions) times the slowest problem's trial count. Here
+// the four lanes of a quad hold one row each: the row-wise work of a trial is split four
+// ways, column sums and column weights are butterfly sums over the quad (DPP quad_perm, so
+// every lane of the quad gets bit-identical results), and the 3x3 solve and step control
+// run redundantly in the four lanes. There is no refill: a wave covers 16 problems and
+// runs until its slowest one is done, which is what a small batch pays anyway.
+
+// Sum over the four lanes of a quad, in the association ((x0 + x1) + (x2 + x3)); all four
+// lanes receive the same value. Contraction is off here: fused into a product computed by the
+// caller, the first add would become fma(own factors, partner's rounded product), which
+// differs between partner lanes, and the quad's replicated step control would split.
+__device__ __forceinline__ float qsum(float x) {
+#pragma clang fp contract(off)
+    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, true));  // (1,0,3,2)
+    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, true));  // (2,3,0,1)
+    return x;
+}
+
+// The value held by lane k of the quad, in every lane of the quad.
+template <int K>
+__device__ __forceinline__ float qget(float x) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), K | (K << 2) | (K << 4) | (K << 6), 0xF, 0xF, true));
+}
+
+// Row q of problem b (4 values).
+template <int DT>
+__device__ __forceinline__ void load_row(const void* base, int64_t b, int q, float h[4]) {
+    if constexpr (DT == BIRKHOFF4_BF16) {
+        const uint32_t* p = static_cast<const uint32_t*>(base) + 8 * b + 2 * q;
+        const uint2 w = *reinterpret_cast<const uint2*>(p);
+        h[0] = __uint_as_float(w.x << 16);
+        h[1] = __uint_as_float(w.x & 0xffff0000u);
+        h[2] = __uint_as_float(w.y << 16);
+        h[3] = __uint_as_float(w.y & 0xffff0000u);
+    } else {
+        const v4f r = reinterpret_cast<const v4f*>(base)[4 * b + q];
+        h[0] = r.x; h[1] = r.y; h[2] = r.z; h[3] = r.w;
+    }
+}
+
+template <int DT, bool WRITE_DUAL, bool WRITE_ITERS>
+__global__ __launch_bounds__(256) void newton_fwd_quad_kernel(const void* __restrict__ H,
+                                                               float* __restrict__ P,
+                                                               float* __restrict__ dual,
+                                                               int32_t* __restrict__ iters, int64_t B,
+                                                               float tol, int max_iter) {
+    const int64_t gt = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    const int64_t b = gt >> 2;       // this quad's problem
+    const int q = threadIdx.x & 3;   // this lane's row
+    const bool valid = b < B;        // uniform across the quad
+    // Initial point (column centring), eq. tij_stable in the log domain, as in init_problem.
+    float h[4] = {0.f, 0.f, 0.f, 0.f};
+    if (valid) load_row<DT>(H, b, q, h);
+    float cm[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cm[j] = 0.25f * kLog2e * qsum(h[j]);
+    const float hs = (cm[0] + cm[1]) + (cm[2] + cm[3]);
+    const float poison = hs - hs;  // 0, or NaN for a non-finite input anywhere in the matrix
+    float b0 = cm[3] - cm[0] + poison, b1 = cm[3] - cm[1] + poison, b2 = cm[3] - cm[2] + poison;
+    float T[4], a;
+    {
+        const float u0 = __builtin_fmaf(h[0], kLog2e, b0), u1 = __builtin_fmaf(h[1], kLog2e, b1),
+                    u2 = __builtin_fmaf(h[2], kLog2e, b2), u3 = __builtin_fmaf(h[3], kLog2e, poison);
+        const float m = __builtin_fmaxf(__builtin_fmaxf(u0, u1), __builtin_fmaxf(u2, u3)) + poison;
+        const float e0 = ex2(u0 - m), e1 = ex2(u1 - m), e2 = ex2(u2 - m), e3 = ex2(u3 - m);
+        const float sum = (e0 + e1) + (e2 + e3);
+        const float r = rcp(sum);
+        T[0] = e0 * r; T[1] = e1 * r; T[2] = e2 * r; T[3] = e3 * r;
+        a = m + lg2(sum);
+    }
+    float g[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) g[j] = qsum(T[j]) - 1.0f;
+    auto gmax_of = [](const float gg[4]) {
+        return __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(gg[0]), __builtin_fabsf(gg[1])),
+                               __builtin_fmaxf(__builtin_fabsf(gg[2]), __builtin_fabsf(gg[3])));
+    };
+    auto weights = [&]() {
+        return Weights{qsum(T[0] * T[1]), qsum(T[0] * T[2]), qsum(T[0] * T[3]),
+                       qsum(T[1] * T[2]), qsum(T[1] * T[3]), qsum(T[2] * T[3])};
+    };
+    float gmax = gmax_of(g);
+    const bool nonfinite = __builtin_isnan(b0);
+    bool active = valid && !(gmax <= tol) && !nonfinite && max_iter > 0;
+    int status = nonfinite ? BIRKHOFF4_NON_FINITE : (gmax <= tol ? 0 : BIRKHOFF4_NOT_CONVERGED);
+    Weights Wa = weights();
+    float ga0 = g[0], ga1 = g[1], ga2 = g[2];
+    float lam = __builtin_fmaxf(kLM * gmax, kLMFloor);
+    float gn2 = g[0] * g[0] + g[1] * g[1] + g[2] * g[2] + g[3] * g[3];
+    float t = 1.f, o0 = 0.f, o1 = 0.f, o2 = 0.f, fofs = 0.f, gsum = 0.f;
+    int cnt = 0;
+    while (__ballot(active)) {
+        if (active) {
+            float d0, d1, d2;
+            newton_solve(Wa, ga0, ga1, ga2, lam, d0, d1, d2);
+            t = __builtin_fminf(t, kCap2 * rcp(__builtin_fmaxf(spread(d0, d1, d2), kTiny)));
+            const float s0 = __builtin_fmaf(t, d0, -o0), s1 = __builtin_fmaf(t, d1, -o1),
+                        s2 = __builtin_fmaf(t, d2, -o2);
+            // trial evaluation of this lane's row (product form, as evaluate())
+            const float e0 = T[0] * ex2(s0), e1 = T[1] * ex2(s1), e2 = T[2] * ex2(s2), e3 = T[3];
+            const float sum = (e0 + e1) + (e2 + e3);
+            const float r = rcp(sum);
+            const float l = lg2(sum);
+            T[0] = e0 * r; T[1] = e1 * r; T[2] = e2 * r; T[3] = e3 * r;
+            float gt4[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) gt4[j] = qsum(T[j]) - 1.0f;
+            a += l;
+            b0 += s0; b1 += s1; b2 += s2;
+            o0 += s0; o1 += s1; o2 += s2;
+            const float df = fofs + qsum(l) - ((s0 + s1) + s2);
+            fofs = df;
+            gsum += spread(s0, s1, s2);
+            ++cnt;
+            const float gm = gmax_of(gt4);
+            const float gn2t = gt4[0] * gt4[0] + gt4[1] * gt4[1] + gt4[2] * gt4[2] + gt4[3] * gt4[3];
+            const float slope = ga0 * d0 + ga1 * d1 + ga2 * d2;
+            const bool accept = (df <= kArmijo * t * slope) || (__builtin_fabsf(df) < kFNoise && gn2t < gn2);
+            const int evals = cnt & 0xffff;
+            const bool conv = accept && gm <= tol;
+            if (!conv && evals < max_iter) {
+                if (gsum >= kReviveBits) {  // flushed entries: re-derive from H (per lane)
+                    gsum = 0.f;
+                    const float bj[4] = {b0, b1, b2, 0.f};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        if (T[j] == 0.f) T[j] = ex2(__builtin_fmaf(h[j], kLog2e, bj[j]) - a);
+                }
+                if (accept) {
+                    const float dd = gt4[0] * d0 + gt4[1] * d1 + gt4[2] * d2;
+                    const int ts = cnt >> 16;
+                    const bool grow = t >= 0.999f * __builtin_ldexpf(1.f, ts) && dd < 0.25f * slope;
+                    cnt = evals | ((grow ? (ts < kMaxExpandLog2 ? ts + 1 : ts) : 0) << 16);
+                    fofs = 0.f;
+                    o0 = o1 = o2 = 0.f;
+                    gn2 = gn2t;
+                    Wa = weights();
+                    ga0 = gt4[0]; ga1 = gt4[1]; ga2 = gt4[2];
+                    lam = __builtin_fmaxf(kLM * gm, kLMFloor);
+                    t = __builtin_ldexpf(1.f, cnt >> 16);
+                } else {
+                    t *= 0.5f;
+                    cnt = evals;
+                    lam = __builtin_fminf(16.f * lam, kMaxShift);
+                }
+            } else {
+                if (!accept) {  // max_iter reached on a rejected trial: back to the accepted point
+                    const float f0 = T[0] * ex2(-o0), f1 = T[1] * ex2(-o1), f2 = T[2] * ex2(-o2), f3 = T[3];
+                    const float s = (f0 + f1) + (f2 + f3);
+                    const float rr = rcp(s);
+                    T[0] = f0 * rr; T[1] = f1 * rr; T[2] = f2 * rr; T[3] = f3 * rr;
+                    a += lg2(s);
+                    b0 -= o0; b1 -= o1; b2 -= o2;
+                }
+                status = conv ? evals : BIRKHOFF4_NOT_CONVERGED;
+                active = false;
+            }
+        }
+    }
+    // outputs: lane q writes row q of P; lanes 0 and 1 write the dual record; lane 0 the status
+    if (valid) {
+        reinterpret_cast<v4f*>(P)[4 * b + q] = v4f{T[0], T[1], T[2], T[3]};
+        const float al0 = qget<0>(a), al1 = qget<1>(a), al2 = qget<2>(a), al3 = qget<3>(a);
+        if constexpr (WRITE_DUAL) {
+            v4f* dp = reinterpret_cast<v4f*>(dual) + 2 * b;
+            if (q == 0) dp[0] = v4f{-al0 * kLn2, -al1 * kLn2, -al2 * kLn2, -al3 * kLn2};
+            if (q == 1) dp[1] = v4f{b0 * kLn2, b1 * kLn2, b2 * kLn2, b0 * 0.f};
+        }
+        if constexpr (WRITE_ITERS)
+            if (q == 0) iters[b] = status;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Backward (Sec. 4.2)
 // ---------------------------------------------------------------------------
 // dH for one problem from T (= P) and G (= dP): -D of eq. derivative, Sec. 4.2.
@@ -978,6 +1157,26 @@ int launch_fwd(const void* H, float* P, float* dual, int32_t* iters, int64_t B, 
     return launch_status();
 }
 
+// Four lanes per problem, one problem per quad, 64 problems per 256-thread block.
+template <int DT, bool WD, bool WI>
+int launch_fwd_quad(const void* H, float* P, float* dual, int32_t* iters, int64_t B, float tol,
+                    int max_iter, hipStream_t stream) {
+    const int64_t blocks = (B + 63) / 64;
+    if (blocks > INT32_MAX) return BIRKHOFF4_ERR_SIZE;
+    hipLaunchKernelGGL((newton_fwd_quad_kernel<DT, WD, WI>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                       stream, H, P, dual, iters, B, tol, max_iter);
+    return launch_status();
+}
+
+template <int DT>
+int dispatch_fwd_quad(const void* H, float* P, float* dual, int32_t* iters, int64_t B, float tol,
+                      int max_iter, hipStream_t stream) {
+    if (dual && iters) return launch_fwd_quad<DT, true, true>(H, P, dual, iters, B, tol, max_iter, stream);
+    if (dual) return launch_fwd_quad<DT, true, false>(H, P, dual, iters, B, tol, max_iter, stream);
+    if (iters) return launch_fwd_quad<DT, false, true>(H, P, dual, iters, B, tol, max_iter, stream);
+    return launch_fwd_quad<DT, false, false>(H, P, dual, iters, B, tol, max_iter, stream);
+}
+
 template <int DT>
 int dispatch_fwd(const void* H, float* P, float* dual, int32_t* iters, int64_t B, float tol,
                  int max_iter, hipStream_t stream, int cus) {
@@ -997,8 +1196,9 @@ int64_t grid_for(int64_t B, int block, int cus, int per_cu) {
 
 extern "C" {
 
-int birkhoff4_fwd_ex(const void* H, int h_dtype, float* P, float* dual, int32_t* iters, int64_t B,
-                     float tol, int max_iter, hipStream_t stream) {
+int birkhoff4_fwd_ex2(const void* H, int h_dtype, float* P, float* dual, int32_t* iters, int64_t B,
+                      float tol, int max_iter, int variant, hipStream_t stream) {
+    if (variant < BIRKHOFF4_AUTO || variant > BIRKHOFF4_LATENCY) return BIRKHOFF4_ERR_VARIANT;
     if (B < 0 || B > (INT64_MAX / 64)) return BIRKHOFF4_ERR_SIZE;
     if (!dtype_ok(h_dtype)) return BIRKHOFF4_ERR_DTYPE;
     if (!(tol >= 0.f)) return BIRKHOFF4_ERR_TOL;
@@ -1012,6 +1212,11 @@ int birkhoff4_fwd_ex(const void* H, int h_dtype, float* P, float* dual, int32_t*
     if (overlaps(H, nh, P, np) || overlaps(H, nh, dual, nd) || overlaps(H, nh, iters, ni) ||
         overlaps(P, np, dual, nd) || overlaps(P, np, iters, ni) || overlaps(dual, nd, iters, ni))
         return BIRKHOFF4_ERR_OVERLAP;
+    if (variant == BIRKHOFF4_LATENCY || (variant == BIRKHOFF4_AUTO && B <= kLatencyMaxB)) {
+        if (h_dtype == BIRKHOFF4_BF16)
+            return dispatch_fwd_quad<BIRKHOFF4_BF16>(H, P, dual, iters, B, tol, max_iter, stream);
+        return dispatch_fwd_quad<BIRKHOFF4_F32>(H, P, dual, iters, B, tol, max_iter, stream);
+    }
     int cus = 0;
     if (int e = device_cus(&cus)) return e;
     if (h_dtype == BIRKHOFF4_BF16)
@@ -1019,9 +1224,14 @@ int birkhoff4_fwd_ex(const void* H, int h_dtype, float* P, float* dual, int32_t*
     return dispatch_fwd<BIRKHOFF4_F32>(H, P, dual, iters, B, tol, max_iter, stream, cus);
 }
 
+int birkhoff4_fwd_ex(const void* H, int h_dtype, float* P, float* dual, int32_t* iters, int64_t B,
+                     float tol, int max_iter, hipStream_t stream) {
+    return birkhoff4_fwd_ex2(H, h_dtype, P, dual, iters, B, tol, max_iter, BIRKHOFF4_AUTO, stream);
+}
+
 int birkhoff4_fwd(const float* H, float* P, float* dual, int64_t B, float tol, int max_iter,
                   hipStream_t stream) {
-    return birkhoff4_fwd_ex(H, BIRKHOFF4_F32, P, dual, nullptr, B, tol, max_iter, stream);
+    return birkhoff4_fwd_ex2(H, BIRKHOFF4_F32, P, dual, nullptr, B, tol, max_iter, BIRKHOFF4_AUTO, stream);
 }
 
 int birkhoff4_bwd_ex(const float* P, const void* dP, int dp_dtype, float* dH, int64_t B,
@@ -1117,6 +1327,7 @@ const char* birkhoff4_strerror(int code) {
         case BIRKHOFF4_ERR_STEPS: return "Sinkhorn step count must be in [1, 48]";
         case BIRKHOFF4_ERR_DEVICE: return "HIP device query failed";
         case BIRKHOFF4_ERR_LAUNCH: return "kernel launch failed";
+        case BIRKHOFF4_ERR_VARIANT: return "unknown forward variant";
         default: return "unknown error";
     }
 }

@@ -29,8 +29,12 @@ def bits_to_dev(bits: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to("cuda:0").view(torch.bfloat16)
 
 
-def gpu_fwd(Hd: torch.Tensor, tol=1e-6, max_iter=MAX_ITER):
-    P, dual, it = b4.fwd(Hd, tol, max_iter, want_dual=True, want_iters=True)
+VARIANTS = [b4.THROUGHPUT, b4.LATENCY]
+VARIANT_IDS = ["throughput", "latency"]
+
+
+def gpu_fwd(Hd: torch.Tensor, tol=1e-6, max_iter=MAX_ITER, variant=b4.AUTO):
+    P, dual, it = b4.fwd(Hd, tol, max_iter, want_dual=True, want_iters=True, variant=variant)
     torch.cuda.synchronize()
     return P, dual, it
 

@@ -18,6 +18,7 @@ HEADER = os.path.join(ROOT, "include", "birkhoff4.h")
 
 OK, ERR_NULL, ERR_SIZE, ERR_TOL, ERR_MAX_ITER, ERR_DTYPE, ERR_ALIGN, ERR_OVERLAP, ERR_STEPS = (
     0, -1, -2, -3, -4, -5, -6, -7, -8)
+ERR_VARIANT = -11
 
 A = 0x10000000        # fake, 16-byte aligned device addresses far apart
 Bp = 0x20000000
@@ -43,7 +44,7 @@ def test_every_declared_symbol_is_exported():
 def test_version_and_strerror():
     lib = b4.lib()
     assert lib.birkhoff4_version() >= 100
-    for code in range(-10, 1):
+    for code in range(-11, 1):
         assert lib.birkhoff4_strerror(code)
     assert lib.birkhoff4_strerror(-999) == b"unknown error"
 
@@ -70,6 +71,13 @@ def test_forward_argument_errors():
     assert fx(A, 1, Bp, C, C + 32 * 3, 10, 1e-6, 20, None) == ERR_OVERLAP  # iters inside dual
     # bf16 H occupies 32 B per matrix: P 32 B too early does overlap
     assert fx(A, 1, A + 32 * 9, None, None, 10, 1e-6, 20, None) == ERR_OVERLAP
+    f2 = lib.birkhoff4_fwd_ex2
+    for variant in (0, 1, 2):
+        assert f2(A, 0, Bp, C, None, 0, 1e-6, 20, variant, None) == OK
+        assert f2(A, 0, Bp, C, None, 10, -1.0, 20, variant, None) == ERR_TOL
+        assert f2(A, 0, A + 64 * 5, C, None, 10, 1e-6, 20, variant, None) == ERR_OVERLAP
+    assert f2(A, 0, Bp, C, None, 10, 1e-6, 20, 3, None) == ERR_VARIANT
+    assert f2(A, 0, Bp, C, None, 10, 1e-6, 20, -1, None) == ERR_VARIANT
 
 
 def test_backward_and_baseline_argument_errors():

@@ -19,8 +19,8 @@ import torch
 import oracle
 import paper_2606_07574_amd as b4
 import workloads
-from tests._gpu import (MAX_ITER, TOL_DH, TOL_MARGINAL, TOL_P, bits_to_dev, check_parity, gpu_fwd,
-                        marginal_linf_device, say, to_dev)
+from tests._gpu import (MAX_ITER, TOL_DH, TOL_MARGINAL, TOL_P, VARIANT_IDS, VARIANTS, bits_to_dev,
+                        check_parity, gpu_fwd, marginal_linf_device, say, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -43,14 +43,15 @@ def _gather(name, indices):
     return np.stack(H), np.stack(dP)
 
 
+@pytest.mark.parametrize("variant", VARIANTS, ids=VARIANT_IDS)
 @pytest.mark.parametrize("name", sorted(CASES))
-def test_regression_cases(name):
-    say(f"test: hard cases of {name}: {CASES[name]}")
+def test_regression_cases(name, variant):
+    say(f"test: hard cases of {name}: {CASES[name]}, variant {variant}")
     H, dP = _gather(name, CASES[name])
     # also run each one surrounded by easy neighbours, as inside a full wave
     Hw = np.concatenate([workloads.gauss(200, 1.0, seed=5)[0], H, workloads.gauss(200, 1.0, seed=6)[0]])
-    P, dual, it = gpu_fwd(to_dev(H))
-    Pw, _, itw = gpu_fwd(to_dev(Hw))
+    P, dual, it = gpu_fwd(to_dev(H), variant=variant)
+    Pw, _, itw = gpu_fwd(to_dev(Hw), variant=variant)
     dH = b4.bwd(P, to_dev(dP))
     torch.cuda.synchronize()
     itn = it.cpu().numpy()
@@ -60,11 +61,12 @@ def test_regression_cases(name):
     check_parity(H, P.cpu().numpy(), dual.cpu().numpy(), dP, dH.cpu().numpy(), name)
 
 
-def test_sigma50_two_million():
-    say("test: 2^21 matrices at sigma = 50")
+@pytest.mark.parametrize("variant", VARIANTS, ids=VARIANT_IDS)
+def test_sigma50_two_million(variant):
+    say(f"test: 2^21 matrices at sigma = 50, variant {variant}")
     H, dP = workloads.gauss(1 << 21, 50.0, seed=99)
     Hd = to_dev(H)
-    P, dual, it = gpu_fwd(Hd)
+    P, dual, it = gpu_fwd(Hd, variant=variant)
     dH = b4.bwd(P, to_dev(dP))
     torch.cuda.synchronize()
     itn = it.cpu().numpy()

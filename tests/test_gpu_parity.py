@@ -10,17 +10,20 @@ import torch
 import oracle
 import paper_2606_07574_amd as b4
 import workloads
-from tests._gpu import (MAX_ITER, TOL_DH, TOL_P, bits_to_dev, check_parity, dh_rel_err, gpu_fwd,
-                        say, to_dev)
+from tests._gpu import (MAX_ITER, TOL_DH, TOL_P, VARIANT_IDS, VARIANTS, bits_to_dev, check_parity,
+                        dh_rel_err, gpu_fwd, say, to_dev)
+
+variants = pytest.mark.parametrize("variant", VARIANTS, ids=VARIANT_IDS)
 
 pytestmark = pytest.mark.gpu
 
 
-def test_n01_b4096_fwd_bwd():
-    say("test: n01_b4096 full parity (fwd + bwd)")
+@variants
+def test_n01_b4096_fwd_bwd(variant):
+    say(f"test: n01_b4096 full parity (fwd + bwd), variant {variant}")
     ch = workloads.make_chunk(workloads.WORKLOADS["n01_b4096"], 0)
     Hd = to_dev(ch.H)
-    P, dual, it = gpu_fwd(Hd)
+    P, dual, it = gpu_fwd(Hd, variant=variant)
     dH = b4.bwd(P, to_dev(ch.dP))
     torch.cuda.synchronize()
     it = it.cpu().numpy()
@@ -29,22 +32,24 @@ def test_n01_b4096_fwd_bwd():
     check_parity(ch.H, P.cpu().numpy(), dual.cpu().numpy(), ch.dP, dH.cpu().numpy(), "n01_b4096")
 
 
-@pytest.mark.parametrize("B", [1, 2, 63, 64, 65, 255, 257, 1000, 4097, 20011])
-def test_ragged_batches(B):
-    say(f"test: ragged B={B}")
+@variants
+@pytest.mark.parametrize("B", [1, 2, 3, 15, 16, 17, 63, 64, 65, 255, 257, 1000, 4097, 20011])
+def test_ragged_batches(B, variant):
+    say(f"test: ragged B={B} variant {variant}")
     H, dP = workloads.gauss(B, 5.0, seed=B)
-    P, dual, it = gpu_fwd(to_dev(H))
+    P, dual, it = gpu_fwd(to_dev(H), variant=variant)
     dH = b4.bwd(P, to_dev(dP))
     torch.cuda.synchronize()
     assert (it.cpu().numpy() >= 0).all()
     check_parity(H, P.cpu().numpy(), dual.cpu().numpy(), dP, dH.cpu().numpy(), f"B={B}")
 
 
+@variants
 @pytest.mark.parametrize("sigma", [0.1, 1.0, 10.0, 20.0, 50.0])
-def test_scales(sigma):
-    say(f"test: gauss sigma={sigma}")
+def test_scales(sigma, variant):
+    say(f"test: gauss sigma={sigma} variant {variant}")
     H, dP = workloads.gauss(30000, sigma, seed=7)
-    P, dual, it = gpu_fwd(to_dev(H))
+    P, dual, it = gpu_fwd(to_dev(H), variant=variant)
     dH = b4.bwd(P, to_dev(dP))
     torch.cuda.synchronize()
     itn = it.cpu().numpy()
@@ -53,24 +58,26 @@ def test_scales(sigma):
     check_parity(H, P.cpu().numpy(), dual.cpu().numpy(), dP, dH.cpu().numpy(), f"sigma={sigma}")
 
 
-def test_near_permutation():
-    say("test: near permutations 20 Pi + 0.1 N and 60 Pi + N")
+@variants
+def test_near_permutation(variant):
+    say(f"test: near permutations 20 Pi + 0.1 N and 60 Pi + N, variant {variant}")
     for gap, noise in [(20.0, 0.1), (60.0, 1.0)]:
         H, dP = workloads.near_permutation(20000, gap, noise, seed=3)
-        P, dual, it = gpu_fwd(to_dev(H))
+        P, dual, it = gpu_fwd(to_dev(H), variant=variant)
         dH = b4.bwd(P, to_dev(dP))
         torch.cuda.synchronize()
         assert (it.cpu().numpy() >= 0).all()
         check_parity(H, P.cpu().numpy(), dual.cpu().numpy(), dP, dH.cpu().numpy(), f"perm gap={gap}")
 
 
-def test_bf16_mixture():
-    say("test: bf16 mixture (workload mix_bf16_b2e24, first 2^17 matrices)")
+@variants
+def test_bf16_mixture(variant):
+    say(f"test: bf16 mixture (workload mix_bf16_b2e24, first 2^17 matrices), variant {variant}")
     w = workloads.WORKLOADS["mix_bf16_b2e24"]
     ch = workloads.make_chunk(w, 0, B=1 << 17)
     Hd = bits_to_dev(ch.H_bits)
     dPd = bits_to_dev(ch.dP_bits)
-    P, dual, it = gpu_fwd(Hd)
+    P, dual, it = gpu_fwd(Hd, variant=variant)
     dH = b4.bwd(P, dPd)
     torch.cuda.synchronize()
     itn = it.cpu().numpy()
@@ -79,25 +86,27 @@ def test_bf16_mixture():
     check_parity(ch.H, P.cpu().numpy(), dual.cpu().numpy(), ch.dP, dH.cpu().numpy(), "bf16 mix")
 
 
-def test_fp32_and_bf16_paths_agree_on_same_values():
-    say("test: bf16 storage == fp32 storage of the same values")
+@variants
+def test_fp32_and_bf16_paths_agree_on_same_values(variant):
+    say(f"test: bf16 storage == fp32 storage of the same values, variant {variant}")
     w = workloads.WORKLOADS["mix_bf16_b2e24"]
     ch = workloads.make_chunk(w, 0, B=10000)
-    P1, d1, i1 = gpu_fwd(bits_to_dev(ch.H_bits))
-    P2, d2, i2 = gpu_fwd(to_dev(ch.H))
+    P1, d1, i1 = gpu_fwd(bits_to_dev(ch.H_bits), variant=variant)
+    P2, d2, i2 = gpu_fwd(to_dev(ch.H), variant=variant)
     assert torch.equal(P1, P2) and torch.equal(i1, i2)
     g1 = b4.bwd(P1, bits_to_dev(ch.dP_bits))
     g2 = b4.bwd(P1, to_dev(ch.dP))
     assert torch.equal(g1, g2)
 
 
-def test_permutation_equivariance_on_gpu():
-    say("test: row/column permutation equivariance")
+@variants
+def test_permutation_equivariance_on_gpu(variant):
+    say(f"test: row/column permutation equivariance, variant {variant}")
     H, dP = workloads.gauss(5000, 8.0, seed=11)
     rng = np.random.default_rng(0)
     pr, pc = rng.permutation(4), rng.permutation(4)
-    P, _, _ = gpu_fwd(to_dev(H))
-    Pp, _, _ = gpu_fwd(to_dev(np.ascontiguousarray(H[:, pr][:, :, pc])))
+    P, _, _ = gpu_fwd(to_dev(H), variant=variant)
+    Pp, _, _ = gpu_fwd(to_dev(np.ascontiguousarray(H[:, pr][:, :, pc])), variant=variant)
     P = P.cpu().numpy()
     Pp = Pp.cpu().numpy()
     assert np.abs(Pp - P[:, pr][:, :, pc]).max() < 2e-6
@@ -113,15 +122,16 @@ def test_autograd_function():
     assert dh_rel_err(Hd.grad.cpu().numpy().astype(np.float64), ref).max() <= TOL_DH
 
 
-def test_edge_cases():
-    say("test: edge cases (B=0, max_iter=0, tol=0, non-finite)")
+@variants
+def test_edge_cases(variant):
+    say(f"test: edge cases (B=0, max_iter=0, tol=0, non-finite), variant {variant}")
     Z = torch.zeros(0, 4, 4, device="cuda:0")
-    P, dual, it = b4.fwd(Z, want_iters=True)
+    P, dual, it = b4.fwd(Z, want_iters=True, variant=variant)
     assert P.shape == (0, 4, 4)
     assert b4.bwd(P, Z).shape == (0, 4, 4)
     # max_iter = 0 returns T at the initial point: row softmax after column centring
     H, _ = workloads.gauss(500, 4.0, seed=13)
-    P, dual, it = b4.fwd(to_dev(H), 1e-6, 0, want_iters=True)
+    P, dual, it = b4.fwd(to_dev(H), 1e-6, 0, want_iters=True, variant=variant)
     Hc = H.astype(np.float64) - H.astype(np.float64).mean(axis=1, keepdims=True)
     E = np.exp(Hc - Hc.max(axis=2, keepdims=True))
     ref = E / E.sum(axis=2, keepdims=True)
@@ -131,7 +141,7 @@ def test_edge_cases():
     assert ((itn == 0) == conv0).all() and ((itn == -1) == ~conv0).all()
     # tol = 0: a matrix stops only when its fp32 column sums are exactly one, else
     # it runs to max_iter and is reported not converged; the result is still valid
-    P, dual, it = b4.fwd(to_dev(H), 0.0, 7, want_iters=True)
+    P, dual, it = b4.fwd(to_dev(H), 0.0, 7, want_iters=True, variant=variant)
     itn = it.cpu().numpy()
     assert ((itn == -1) | ((itn >= 0) & (itn <= 7))).all() and (itn == -1).any()
     assert np.abs(P.cpu().numpy().sum(axis=2) - 1).max() < 1e-5
@@ -141,7 +151,7 @@ def test_edge_cases():
     H2[5, 1, 2] = np.nan
     H2[77, 0, 0] = np.inf
     H2[78, 3, 3] = -np.inf
-    P, dual, it = b4.fwd(to_dev(H2), want_iters=True)
+    P, dual, it = b4.fwd(to_dev(H2), want_iters=True, variant=variant)
     Pn, itn, dn = P.cpu().numpy(), it.cpu().numpy(), dual.cpu().numpy()
     bad = [5, 77, 78]
     assert (itn[bad] == -2).all() and np.isnan(Pn[bad]).all() and np.isnan(dn[bad]).all()
@@ -178,3 +188,15 @@ def test_sinkhorn_baseline(sigma):
     assert dh_rel_err(dH.cpu().numpy().astype(np.float64), dHr).max() <= TOL_DH
     # columns of the SK output sum to one after the final column step
     assert np.abs(P.cpu().numpy().astype(np.float64).sum(axis=1) - 1).max() < 2e-6
+
+
+def test_variants_agree():
+    say("test: throughput and latency variants give the same projection")
+    H, _ = workloads.gauss(50000, 6.0, seed=21)
+    Hd = to_dev(H)
+    P1, d1, i1 = gpu_fwd(Hd, variant=b4.THROUGHPUT)
+    P2, d2, i2 = gpu_fwd(Hd, variant=b4.LATENCY)
+    diff = (P1 - P2).abs().max().item()
+    say(f"  max |P_throughput - P_latency| = {diff:.2e}")
+    assert diff <= 2 * TOL_P
+    assert (i1 >= 0).all() and (i2 >= 0).all()
