@@ -138,6 +138,29 @@ int birkhoff4_sk_fwd(const void* H, int h_dtype, float* P, int64_t B, int n_step
 int birkhoff4_sk_bwd(const void* H, int h_dtype, const void* dP, int dp_dtype, float* dH,
                      int64_t B, int n_steps, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * n = 8 (the mHC layer with eight streams, Sec. 3.1): the same projection and
+ * gradient for 8 x 8 matrices, by Newton on the 7-dimensional reduced dual with the
+ * general gradient and Hessian (eq. grad_hess with a = b = 1, eta = 1) and the general
+ * implicit backward (eq. derivative). Return codes, dtypes and status words as above.
+ *
+ * H     [B][8][8] (h_dtype fp32 or bf16), row-major, device memory.
+ * P     [B][8][8] fp32 output: rows and columns sum to one within tol.
+ * dual  NULL or [B][16] fp32 output: (alpha_1..alpha_8, beta_1..beta_7, beta_8 = 0),
+ *       natural-log units, log P_ij = H_ij + alpha_i + beta_j.
+ * iters NULL or int32 [B] output: trial steps taken, BIRKHOFF4_NOT_CONVERGED or
+ *       BIRKHOFF4_NON_FINITE (that matrix's P and dual are then NaN).
+ * tol, max_iter as in birkhoff4_fwd. Buffers must not overlap; 16-byte alignment.
+ * Asynchronous on `stream`; nothing is allocated. */
+int birkhoff8_fwd(const void* H, int h_dtype, float* P, float* dual, int32_t* iters,
+                  int64_t B, float tol, int max_iter, hipStream_t stream);
+
+/* Backward for n = 8: dH [B][8][8] fp32 = dL/dH from P (the forward's output) and
+ * dP [B][8][8] (dp_dtype fp32 or bf16), eq. derivative with Delta the Hessian of the
+ * reduced dual at P. Rows and columns of dH sum to zero. dH must not overlap P or dP. */
+int birkhoff8_bwd(const float* P, const void* dP, int dp_dtype, float* dH, int64_t B,
+                  hipStream_t stream);
+
 /* Human-readable text for a return code (static storage). */
 const char* birkhoff4_strerror(int code);
 

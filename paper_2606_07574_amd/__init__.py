@@ -10,6 +10,7 @@ a GPU, the calls raise.
     dH = bwd(P, dP)                   # implicit differentiation (Sec. 4, eq. derivative)
     P = project(H)                    # autograd-aware: backward calls bwd
     P = sk_fwd(H, 20); dH = sk_bwd(H, dP, 20)   # Sinkhorn-Knopp baseline
+    P, dual = fwd8(H); dH = bwd8(P, dP); P = project8(H)   # the same for 8 x 8 matrices
 """
 from __future__ import annotations
 
@@ -52,6 +53,8 @@ def _load():
         "birkhoff4_bwd_ex": [vp, vp, i32, vp, i64, st],
         "birkhoff4_sk_fwd": [vp, i32, vp, i64, i32, st],
         "birkhoff4_sk_bwd": [vp, i32, vp, i32, vp, i64, i32, st],
+        "birkhoff8_fwd": [vp, i32, vp, vp, vp, i64, f32, i32, st],
+        "birkhoff8_bwd": [vp, vp, i32, vp, i64, st],
         "birkhoff4_version": [],
     }
     for name, args in sigs.items():
@@ -87,14 +90,14 @@ def _dtype_code(t: torch.Tensor) -> int:
     raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
 
 
-def _batch(t: torch.Tensor, name: str) -> int:
+def _batch(t: torch.Tensor, name: str, n: int = 4) -> int:
     if not t.is_cuda:
         raise Birkhoff4Error(f"{name} must be a GPU tensor (no CPU path)")
-    if t.dim() < 2 or tuple(t.shape[-2:]) != (4, 4):
-        raise ValueError(f"{name} must have shape [..., 4, 4], got {tuple(t.shape)}")
+    if t.dim() < 2 or tuple(t.shape[-2:]) != (n, n):
+        raise ValueError(f"{name} must have shape [..., {n}, {n}], got {tuple(t.shape)}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
-    return t.numel() // 16
+    return t.numel() // (n * n)
 
 
 def _ptr(t: torch.Tensor | None) -> int | None:
@@ -175,6 +178,54 @@ class Birkhoff4Fn(torch.autograd.Function):
 
 def project(H: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER) -> torch.Tensor:
     return Birkhoff4Fn.apply(H, tol, max_iter)
+
+
+def fwd8(H: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER,
+         want_dual: bool = True, want_iters: bool = False, out: torch.Tensor | None = None):
+    """fwd for trailing 8x8 matrices: returns (P, dual [..., 16] or None, iters or None)."""
+    B = _batch(H, "H", 8)
+    lead = H.shape[:-2]
+    P = torch.empty(H.shape, dtype=torch.float32, device=H.device) if out is None else out
+    dual = torch.empty(*lead, 16, dtype=torch.float32, device=H.device) if want_dual else None
+    iters = torch.empty(lead, dtype=torch.int32, device=H.device) if want_iters else None
+    with torch.cuda.device(H.device):
+        _check(_load().birkhoff8_fwd(_ptr(H), _dtype_code(H), _ptr(P), _ptr(dual), _ptr(iters),
+                                     B, float(tol), int(max_iter), _stream(H)))
+    return P, dual, iters
+
+
+def bwd8(P: torch.Tensor, dP: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+    """bwd for trailing 8x8 matrices."""
+    B = _batch(P, "P", 8)
+    if _batch(dP, "dP", 8) != B:
+        raise ValueError("P and dP batch sizes differ")
+    if P.dtype != torch.float32:
+        raise TypeError("P must be float32")
+    dH = torch.empty(P.shape, dtype=torch.float32, device=P.device) if out is None else out
+    with torch.cuda.device(P.device):
+        _check(_load().birkhoff8_bwd(_ptr(P), _ptr(dP), _dtype_code(dP), _ptr(dH), B, _stream(P)))
+    return dH
+
+
+class Birkhoff8Fn(torch.autograd.Function):
+    """Birkhoff4Fn for 8x8 matrices."""
+
+    @staticmethod
+    def forward(ctx, H, tol=DEFAULT_TOL, max_iter=DEFAULT_MAX_ITER):
+        P, _, _ = fwd8(H.contiguous(), tol, max_iter, want_dual=False)
+        ctx.save_for_backward(P)
+        ctx.in_dtype = H.dtype
+        return P
+
+    @staticmethod
+    def backward(ctx, dP):
+        (P,) = ctx.saved_tensors
+        dH = bwd8(P, dP.contiguous())
+        return dH.to(ctx.in_dtype), None, None
+
+
+def project8(H: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER) -> torch.Tensor:
+    return Birkhoff8Fn.apply(H, tol, max_iter)
 
 
 def version() -> int:

@@ -1093,6 +1093,402 @@ __global__ __launch_bounds__(64) void sk_bwd_kernel(const void* __restrict__ H,
 }
 
 // ---------------------------------------------------------------------------
+// n = 8 (Sec. 3.1 and eq. grad_hess / eq. derivative with n = m = 8): one problem per
+// lane. The forward is the 4 x 4 kernel's iteration written for 7 free potentials (the
+// row-softmax state in product form, trial steps capped in spread, Armijo with the
+// rounding-noise test, Levenberg-Marquardt shift, re-derivation of flushed entries),
+// without lane refill: a wave takes 64 consecutive problems and runs until the slowest
+// is done. The Newton system is the column Laplacian with 28 weights, grounded at
+// column 8 and solved by subtraction-free elimination of nodes 1..7.
+// ---------------------------------------------------------------------------
+constexpr int kB8Block = 256;
+constexpr int kB8Waves = kB8Block / 64;
+
+// Index of the weight of column pair (j, k), j < k < 8, in a packed array of 28.
+__host__ __device__ constexpr int pw8(int j, int k) { return j * 8 - (j * (j + 1)) / 2 + (k - j - 1); }
+
+// Row i (8 values) of problem b of an [B][8][8] array stored as fp32 or bf16.
+template <int DT>
+__device__ __forceinline__ void load_row8(const void* base, int64_t b, int i, float h[8]) {
+    if constexpr (DT == BIRKHOFF4_BF16) {
+        const v4u r = reinterpret_cast<const v4u*>(base)[8 * b + i];
+        const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            h[2 * k] = __uint_as_float(w[k] << 16);
+            h[2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
+        }
+    } else {
+        const v4f* p = reinterpret_cast<const v4f*>(base) + 16 * b + 2 * i;
+        const v4f r0 = p[0], r1 = p[1];
+        h[0] = r0.x; h[1] = r0.y; h[2] = r0.z; h[3] = r0.w;
+        h[4] = r1.x; h[5] = r1.y; h[6] = r1.z; h[7] = r1.w;
+    }
+}
+
+__device__ __forceinline__ float sum8(const float v[8]) {
+    return ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+}
+
+// Column sum j of T minus one (eq. c_g).
+__device__ __forceinline__ float colgrad8(const float T[64], int j) {
+    return (((T[j] + T[8 + j]) + (T[16 + j] + T[24 + j])) + ((T[32 + j] + T[40 + j]) + (T[48 + j] + T[56 + j]))) - 1.0f;
+}
+
+// W_jk = sum_i T_ij T_ik for the 28 column pairs.
+__device__ __forceinline__ void weights8(const float T[64], float W[28]) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int k = j + 1; k < 8; ++k) {
+            float s = T[j] * T[k];
+#pragma unroll
+            for (int i = 1; i < 8; ++i) s = __builtin_fmaf(T[8 * i + j], T[8 * i + k], s);
+            W[pw8(j, k)] = s;
+        }
+}
+
+// Newton direction in log2 units, d = -log2(e) (Lap(W) + lam I)^{-1} g over nodes 0..6
+// (node 7 is the ground; lam acts as a conductance from every node to it). Eliminating
+// node p joins nodes j, k by W_jp W_pk / piv_p and moves W_jp q_p / piv_p of its ground
+// conductance q_p onto node j, piv_p being node p's remaining conductance: every pivot
+// is a sum of non-negative terms. A node without conductance gets d = 0.
+__device__ __forceinline__ void newton_solve8(const float W[28], const float g[7], float lam, float d[7]) {
+    float A[28], q[7], r[7], ip[7];
+#pragma unroll
+    for (int k = 0; k < 28; ++k) A[k] = W[k];
+#pragma unroll
+    for (int j = 0; j < 7; ++j) {
+        q[j] = W[pw8(j, 7)] + lam;
+        r[j] = -kLog2e * g[j];
+    }
+#pragma unroll
+    for (int p = 0; p < 7; ++p) {
+        float piv = q[p];
+#pragma unroll
+        for (int k = p + 1; k < 7; ++k) piv += A[pw8(p, k)];
+        ip[p] = rcp(__builtin_fmaxf(piv, kTiny));
+#pragma unroll
+        for (int j = p + 1; j < 7; ++j) {
+            const float f = A[pw8(p, j)] * ip[p];
+#pragma unroll
+            for (int k = j + 1; k < 7; ++k) A[pw8(j, k)] = __builtin_fmaf(f, A[pw8(p, k)], A[pw8(j, k)]);
+            q[j] = __builtin_fmaf(f, q[p], q[j]);
+            r[j] = __builtin_fmaf(f, r[p], r[j]);
+        }
+    }
+#pragma unroll
+    for (int p = 6; p >= 0; --p) {
+        float s = r[p];
+#pragma unroll
+        for (int k = p + 1; k < 7; ++k) s = __builtin_fmaf(A[pw8(p, k)], d[k], s);
+        d[p] = s * ip[p];
+    }
+}
+
+// max_j v_j - min_j v_j over the 7 free shifts and v_8 = 0
+__device__ __forceinline__ float spread8(const float v[7]) {
+    float hi = 0.f, lo = 0.f;
+#pragma unroll
+    for (int j = 0; j < 7; ++j) {
+        hi = __builtin_fmaxf(hi, v[j]);
+        lo = __builtin_fminf(lo, v[j]);
+    }
+    return hi - lo;
+}
+
+// Trial evaluation in product form (the 4 x 4 kernel's evaluate for 8 columns): column
+// j < 7 of T is multiplied by 2^(s_j), rows are renormalised, l receives the log2 row
+// sums and g the column sums minus one.
+__device__ __forceinline__ void evaluate8(float T[64], const float s[7], float l[8], float g[8]) {
+    float S[7];
+#pragma unroll
+    for (int j = 0; j < 7; ++j) S[j] = ex2(s[j]);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        float e[8];
+#pragma unroll
+        for (int j = 0; j < 7; ++j) e[j] = T[8 * i + j] * S[j];
+        e[7] = T[8 * i + 7];
+        const float sum = sum8(e);
+        const float r = rcp(sum);
+        l[i] = lg2(sum);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) T[8 * i + j] = e[j] * r;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) g[j] = colgrad8(T, j);
+}
+
+// Initial point: beta_j = mean_i H_i8 - mean_i H_ij (log2 units), T the row softmax of
+// H log2(e) + 1 beta^T with the row maxima subtracted, a the log2 row normalisers,
+// g the column sums minus one. Returns false for a non-finite input (T, a, beta NaN).
+template <int DT>
+__device__ __forceinline__ bool init8(const void* H, int64_t b, float T[64], float a[8], float beta[7],
+                                      float g[8]) {
+    bool finite = true;
+    float cm[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) cm[j] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        float h[8];
+        load_row8<DT>(H, b, i, h);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            finite = finite && __builtin_isfinite(h[j]);
+            T[8 * i + j] = h[j] * kLog2e;
+            cm[j] += T[8 * i + j];
+        }
+    }
+    const float poison = finite ? 0.f : __builtin_nanf("");
+#pragma unroll
+    for (int j = 0; j < 7; ++j) beta[j] = 0.125f * (cm[7] - cm[j]) + poison;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        float u[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) u[j] = T[8 * i + j] + (j < 7 ? beta[j] : poison);
+        float m = u[0];
+#pragma unroll
+        for (int j = 1; j < 8; ++j) m = __builtin_fmaxf(m, u[j]);
+        m += poison;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) u[j] = ex2(u[j] - m);
+        const float sum = sum8(u);
+        const float r = rcp(sum);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) T[8 * i + j] = u[j] * r;
+        a[i] = m + lg2(sum);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) g[j] = colgrad8(T, j);
+    return finite;
+}
+
+template <bool WRITE_DUAL, bool WRITE_ITERS>
+__device__ __forceinline__ void store_output8(float* __restrict__ P, float* __restrict__ dual,
+                                              int32_t* __restrict__ iters, int64_t b, const float T[64],
+                                              const float a[8], const float beta[7], int status) {
+    v4f* pp = reinterpret_cast<v4f*>(P) + 16 * b;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) pp[q] = v4f{T[4 * q], T[4 * q + 1], T[4 * q + 2], T[4 * q + 3]};
+    if constexpr (WRITE_DUAL) {
+        v4f* dp = reinterpret_cast<v4f*>(dual) + 4 * b;
+        dp[0] = v4f{-a[0] * kLn2, -a[1] * kLn2, -a[2] * kLn2, -a[3] * kLn2};
+        dp[1] = v4f{-a[4] * kLn2, -a[5] * kLn2, -a[6] * kLn2, -a[7] * kLn2};
+        dp[2] = v4f{beta[0] * kLn2, beta[1] * kLn2, beta[2] * kLn2, beta[3] * kLn2};
+        dp[3] = v4f{beta[4] * kLn2, beta[5] * kLn2, beta[6] * kLn2, beta[0] * 0.f};  // beta_8 = 0
+    }
+    if constexpr (WRITE_ITERS) iters[b] = status;
+}
+
+template <int DT, bool WRITE_DUAL, bool WRITE_ITERS>
+__global__ __launch_bounds__(kB8Block) void newton8_fwd_kernel(const void* __restrict__ H, float* __restrict__ P,
+                                                                float* __restrict__ dual,
+                                                                int32_t* __restrict__ iters, int64_t B, float tol,
+                                                                int max_iter) {
+    const int lane = threadIdx.x & 63;
+    const int64_t nchunk = (B + 63) / 64;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kB8Waves;
+    for (int64_t c = static_cast<int64_t>(blockIdx.x) * kB8Waves + (threadIdx.x >> 6); c < nchunk; c += stride) {
+        const int64_t b = 64 * c + lane;
+        const bool valid = b < B;
+        float T[64], a[8], beta[7], g[8];
+        bool finite = true;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) g[j] = 0.f;
+        if (valid) finite = init8<DT>(H, b, T, a, beta, g);
+        float gmax0 = 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) gmax0 = __builtin_fmaxf(gmax0, __builtin_fabsf(g[j]));
+        int status = finite ? 0 : BIRKHOFF4_NON_FINITE;
+        bool active = valid && finite && !(gmax0 <= tol) && max_iter > 0;
+        if (valid && finite && !(gmax0 <= tol) && max_iter == 0) status = BIRKHOFF4_NOT_CONVERGED;
+
+        float W[28], ga[7], o[7];
+        float lam = __builtin_fmaxf(kLM * gmax0, kLMFloor);
+        float gn2 = 0.f, t = 1.f, fofs = 0.f, gsum = 0.f;
+        int cnt = 0;  // bits 0-15: trial steps; bits 16-18: log2 of the initial trial step
+        if (active) {
+            weights8(T, W);
+#pragma unroll
+            for (int j = 0; j < 7; ++j) ga[j] = g[j];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) gn2 = __builtin_fmaf(g[j], g[j], gn2);
+        }
+#pragma unroll
+        for (int j = 0; j < 7; ++j) o[j] = 0.f;
+
+        while (__ballot(active) != 0) {
+            if (active) {
+            float d[7], s[7], l[8];
+            newton_solve8(W, ga, lam, d);
+            t = __builtin_fminf(t, kCap2 * rcp(__builtin_fmaxf(spread8(d), kTiny)));
+#pragma unroll
+            for (int j = 0; j < 7; ++j) s[j] = __builtin_fmaf(t, d[j], -o[j]);
+            evaluate8(T, s, l, g);
+            float ls = 0.f, ss = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                a[i] += l[i];
+                ls += l[i];
+            }
+#pragma unroll
+            for (int j = 0; j < 7; ++j) {
+                beta[j] += s[j];
+                o[j] += s[j];
+                ss += s[j];
+            }
+            const float df = fofs + (ls - ss);
+            fofs = df;
+            gsum += spread8(s);
+            ++cnt;
+            float gmax = 0.f, gn2t = 0.f, slope = 0.f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                gmax = __builtin_fmaxf(gmax, __builtin_fabsf(g[j]));
+                gn2t = __builtin_fmaf(g[j], g[j], gn2t);
+            }
+#pragma unroll
+            for (int j = 0; j < 7; ++j) slope = __builtin_fmaf(ga[j], d[j], slope);
+            const bool accept = (df <= kArmijo * t * slope) || (__builtin_fabsf(df) < kFNoise && gn2t < gn2);
+            const int evals = cnt & 0xffff;
+            const bool conv = accept && gmax <= tol;
+            if (!conv && evals < max_iter) {
+                if (gsum >= kReviveBits) {
+                    gsum = 0.f;
+                    float tmin = T[0];
+#pragma unroll
+                    for (int q = 1; q < 64; ++q) tmin = __builtin_fminf(tmin, T[q]);
+                    if (tmin == 0.f) {
+#pragma unroll
+                        for (int i = 0; i < 8; ++i) {
+                            float h[8];
+                            load_row8<DT>(H, b, i, h);
+#pragma unroll
+                            for (int j = 0; j < 8; ++j)
+                                if (T[8 * i + j] == 0.f)
+                                    T[8 * i + j] = ex2(__builtin_fmaf(h[j], kLog2e, j < 7 ? beta[j] : 0.f) - a[i]);
+                        }
+                    }
+                }
+                if (accept) {
+                    float dd = 0.f;
+#pragma unroll
+                    for (int j = 0; j < 7; ++j) dd = __builtin_fmaf(g[j], d[j], dd);
+                    const int ts = cnt >> 16;
+                    const bool grow = t >= 0.999f * __builtin_ldexpf(1.f, ts) && dd < 0.25f * slope;
+                    cnt = evals | ((grow ? (ts < kMaxExpandLog2 ? ts + 1 : ts) : 0) << 16);
+                    fofs = 0.f;
+#pragma unroll
+                    for (int j = 0; j < 7; ++j) {
+                        o[j] = 0.f;
+                        ga[j] = g[j];
+                    }
+                    gn2 = gn2t;
+                    weights8(T, W);
+                    lam = __builtin_fmaxf(kLM * gmax, kLMFloor);
+                    t = __builtin_ldexpf(1.f, cnt >> 16);
+                } else {
+                    t *= 0.5f;
+                    cnt = evals;
+                    lam = __builtin_fminf(16.f * lam, kMaxShift);
+                }
+            } else {
+                if (!accept) {  // max_iter reached on a rejected trial: back to the accepted point
+                    float back[7];
+#pragma unroll
+                    for (int j = 0; j < 7; ++j) back[j] = -o[j];
+                    evaluate8(T, back, l, g);
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) a[i] += l[i];
+#pragma unroll
+                    for (int j = 0; j < 7; ++j) beta[j] -= o[j];
+                }
+                status = conv ? evals : BIRKHOFF4_NOT_CONVERGED;
+                active = false;
+            }
+            }
+        }
+        if (valid) store_output8<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, b, T, a, beta, status);
+    }
+}
+
+// Backward for n = 8 (eq. derivative, a = b = 1, eta = 1), the flow form of the 4 x 4
+// kernel: W_jk = sum_i T_ij T_ik and antisymmetric flows F_jk = sum_i T_ij T_ik
+// (G_ij - G_ik); eliminating node p adds W_jp W_pk / piv to edge (j, k) and
+// (W_pk F_jp + W_jp F_pk) / piv to its flow, piv = sum_{k > p} W_pk (ground = node 8);
+// back-substitution gives the potentials w (w_8 = 0), and dH_ij = T_ij (psi_ij -
+// sum_k T_ik psi_ik) with psi = G - 1 w^T. Products are formed ratio-first so that a
+// term underflows only when its value does.
+template <int DT>
+__global__ __launch_bounds__(kB8Block) void implicit8_bwd_kernel(const float* __restrict__ P,
+                                                                  const void* __restrict__ dP,
+                                                                  float* __restrict__ dH, int64_t B) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kB8Block;
+    for (int64_t b = static_cast<int64_t>(blockIdx.x) * kB8Block + threadIdx.x; b < B; b += stride) {
+        float T[64], W[28], F[28], w[8], ip[7];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) load_row8<BIRKHOFF4_F32>(P, b, i, T + 8 * i);
+        weights8(T, W);
+#pragma unroll
+        for (int k = 0; k < 28; ++k) F[k] = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            float G[8];
+            load_row8<DT>(dP, b, i, G);
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+#pragma unroll
+                for (int k = j + 1; k < 8; ++k)
+                    F[pw8(j, k)] = __builtin_fmaf(T[8 * i + j] * T[8 * i + k], G[j] - G[k], F[pw8(j, k)]);
+        }
+#pragma unroll
+        for (int p = 0; p < 7; ++p) {
+            float piv = 0.f;
+#pragma unroll
+            for (int k = p + 1; k < 8; ++k) piv += W[pw8(p, k)];
+            ip[p] = (piv > kPivMin) ? rcp(piv) : 0.f;
+#pragma unroll
+            for (int j = p + 1; j < 8; ++j)
+#pragma unroll
+                for (int k = j + 1; k < 8; ++k) {
+                    const float fj = W[pw8(p, j)] * ip[p], fk = W[pw8(p, k)] * ip[p];
+                    // F_jp = -F_pj, F_pk as stored (p < j < k)
+                    F[pw8(j, k)] = __builtin_fmaf(fj, F[pw8(p, k)], __builtin_fmaf(-fk, F[pw8(p, j)], F[pw8(j, k)]));
+                    W[pw8(j, k)] = __builtin_fmaf(fj, W[pw8(p, k)], W[pw8(j, k)]);
+                }
+        }
+        w[7] = 0.f;
+#pragma unroll
+        for (int p = 6; p >= 0; --p) {
+            float s = 0.f;
+#pragma unroll
+            for (int k = p + 1; k < 8; ++k) s += __builtin_fmaf(W[pw8(p, k)], w[k], F[pw8(p, k)]);
+            w[p] = s * ip[p];
+        }
+        v4f* out = reinterpret_cast<v4f*>(dH) + 16 * b;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            float G[8], psi[8];
+            load_row8<DT>(dP, b, i, G);
+            float mu = 0.f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                psi[j] = G[j] - w[j];
+                mu = __builtin_fmaf(T[8 * i + j], psi[j], mu);
+            }
+            float o[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) o[j] = T[8 * i + j] * (psi[j] - mu);
+            out[2 * i] = v4f{o[0], o[1], o[2], o[3]};
+            out[2 * i + 1] = v4f{o[4], o[5], o[6], o[7]};
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
 constexpr int kMaxDevices = 64;
@@ -1186,6 +1582,28 @@ int dispatch_fwd(const void* H, float* P, float* dual, int32_t* iters, int64_t B
     return launch_fwd<DT, false, false>(H, P, dual, iters, B, tol, max_iter, stream, cus);
 }
 
+// n = 8: one 64-problem chunk per wave, blocks scheduled by the hardware; batches beyond
+// kMaxGrid blocks loop.
+template <int DT, bool WD, bool WI>
+int launch_fwd8(const void* H, float* P, float* dual, int32_t* iters, int64_t B, float tol, int max_iter,
+                hipStream_t stream) {
+    const int64_t chunks = (B + 63) / 64;
+    const int64_t want = (chunks + kB8Waves - 1) / kB8Waves;
+    const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
+    hipLaunchKernelGGL((newton8_fwd_kernel<DT, WD, WI>), dim3(static_cast<unsigned>(grid)), dim3(kB8Block), 0,
+                       stream, H, P, dual, iters, B, tol, max_iter);
+    return launch_status();
+}
+
+template <int DT>
+int dispatch_fwd8(const void* H, float* P, float* dual, int32_t* iters, int64_t B, float tol, int max_iter,
+                  hipStream_t stream) {
+    if (dual && iters) return launch_fwd8<DT, true, true>(H, P, dual, iters, B, tol, max_iter, stream);
+    if (dual) return launch_fwd8<DT, true, false>(H, P, dual, iters, B, tol, max_iter, stream);
+    if (iters) return launch_fwd8<DT, false, true>(H, P, dual, iters, B, tol, max_iter, stream);
+    return launch_fwd8<DT, false, false>(H, P, dual, iters, B, tol, max_iter, stream);
+}
+
 int64_t grid_for(int64_t B, int block, int cus, int per_cu) {
     int64_t blocks = (B + block - 1) / block;
     const int64_t cap = static_cast<int64_t>(cus) * per_cu;
@@ -1232,6 +1650,44 @@ int birkhoff4_fwd_ex(const void* H, int h_dtype, float* P, float* dual, int32_t*
 int birkhoff4_fwd(const float* H, float* P, float* dual, int64_t B, float tol, int max_iter,
                   hipStream_t stream) {
     return birkhoff4_fwd_ex2(H, BIRKHOFF4_F32, P, dual, nullptr, B, tol, max_iter, BIRKHOFF4_AUTO, stream);
+}
+
+int birkhoff8_fwd(const void* H, int h_dtype, float* P, float* dual, int32_t* iters, int64_t B, float tol,
+                  int max_iter, hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 256)) return BIRKHOFF4_ERR_SIZE;
+    if (!dtype_ok(h_dtype)) return BIRKHOFF4_ERR_DTYPE;
+    if (!(tol >= 0.f)) return BIRKHOFF4_ERR_TOL;
+    if (max_iter < 0 || max_iter > kMaxIterCap) return BIRKHOFF4_ERR_MAX_ITER;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!H || !P) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(H) || misaligned(P) || misaligned(dual) || misaligned(iters)) return BIRKHOFF4_ERR_ALIGN;
+    const size_t nh = static_cast<size_t>(B) * 64 * dtype_bytes(h_dtype);
+    const size_t np = static_cast<size_t>(B) * 256, nd = dual ? static_cast<size_t>(B) * 64 : 0,
+                 ni = iters ? static_cast<size_t>(B) * 4 : 0;
+    if (overlaps(H, nh, P, np) || overlaps(H, nh, dual, nd) || overlaps(H, nh, iters, ni) ||
+        overlaps(P, np, dual, nd) || overlaps(P, np, iters, ni) || overlaps(dual, nd, iters, ni))
+        return BIRKHOFF4_ERR_OVERLAP;
+    if (h_dtype == BIRKHOFF4_BF16) return dispatch_fwd8<BIRKHOFF4_BF16>(H, P, dual, iters, B, tol, max_iter, stream);
+    return dispatch_fwd8<BIRKHOFF4_F32>(H, P, dual, iters, B, tol, max_iter, stream);
+}
+
+int birkhoff8_bwd(const float* P, const void* dP, int dp_dtype, float* dH, int64_t B, hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 256)) return BIRKHOFF4_ERR_SIZE;
+    if (!dtype_ok(dp_dtype)) return BIRKHOFF4_ERR_DTYPE;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!P || !dP || !dH) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(P) || misaligned(dP) || misaligned(dH)) return BIRKHOFF4_ERR_ALIGN;
+    const size_t n = static_cast<size_t>(B) * 256, ng = static_cast<size_t>(B) * 64 * dtype_bytes(dp_dtype);
+    if (overlaps(dH, n, P, n) || overlaps(dH, n, dP, ng)) return BIRKHOFF4_ERR_OVERLAP;
+    const int64_t want = (B + kB8Block - 1) / kB8Block;
+    const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
+    if (dp_dtype == BIRKHOFF4_BF16)
+        hipLaunchKernelGGL(implicit8_bwd_kernel<BIRKHOFF4_BF16>, dim3(static_cast<unsigned>(grid)),
+                           dim3(kB8Block), 0, stream, P, dP, dH, B);
+    else
+        hipLaunchKernelGGL(implicit8_bwd_kernel<BIRKHOFF4_F32>, dim3(static_cast<unsigned>(grid)),
+                           dim3(kB8Block), 0, stream, P, dP, dH, B);
+    return launch_status();
 }
 
 int birkhoff4_bwd_ex(const float* P, const void* dP, int dp_dtype, float* dH, int64_t B,

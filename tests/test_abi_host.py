@@ -29,14 +29,14 @@ D = 0x40000000
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(birkhoff4_\w+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(birkhoff[48]_\w+)\s*\(", text)))
 
 
 def test_every_declared_symbol_is_exported():
     lib = ctypes.CDLL(b4.LIB_PATH)
     names = declared_functions()
     assert {"birkhoff4_fwd", "birkhoff4_bwd", "birkhoff4_fwd_ex", "birkhoff4_bwd_ex",
-            "birkhoff4_sk_fwd", "birkhoff4_sk_bwd"} <= set(names)
+            "birkhoff4_sk_fwd", "birkhoff4_sk_bwd", "birkhoff8_fwd", "birkhoff8_bwd"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
 
@@ -78,6 +78,27 @@ def test_forward_argument_errors():
         assert f2(A, 0, A + 64 * 5, C, None, 10, 1e-6, 20, variant, None) == ERR_OVERLAP
     assert f2(A, 0, Bp, C, None, 10, 1e-6, 20, 3, None) == ERR_VARIANT
     assert f2(A, 0, Bp, C, None, 10, 1e-6, 20, -1, None) == ERR_VARIANT
+
+
+def test_n8_argument_errors():
+    lib = b4.lib()
+    f = lib.birkhoff8_fwd
+    assert f(A, 0, Bp, C, None, 0, 1e-6, 20, None) == OK
+    assert f(A, 0, Bp, C, None, -1, 1e-6, 20, None) == ERR_SIZE
+    assert f(None, 0, Bp, C, None, 10, 1e-6, 20, None) == ERR_NULL
+    assert f(A, 2, Bp, C, None, 10, 1e-6, 20, None) == ERR_DTYPE
+    assert f(A, 0, Bp, C, None, 10, -1.0, 20, None) == ERR_TOL
+    assert f(A, 0, Bp, C, None, 10, 1e-6, 10001, None) == ERR_MAX_ITER
+    assert f(A, 0, Bp + 4, C, None, 10, 1e-6, 20, None) == ERR_ALIGN
+    assert f(A, 0, A + 256 * 9, C, None, 10, 1e-6, 20, None) == ERR_OVERLAP   # P inside H
+    assert f(A, 1, A + 128 * 9, None, None, 10, 1e-6, 20, None) == ERR_OVERLAP  # bf16 H: 128 B each
+    assert f(A, 0, Bp, Bp + 256 * 9, None, 10, 1e-6, 20, None) == ERR_OVERLAP  # dual inside P
+    g = lib.birkhoff8_bwd
+    assert g(A, Bp, 0, C, 0, None) == OK
+    assert g(A, Bp, 0, C, -3, None) == ERR_SIZE
+    assert g(A, None, 0, C, 3, None) == ERR_NULL
+    assert g(A, Bp, 5, C, 3, None) == ERR_DTYPE
+    assert g(A, Bp, 0, A + 256, 3, None) == ERR_OVERLAP
 
 
 def test_backward_and_baseline_argument_errors():
