@@ -27,6 +27,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "4×4 Birkhoff projections/sec fwd+bwd at B=2^24 (fp32); % HBM peak; max marginal err"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+# VALU issue peak without packed fp32: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz lane-instructions/s
+VALU_PEAK_T = 256 * 4 * 16 * 2.4e9 / 1e12
 SRC = os.path.join(ROOT, "paper_2606_07574_amd", "csrc", "birkhoff4.hip")
 
 
@@ -36,6 +38,20 @@ def log(*a):
 
 def in_bytes(dtype_is_bf16: bool) -> int:
     return 32 if dtype_is_bf16 else 64
+
+
+def valu_from_profiles(workload: str, kernel: str):
+    """VALU lane-instructions per launch counted by rocprofv3 (SQ_INSTS_VALU x 64) for the
+    current kernel source (profiles/valu_<workload>.md), else None."""
+    path = os.path.join(ROOT, "profiles", f"valu_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"source_sha256:\s*([0-9a-f]{64})", text)
+    if not m or m.group(1) != hashlib.sha256(open(SRC, "rb").read()).hexdigest():
+        return None
+    mm = re.search(rf"{kernel}_valu_lane_instr_per_launch:\s*([0-9.eE+]+)", text)
+    return float(mm.group(1)) if mm else None
 
 
 def traffic_from_profiles(workload: str):
@@ -69,6 +85,8 @@ def main() -> int:
                     help="matrices in the oracle's CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sk", action="store_true")
+    ap.add_argument("--no-n8", action="store_true", help="skip the 8x8 measurement")
+    ap.add_argument("--n8-only", action="store_true", help="time only the 8x8 path (for profiler runs)")
     ap.add_argument("--no-extras", action="store_true",
                     help="time only the path (for profiler runs)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -100,6 +118,9 @@ def main() -> int:
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration": {"bytes_read": X.numel() * 4, "bytes_written": Y.numel() * 4,
                                                "launches": 5}}), flush=True)
+        return 0
+    if args.n8_only:
+        print(json.dumps({"n8": bench_n8(args, dev, torch.cuda.current_stream(dev))}), flush=True)
         return 0
     w = workloads.WORKLOADS[args.workload]
     B = w.B
@@ -282,8 +303,122 @@ def main() -> int:
                                         "tol": args.tol, "seconds": round(rates["gpu_tol"][1], 2)}
         log(f"cpu baseline: {out['cpu_baseline']}")
 
+    if not args.no_n8:
+        out["n8"] = bench_n8(args, dev, stream)
+
     print(json.dumps(out), flush=True)
     return 0
+
+
+N8_B = 1 << 22
+N8_DESC = ("B=2^22 8x8 matrices, bf16 storage, fp32 compute; half sigma*N(0,1) with sigma in {1,5,20}, "
+           "half 20*Pi + 0.1 N(0,1) (Pi a random permutation); dP ~ N(0,1) bf16; fwd + bwd")
+
+
+def n8_inputs(B: int, seed: int, dev):
+    """The 8x8 mixture, drawn on the device with torch's seeded generator."""
+    import torch
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    Z = torch.randn(B, 8, 8, device=dev, generator=g)
+    kind = torch.randint(0, 2, (B,), device=dev, generator=g)
+    sig = torch.tensor([1.0, 5.0, 20.0], device=dev)[torch.randint(0, 3, (B,), device=dev, generator=g)]
+    perm = torch.argsort(torch.rand(B, 8, device=dev, generator=g), dim=1)
+    Pi = torch.zeros(B, 8, 8, device=dev).scatter_(2, perm[:, :, None], 1.0)
+    H = torch.where(kind[:, None, None] == 0, sig[:, None, None] * Z, 20.0 * Pi + 0.1 * Z)
+    G = torch.randn(B, 8, 8, device=dev, generator=g)
+    return H.to(torch.bfloat16).contiguous(), G.to(torch.bfloat16).contiguous()
+
+
+def bench_n8(args, dev, stream) -> dict:
+    """fwd + bwd of the 8x8 projection on its mixture workload (reported beside the 4x4 path)."""
+    import torch
+
+    import paper_2606_07574_amd as b4
+    B = N8_B
+    H, G = n8_inputs(B, 8, dev)
+    P = torch.empty(B, 8, 8, device=dev)
+    dual = torch.empty(B, 16, device=dev)
+    dH = torch.empty(B, 8, 8, device=dev)
+    lib = b4.lib()
+    sptr = stream.cuda_stream
+
+    def step():
+        rc = lib.birkhoff8_fwd(H.data_ptr(), b4.BF16, P.data_ptr(), dual.data_ptr(), None, B, args.tol,
+                               args.max_iter, sptr)
+        if rc:
+            raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+        e_mid.record(stream)
+        rc = lib.birkhoff8_bwd(P.data_ptr(), G.data_ptr(), b4.BF16, dH.data_ptr(), B, sptr)
+        if rc:
+            raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+
+    K = max(3, args.steps // 4)
+    e0, e_mid, e1 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    step()
+    torch.cuda.synchronize()
+    f_ms = b_ms = 0.0
+    t_start = time.perf_counter()
+    for _ in range(K):
+        e0.record(stream)
+        step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        f_ms += e0.elapsed_time(e_mid)
+        b_ms += e_mid.elapsed_time(e1)
+    wall = time.perf_counter() - t_start
+    f_ms /= K
+    b_ms /= K
+    fwd_bytes = B * (128 + 256 + 64)
+    bwd_bytes = B * (256 + 128 + 256)
+    res = {"workload": "n8_mix_bf16_b2e22", "B": B, "desc": N8_DESC, "steps": K,
+           "value": round(B / ((f_ms + b_ms) * 1e-3), 1), "unit": "proj/s",
+           "ms_per_step": round(wall * 1e3 / K, 4), "fwd_ms": round(f_ms, 4), "bwd_ms": round(b_ms, 4),
+           "kernels": {"newton8_fwd": {"alg_bytes_per_launch": fwd_bytes,
+                                       "achieved_GBs": round(fwd_bytes / (f_ms * 1e-3) / 1e9, 1)},
+                       "implicit8_bwd": {"alg_bytes_per_launch": bwd_bytes,
+                                         "achieved_GBs": round(bwd_bytes / (b_ms * 1e-3) / 1e9, 1)}},
+           "path_hbm_frac": round((fwd_bytes + bwd_bytes) / ((f_ms + b_ms) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    valu = valu_from_profiles("n8_mix_bf16_b2e22", "newton8_fwd")
+    ach = valu / (f_ms * 1e-3) / 1e12 if valu else None
+    res["roofline"] = {"bound": "alu", "kernel": "newton8_fwd",
+                       "achieved": round(ach, 2) if ach else None, "peak": VALU_PEAK_T,
+                       "unit": "T lane-instr/s", "frac": round(ach / VALU_PEAK_T, 4) if ach else None,
+                       "counted_lane_instr_per_launch": valu}
+    if args.n8_only:
+        return res
+    _, _, it = b4.fwd8(H, args.tol, args.max_iter, want_dual=False, want_iters=True)
+    torch.cuda.synchronize()
+    itn = it.cpu().numpy()
+    P64 = P.double()
+    marg = torch.maximum((P64.sum(-1) - 1).abs().amax(-1), (P64.sum(-2) - 1).abs().amax(-1))
+    conv = itn[itn >= 0]
+    n64 = (len(itn) // 64) * 64
+    res["newton_steps"] = {"mean": round(float(conv.mean()), 3), "p99": int(np.percentile(conv, 99)),
+                           "max": int(conv.max()),
+                           "mean_of_wave_max": round(float(np.clip(itn[:n64], 0, None).reshape(-1, 64)
+                                                           .max(axis=1).mean()), 3),
+                           "not_converged": int((itn == -1).sum()), "non_finite": int((itn == -2).sum())}
+    res["max_marginal_err"] = float(marg.max().item())
+    del P64
+    log(f"n8: {res['value']:.4g} proj/s fwd {f_ms:.3f} ms bwd {b_ms:.3f} ms; steps {res['newton_steps']}; "
+        f"max marginal {res['max_marginal_err']:.3e}")
+    if not args.no_cpu_baseline:
+        from oracle import birkhoffn
+        n = 1 << 20
+        Hs = H[:n].float().cpu().numpy().astype(np.float64)
+        Gs = G[:n].float().cpu().numpy().astype(np.float64)
+        threads = max(1, min(16, os.cpu_count() or 1))
+        t0 = time.perf_counter()
+        Pr, _, _ = birkhoffn.fwd(Hs, threads=threads)
+        birkhoffn.bwd(Pr, Gs, threads=threads)
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": round(n / dt, 1), "unit": "proj/s", "cores": threads, "kind": "oracle",
+                               "sample": f"first {n} matrices of n8_mix_bf16_b2e22; fp64 size-generic oracle "
+                                         f"forward (tol {birkhoffn.DEFAULT_TOL:g}) + backward, {threads} threads, "
+                                         f"{dt:.1f} s"}
+        log(f"n8 cpu baseline: {res['cpu_baseline']}")
+    return res
 
 
 if __name__ == "__main__":
