@@ -1103,6 +1103,14 @@ __global__ __launch_bounds__(64) void sk_bwd_kernel(const void* __restrict__ H,
 // ---------------------------------------------------------------------------
 constexpr int kB8Block = 256;
 constexpr int kB8Waves = kB8Block / 64;
+#ifndef B8_REFILL_MIN
+#define B8_REFILL_MIN 32
+#endif
+#ifndef B8_RANGES
+#define B8_RANGES 4096
+#endif
+constexpr int kB8RefillMin = B8_REFILL_MIN;  // idle lanes that trigger a refill
+constexpr int64_t kB8Ranges = B8_RANGES;      // wave ranges per launch (blocks are scheduled dynamically)
 
 // Index of the weight of column pair (j, k), j < k < 8, in a packed array of 28.
 __host__ __device__ constexpr int pw8(int j, int k) { return j * 8 - (j * (j + 1)) / 2 + (k - j - 1); }
@@ -1287,41 +1295,66 @@ template <int DT, bool WRITE_DUAL, bool WRITE_ITERS>
 __global__ __launch_bounds__(kB8Block) void newton8_fwd_kernel(const void* __restrict__ H, float* __restrict__ P,
                                                                 float* __restrict__ dual,
                                                                 int32_t* __restrict__ iters, int64_t B, float tol,
-                                                                int max_iter) {
+                                                                int max_iter, int64_t per_wave) {
     const int lane = threadIdx.x & 63;
-    const int64_t nchunk = (B + 63) / 64;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kB8Waves;
-    for (int64_t c = static_cast<int64_t>(blockIdx.x) * kB8Waves + (threadIdx.x >> 6); c < nchunk; c += stride) {
-        const int64_t b = 64 * c + lane;
-        const bool valid = b < B;
-        float T[64], a[8], beta[7], g[8];
-        bool finite = true;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) g[j] = 0.f;
-        if (valid) finite = init8<DT>(H, b, T, a, beta, g);
-        float gmax0 = 0.f;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) gmax0 = __builtin_fmaxf(gmax0, __builtin_fabsf(g[j]));
-        int status = finite ? 0 : BIRKHOFF4_NON_FINITE;
-        bool active = valid && finite && !(gmax0 <= tol) && max_iter > 0;
-        if (valid && finite && !(gmax0 <= tol) && max_iter == 0) status = BIRKHOFF4_NOT_CONVERGED;
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    // The wave owns problems r0 .. r1 - 1 and hands them out to its lanes as they free up.
+    const int64_t r0 = (static_cast<int64_t>(blockIdx.x) * kB8Waves + (threadIdx.x >> 6)) * per_wave;
+    if (r0 >= B) return;  // uniform across the wave
+    const int64_t r1 = (r0 + per_wave < B) ? r0 + per_wave : B;
+    int64_t cursor = r0;  // next unclaimed problem (uniform)
 
-        float W[28], ga[7], o[7];
-        float lam = __builtin_fmaxf(kLM * gmax0, kLMFloor);
-        float gn2 = 0.f, t = 1.f, fofs = 0.f, gsum = 0.f;
-        int cnt = 0;  // bits 0-15: trial steps; bits 16-18: log2 of the initial trial step
-        if (active) {
-            weights8(T, W);
+    bool active = false;  // holds an unfinished problem
+    int64_t b = 0;
+    float T[64], a[8], beta[7], g[8], W[28], ga[7], o[7];
+    float lam = 0.f, gn2 = 0.f, t = 1.f, fofs = 0.f, gsum = 0.f;
+    int cnt = 0;  // bits 0-15: trial steps; bits 16-18: log2 of the initial trial step
 #pragma unroll
-            for (int j = 0; j < 7; ++j) ga[j] = g[j];
+    for (int j = 0; j < 7; ++j) o[j] = 0.f;
+
+    for (;;) {
+        // Refill: once enough lanes are idle (or none is working), idle lanes take the next
+        // problems of the range and evaluate their initial points; problems already within
+        // tol there (or non-finite, or max_iter = 0) are written at once and the lane takes
+        // another.
+        uint64_t idle = __ballot(!active);
+        while (cursor < r1 && (__popcll(idle) >= kB8RefillMin || idle == ~0ull)) {
+            const int64_t left = r1 - cursor;
+            const int n_idle = __popcll(idle);
+            const int take = (left < n_idle) ? static_cast<int>(left) : n_idle;
+            const int rank = __popcll(idle & below);
+            if (!active && rank < take) {
+                b = cursor + rank;
+                const bool finite = init8<DT>(H, b, T, a, beta, g);
+                float gmax = 0.f;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) gn2 = __builtin_fmaf(g[j], g[j], gn2);
+                for (int j = 0; j < 8; ++j) gmax = __builtin_fmaxf(gmax, __builtin_fabsf(g[j]));
+                if (!finite || gmax <= tol || max_iter == 0) {
+                    const int st = !finite ? BIRKHOFF4_NON_FINITE : (gmax <= tol ? 0 : BIRKHOFF4_NOT_CONVERGED);
+                    store_output8<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, b, T, a, beta, st);
+                } else {
+                    weights8(T, W);
+                    gn2 = 0.f;
+#pragma unroll
+                    for (int j = 0; j < 7; ++j) {
+                        ga[j] = g[j];
+                        o[j] = 0.f;
+                    }
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) gn2 = __builtin_fmaf(g[j], g[j], gn2);
+                    lam = __builtin_fmaxf(kLM * gmax, kLMFloor);
+                    t = 1.f;
+                    fofs = gsum = 0.f;
+                    cnt = 0;
+                    active = true;
+                }
+            }
+            cursor += take;
+            idle = __ballot(!active);
         }
-#pragma unroll
-        for (int j = 0; j < 7; ++j) o[j] = 0.f;
+        if (idle == ~0ull) break;  // nothing left in the range and no lane working
 
-        while (__ballot(active) != 0) {
-            if (active) {
+        if (active) {
             float d[7], s[7], l[8];
             newton_solve8(W, ga, lam, d);
             t = __builtin_fminf(t, kCap2 * rcp(__builtin_fmaxf(spread8(d), kTiny)));
@@ -1406,12 +1439,11 @@ __global__ __launch_bounds__(kB8Block) void newton8_fwd_kernel(const void* __res
 #pragma unroll
                     for (int j = 0; j < 7; ++j) beta[j] -= o[j];
                 }
-                status = conv ? evals : BIRKHOFF4_NOT_CONVERGED;
+                store_output8<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, b, T, a, beta,
+                                                       conv ? evals : BIRKHOFF4_NOT_CONVERGED);
                 active = false;
             }
-            }
         }
-        if (valid) store_output8<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, b, T, a, beta, status);
     }
 }
 
@@ -1421,23 +1453,91 @@ __global__ __launch_bounds__(kB8Block) void newton8_fwd_kernel(const void* __res
 // (W_pk F_jp + W_jp F_pk) / piv to its flow, piv = sum_{k > p} W_pk (ground = node 8);
 // back-substitution gives the potentials w (w_8 = 0), and dH_ij = T_ij (psi_ij -
 // sum_k T_ik psi_ik) with psi = G - 1 w^T. Products are formed ratio-first so that a
-// term underflows only when its value does.
+// term underflows only when its value does. Memory traffic is coalesced: a wave moves
+// the 64 problems of a chunk between HBM and an LDS tile (one problem per 17 x 16 bytes,
+// so that lanes reading their own problem hit distinct banks) with whole-wave
+// non-temporal accesses, and each lane works on its own problem from the tile.
+constexpr int kB8Stride = 17;  // v4f per problem in the LDS tile
+
 template <int DT>
-__global__ __launch_bounds__(kB8Block) void implicit8_bwd_kernel(const float* __restrict__ P,
-                                                                  const void* __restrict__ dP,
-                                                                  float* __restrict__ dH, int64_t B) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kB8Block;
-    for (int64_t b = static_cast<int64_t>(blockIdx.x) * kB8Block + threadIdx.x; b < B; b += stride) {
-        float T[64], W[28], F[28], w[8], ip[7];
+__global__ __launch_bounds__(kB8Block, 2) void implicit8_bwd_kernel(const float* __restrict__ P,
+                                                                     const void* __restrict__ dP,
+                                                                     float* __restrict__ dH, int64_t B) {
+    __shared__ v4f tile_all[kB8Waves][64 * kB8Stride];
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+    v4f* const tile = tile_all[wv];
+    v4u* const tileu = reinterpret_cast<v4u*>(tile);
+    const v4f* P4 = reinterpret_cast<const v4f*>(P);
+    const v4u* G4 = reinterpret_cast<const v4u*>(dP);
+    v4f* dH4 = reinterpret_cast<v4f*>(dH);
+    constexpr int GP = (DT == BIRKHOFF4_BF16) ? 8 : 16;  // 16-byte pieces of dP per problem
+    const int64_t nchunk = (B + 63) / 64;
+    for (int64_t c = static_cast<int64_t>(blockIdx.x) * kB8Waves + wv; c < nchunk;
+         c += static_cast<int64_t>(gridDim.x) * kB8Waves) {
+        const int64_t base = c * 64;
+        const int n = (B - base < 64) ? static_cast<int>(B - base) : 64;  // problems in this chunk
+        // P: 16 pieces per problem, piece k of the chunk goes to problem k / 16, slot k % 16
+        {
+            v4f pc[16];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) load_row8<BIRKHOFF4_F32>(P, b, i, T + 8 * i);
+            for (int q = 0; q < 16; ++q) {
+                const int k = 64 * q + lane;
+                pc[q] = k < 16 * n ? __builtin_nontemporal_load(P4 + 16 * base + k) : v4f{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                const int k = 64 * q + lane;
+                tile[(k >> 4) * kB8Stride + (k & 15)] = pc[q];
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        float T[64];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const v4f t = tile[lane * kB8Stride + r];
+            T[4 * r] = t.x; T[4 * r + 1] = t.y; T[4 * r + 2] = t.z; T[4 * r + 3] = t.w;
+        }
+        __builtin_amdgcn_wave_barrier();
+        // dP: GP pieces per problem, kept in the tile (read twice below)
+        {
+            v4u gc[GP];
+#pragma unroll
+            for (int q = 0; q < GP; ++q) {
+                const int k = 64 * q + lane;
+                gc[q] = k < GP * n ? __builtin_nontemporal_load(G4 + GP * base + k) : v4u{0u, 0u, 0u, 0u};
+            }
+#pragma unroll
+            for (int q = 0; q < GP; ++q) {
+                const int k = 64 * q + lane;
+                tileu[(k / GP) * kB8Stride + (k % GP)] = gc[q];
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        // row i of this lane's G from the tile
+        auto grow = [&](int i, float G[8]) {
+            if constexpr (DT == BIRKHOFF4_BF16) {
+                const v4u r = tileu[lane * kB8Stride + i];
+                const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    G[2 * k] = __uint_as_float(w[k] << 16);
+                    G[2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
+                }
+            } else {
+                const v4f r0 = tile[lane * kB8Stride + 2 * i], r1 = tile[lane * kB8Stride + 2 * i + 1];
+                G[0] = r0.x; G[1] = r0.y; G[2] = r0.z; G[3] = r0.w;
+                G[4] = r1.x; G[5] = r1.y; G[6] = r1.z; G[7] = r1.w;
+            }
+        };
+        float W[28], F[28], w[8], ip[7];
         weights8(T, W);
 #pragma unroll
         for (int k = 0; k < 28; ++k) F[k] = 0.f;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             float G[8];
-            load_row8<DT>(dP, b, i, G);
+            grow(i, G);
 #pragma unroll
             for (int j = 0; j < 8; ++j)
 #pragma unroll
@@ -1468,11 +1568,12 @@ __global__ __launch_bounds__(kB8Block) void implicit8_bwd_kernel(const float* __
             for (int k = p + 1; k < 8; ++k) s += __builtin_fmaf(W[pw8(p, k)], w[k], F[pw8(p, k)]);
             w[p] = s * ip[p];
         }
-        v4f* out = reinterpret_cast<v4f*>(dH) + 16 * b;
+        // dH row i replaces tile slots 2i, 2i+1 of this lane's problem; going down from the
+        // last row, those slots hold only dP rows already read (bf16 rows are 16 bytes)
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
+        for (int i = 7; i >= 0; --i) {
             float G[8], psi[8];
-            load_row8<DT>(dP, b, i, G);
+            grow(i, G);
             float mu = 0.f;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
@@ -1482,9 +1583,17 @@ __global__ __launch_bounds__(kB8Block) void implicit8_bwd_kernel(const float* __
             float o[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) o[j] = T[8 * i + j] * (psi[j] - mu);
-            out[2 * i] = v4f{o[0], o[1], o[2], o[3]};
-            out[2 * i + 1] = v4f{o[4], o[5], o[6], o[7]};
+            tile[lane * kB8Stride + 2 * i] = v4f{o[0], o[1], o[2], o[3]};
+            tile[lane * kB8Stride + 2 * i + 1] = v4f{o[4], o[5], o[6], o[7]};
         }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            const int k = 64 * q + lane;
+            const v4f o = tile[(k >> 4) * kB8Stride + (k & 15)];
+            if (k < 16 * n) __builtin_nontemporal_store(o, dH4 + 16 * base + k);
+        }
+        __builtin_amdgcn_wave_barrier();
     }
 }
 
@@ -1582,16 +1691,19 @@ int dispatch_fwd(const void* H, float* P, float* dual, int32_t* iters, int64_t B
     return launch_fwd<DT, false, false>(H, P, dual, iters, B, tol, max_iter, stream, cus);
 }
 
-// n = 8: one 64-problem chunk per wave, blocks scheduled by the hardware; batches beyond
-// kMaxGrid blocks loop.
+// n = 8: one range of problems per wave, blocks scheduled by the hardware.
 template <int DT, bool WD, bool WI>
 int launch_fwd8(const void* H, float* P, float* dual, int32_t* iters, int64_t B, float tol, int max_iter,
                 hipStream_t stream) {
-    const int64_t chunks = (B + 63) / 64;
-    const int64_t want = (chunks + kB8Waves - 1) / kB8Waves;
-    const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
+    // about kB8Ranges ranges in all (several per resident wave slot), at least 64 problems each
+    const int64_t waves_min = (B + kMaxGrid * kB8Waves - 1) / (kMaxGrid * kB8Waves);
+    int64_t per_wave = (B + kB8Ranges - 1) / kB8Ranges;
+    if (per_wave < 64) per_wave = 64;
+    if (per_wave < waves_min) per_wave = waves_min;
+    const int64_t waves = (B + per_wave - 1) / per_wave;
+    const int64_t grid = (waves + kB8Waves - 1) / kB8Waves;
     hipLaunchKernelGGL((newton8_fwd_kernel<DT, WD, WI>), dim3(static_cast<unsigned>(grid)), dim3(kB8Block), 0,
-                       stream, H, P, dual, iters, B, tol, max_iter);
+                       stream, H, P, dual, iters, B, tol, max_iter, per_wave);
     return launch_status();
 }
 
@@ -1679,7 +1791,8 @@ int birkhoff8_bwd(const float* P, const void* dP, int dp_dtype, float* dH, int64
     if (misaligned(P) || misaligned(dP) || misaligned(dH)) return BIRKHOFF4_ERR_ALIGN;
     const size_t n = static_cast<size_t>(B) * 256, ng = static_cast<size_t>(B) * 64 * dtype_bytes(dp_dtype);
     if (overlaps(dH, n, P, n) || overlaps(dH, n, dP, ng)) return BIRKHOFF4_ERR_OVERLAP;
-    const int64_t want = (B + kB8Block - 1) / kB8Block;
+    const int64_t chunks = (B + 63) / 64;
+    const int64_t want = (chunks + kB8Waves - 1) / kB8Waves;
     const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
     if (dp_dtype == BIRKHOFF4_BF16)
         hipLaunchKernelGGL(implicit8_bwd_kernel<BIRKHOFF4_BF16>, dim3(static_cast<unsigned>(grid)),
