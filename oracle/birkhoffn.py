@@ -12,6 +12,12 @@ threads.
                                             eq. min_fx with eq. grad_hess (a = b = 1, eta = 1)
   bwd(P, dP) -> dH                          eq. derivative (a = b = 1, eta = 1), sign of R = -M
   sinkhorn(H, tol, max_steps) -> P, steps   eq. sinkhorn_knopp run to a row-sum tolerance
+
+General entropic OT (eq. entropic with cost M, marginals a, b, regulariser eta):
+  ot_fwd(M, a, b, eta) -> T, dual, iters    the same damped Newton on eq. min_fx with the
+                                            general eq. grad_hess; dual = (alpha, beta), beta_n = 0
+  ot_bwd(T, a, G, eta) -> dM                eq. derivative (dL/dM)
+  ot_sinkhorn(M, a, b, eta) -> T, steps     u = a / (K v), v = b / (K^T u), K = exp(-M / eta)
 """
 from __future__ import annotations
 
@@ -54,7 +60,12 @@ def _load():
         lib.oraclen_fwd.argtypes = [i32, dp, dp, dp, ip, i64, i64, ctypes.c_double, i32]
         lib.oraclen_bwd.argtypes = [i32, dp, dp, dp, i64, i64]
         lib.oraclen_sinkhorn.argtypes = [i32, dp, dp, ip, i64, i64, ctypes.c_double, i32]
-        for f in (lib.oraclen_fwd, lib.oraclen_bwd, lib.oraclen_sinkhorn):
+        d = ctypes.c_double
+        lib.oraclen_ot_fwd.argtypes = [i32, dp, dp, dp, d, dp, dp, ip, i64, i64, d, i32]
+        lib.oraclen_ot_bwd.argtypes = [i32, dp, dp, d, dp, dp, i64, i64]
+        lib.oraclen_ot_sinkhorn.argtypes = [i32, dp, dp, dp, d, dp, ip, i64, i64, d, i32]
+        for f in (lib.oraclen_fwd, lib.oraclen_bwd, lib.oraclen_sinkhorn, lib.oraclen_ot_fwd,
+                  lib.oraclen_ot_bwd, lib.oraclen_ot_sinkhorn):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -134,3 +145,61 @@ def marginal_errors(P) -> np.ndarray:
     """Per matrix: max over rows and columns of |sum - 1|, in fp64."""
     P = _f64(P)
     return np.maximum(np.abs(P.sum(axis=2) - 1.0).max(axis=1), np.abs(P.sum(axis=1) - 1.0).max(axis=1))
+
+
+def _marg(x, B, n, name):
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+    if a.shape != (B, n):
+        raise ValueError(f"{name} must have shape {(B, n)}, got {a.shape}")
+    return a
+
+
+def ot_fwd(M, a, b, eta: float = 1.0, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER,
+           threads: int | None = None):
+    """Entropic OT per matrix: T = argmin <T, M> - eta h(T) over Pi(a[b], b[b]), fp64.
+
+    Returns (T [B,n,n], dual [B,2n] = (alpha_1..n, beta_1..n-1, 0), iters [B] int32)."""
+    lib = _load()
+    M = _f64(M)
+    B, n = M.shape[0], M.shape[1]
+    a = _marg(a, B, n, "a")
+    b = _marg(b, B, n, "b")
+    T = np.empty_like(M)
+    dual = np.empty((B, 2 * n), np.float64)
+    iters = np.empty(B, np.int32)
+    rc = []
+    _run(lambda r: rc.append(lib.oraclen_ot_fwd(n, _ptr(M), _ptr(a), _ptr(b), float(eta), _ptr(T), _ptr(dual),
+                                                _ptr(iters, ctypes.c_int32), r[0], r[1], tol, max_iter)),
+         B, threads)
+    if any(rc):
+        raise ValueError("eta must be positive")
+    return T, dual, iters
+
+
+def ot_bwd(T, a, G, eta: float = 1.0, threads: int | None = None) -> np.ndarray:
+    """dL/dM at the OT solution T (eq. derivative) for upstream gradient G = dL/dT."""
+    lib = _load()
+    T = _f64(T)
+    G = _f64(G)
+    B, n = T.shape[0], T.shape[1]
+    a = _marg(a, B, n, "a")
+    dM = np.empty_like(T)
+    _run(lambda r: lib.oraclen_ot_bwd(n, _ptr(T), _ptr(a), float(eta), _ptr(G), _ptr(dM), r[0], r[1]),
+         B, threads)
+    return dM
+
+
+def ot_sinkhorn(M, a, b, eta: float = 1.0, tol: float = 1e-14, max_steps: int = 1_000_000,
+                threads: int | None = None):
+    """Sinkhorn iterations with marginals until the row sums are within tol of a."""
+    lib = _load()
+    M = _f64(M)
+    B, n = M.shape[0], M.shape[1]
+    a = _marg(a, B, n, "a")
+    b = _marg(b, B, n, "b")
+    T = np.empty_like(M)
+    steps = np.empty(B, np.int32)
+    _run(lambda r: lib.oraclen_ot_sinkhorn(n, _ptr(M), _ptr(a), _ptr(b), float(eta), _ptr(T),
+                                           _ptr(steps, ctypes.c_int32), r[0], r[1], tol, max_steps),
+         B, threads)
+    return T, steps

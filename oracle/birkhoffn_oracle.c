@@ -339,3 +339,230 @@ int oraclen_sinkhorn(int n, const double *H, double *P, int32_t *steps, int64_t 
         steps[b] = sinkhorn_one(n, H + (int64_t)n * n * b, P + (int64_t)n * n * b, tol, max_steps);
     return 0;
 }
+
+/* ---------------------------------------------------------------------------
+ * General entropic OT (eq. entropic): cost M, marginals a > 0, b > 0 with equal sums,
+ * regulariser eta > 0. Dual eq. dual, partial maximiser eq. alpha_opt, reduced
+ * problem eq. min_fx over x = beta_{-m}, gradient and Hessian eq. grad_hess:
+ *   T_ij = a_i softmax_j((beta_j - M_ij) / eta),
+ *   grad f = T_{-m}^T 1 - b_{-m},
+ *   hess f = eta^{-1} (diag(c_{-m}) - T_{-m}^T diag(a)^{-1} T_{-m}),
+ * whose diagonal c_j - sum_i T_ij^2 / a_i = sum_{k != j} W_jk with
+ * W_jk = sum_i T_ij T_ik / a_i (rows of T sum to a_i): the grounded Laplacian of the
+ * column graph again. The same damped Newton as for the projection, with
+ * f(beta) = eta sum_i a_i - alpha*(beta)^T a - beta^T b and the stop test
+ * max_j |c_j - b_j| <= tol. Backward: eq. derivative with
+ *   mu_c - T_{-m}^T (mu_r / a) = sum_{k != j} F_jk,  F_jk = sum_i T_ij T_ik (G_ij - G_ik) / a_i,
+ *   D_ij = -eta^{-1} T_ij (psi_ij - sum_k T_ik psi_ik / a_i),  psi = G - 1 w^T,
+ * returned as dL/dM = D.
+ * ------------------------------------------------------------------------- */
+
+/* T_ij = a_i exp(U_ij - mu_i) / s_i with U_ij = (beta_j - M_ij) / eta; lse_i = mu_i + log s_i */
+static void ot_evaluate(int n, const double *M, const double *a, double eta, const double *beta,
+                        double *T, double *lse)
+{
+    for (int i = 0; i < n; ++i) {
+        double U[NMAX], mu = -INFINITY, s = 0.0;
+        for (int j = 0; j < n; ++j) {
+            U[j] = (beta[j] - M[n * i + j]) / eta;
+            if (U[j] > mu) mu = U[j];
+        }
+        for (int j = 0; j < n; ++j) s += exp(U[j] - mu);
+        for (int j = 0; j < n; ++j) T[n * i + j] = a[i] * exp(U[j] - mu) / s;
+        lse[i] = mu + log(s);
+    }
+}
+
+/* g_j = c_j - b_j; near a permutation-like T the column sums are formed from the
+ * small entries: for the dominant entry of row i, T_{i,dom} = a_i - sum_{k != dom} T_ik */
+static void ot_gradient(int n, const double *T, const double *a, const double *b, double *g)
+{
+    int dom[NMAX];
+    for (int i = 0; i < n; ++i) {
+        dom[i] = 0;
+        for (int j = 1; j < n; ++j)
+            if (T[n * i + j] > T[n * i + dom[i]]) dom[i] = j;
+    }
+    for (int j = 0; j < n; ++j) {
+        double s = -b[j];
+        for (int i = 0; i < n; ++i) {
+            if (dom[i] == j) {
+                s += a[i];
+                for (int k = 0; k < n; ++k)
+                    if (k != j) s -= T[n * i + k];
+            } else {
+                s += T[n * i + j];
+            }
+        }
+        g[j] = s;
+    }
+}
+
+static int ot_one(int n, const double *M, const double *a, const double *b, double eta, double *T,
+                  double *dual, double tol, int max_iter)
+{
+    const int m = n - 1;
+    if (!all_finite(M, n * n) || !all_finite(a, n) || !all_finite(b, n)) {
+        for (int q = 0; q < n * n; ++q) T[q] = NAN;
+        for (int q = 0; q < 2 * n; ++q) dual[q] = NAN;
+        return -2;
+    }
+    double beta[NMAX] = {0.0}, lse[NMAX], g[NMAX];
+    int it = 0, converged = 0;
+    ot_evaluate(n, M, a, eta, beta, T, lse);
+    ot_gradient(n, T, a, b, g);
+    for (;;) {
+        const double res = max_abs(n, g);
+        if (res <= tol) { converged = 1; break; }
+        if (it >= max_iter) break;
+        /* Newton direction d = -[hess f + lambda I]^{-1} grad f; hess f = L(W) / eta */
+        double W[NMAX][NMAX], rhs[NMAX], d[NMAX];
+        for (int j = 0; j < n; ++j)
+            for (int k = 0; k < n; ++k) {
+                double s = 0.0;
+                for (int i = 0; i < n; ++i) s += T[n * i + j] * T[n * i + k] / a[i];
+                W[j][k] = s / eta;
+            }
+        for (int j = 0; j < m; ++j) rhs[j] = -g[j];
+        laplacian_solve(n, W, LM * res, rhs, d);
+        double dmax = 0.0;
+        for (int j = 0; j < m; ++j) dmax = fmax(dmax, fabs(d[j]));
+        if (dmax > CAP * eta)
+            for (int j = 0; j < m; ++j) d[j] *= CAP * eta / dmax;
+        double slope = 0.0, gn2 = 0.0, dn2 = 0.0;
+        for (int j = 0; j < m; ++j) {
+            slope += g[j] * d[j];
+            gn2 += g[j] * g[j];
+            dn2 += d[j] * d[j];
+        }
+        double fscale = 1.0;
+        for (int i = 0; i < n; ++i) fscale += fabs(eta * a[i] * lse[i]);
+        for (int j = 0; j < m; ++j) fscale += fabs(b[j] * beta[j]);
+        double bn[NMAX], Tn[NMAX * NMAX], ln[NMAX], gn[NMAX];
+        int accepted = 0;
+        if (slope < -1e-12 * sqrt(gn2 * dn2)) {
+            double t = 1.0;
+            for (int bt = 0; bt < 40 && !accepted; ++bt, t *= 0.5) {
+                for (int j = 0; j < m; ++j) bn[j] = beta[j] + t * d[j];
+                bn[m] = 0.0;
+                ot_evaluate(n, M, a, eta, bn, Tn, ln);
+                ot_gradient(n, Tn, a, b, gn);
+                /* f = eta sum_i a_i (1 + lse_i - log a_i) - beta^T b: its change, row by row */
+                double df = 0.0;
+                for (int i = 0; i < n; ++i) df += eta * a[i] * (ln[i] - lse[i]);
+                for (int j = 0; j < m; ++j) df -= b[j] * t * d[j];
+                if (df <= ARMIJO * t * slope) accepted = 1;
+                else if (fabs(df) <= 1e-13 * fscale && max_abs(n, gn) < res) accepted = 1;
+            }
+        }
+        if (accepted) {
+            for (int j = 0; j < n; ++j) beta[j] = bn[j];
+        } else {
+            /* beta <- beta*(alpha*(beta)) (eq. bca, eq. beta_opt), gauge beta_n = 0 */
+            for (int j = 0; j < n; ++j) {
+                double mu = -INFINITY, s = 0.0, al[NMAX];
+                for (int i = 0; i < n; ++i) {
+                    al[i] = eta * (log(a[i]) - lse[i]); /* alpha*_i(beta) */
+                    mu = fmax(mu, (al[i] - M[n * i + j]) / eta);
+                }
+                for (int i = 0; i < n; ++i) s += exp((al[i] - M[n * i + j]) / eta - mu);
+                bn[j] = eta * log(b[j]) - eta * (mu + log(s));
+            }
+            for (int j = 0; j < n; ++j) beta[j] = bn[j] - bn[m];
+        }
+        ++it;
+        ot_evaluate(n, M, a, eta, beta, T, lse);
+        ot_gradient(n, T, a, b, g);
+    }
+    for (int i = 0; i < n; ++i) dual[i] = eta * (log(a[i]) - lse[i]);
+    for (int j = 0; j < n; ++j) dual[n + j] = beta[j];
+    return converged ? it : -1;
+}
+
+static void ot_backward_one(int n, const double *T, const double *a, double eta, const double *G,
+                            double *dM)
+{
+    double W[NMAX][NMAX], F[NMAX][NMAX], w[NMAX];
+    for (int j = 0; j < n; ++j)
+        for (int k = 0; k < n; ++k) {
+            double sw = 0.0, sf = 0.0;
+            for (int i = 0; i < n; ++i) {
+                const double q = T[n * i + j] * T[n * i + k] / a[i];
+                sw += q;
+                sf += q * (G[n * i + j] - G[n * i + k]);
+            }
+            W[j][k] = sw;
+            F[j][k] = sf;
+        }
+    laplacian_solve_flows(n, W, F, w); /* Delta w = mu_c - T^T (mu_r / a), Delta = L(W) */
+    for (int i = 0; i < n; ++i) {
+        double s = 0.0;
+        for (int k = 0; k < n; ++k) s += T[n * i + k] * (G[n * i + k] - w[k]);
+        s /= a[i];
+        for (int j = 0; j < n; ++j)
+            dM[n * i + j] = -T[n * i + j] * ((G[n * i + j] - w[j]) - s) / eta;
+    }
+}
+
+/* Sinkhorn with marginals: u = a / (K v), v = b / (K^T u), K = exp(-(M - min M) / eta) */
+static int ot_sinkhorn_one(int n, const double *M, const double *a, const double *b, double eta,
+                           double *T, double tol, int max_steps)
+{
+    double K[NMAX * NMAX], u[NMAX], v[NMAX], mn = INFINITY;
+    for (int q = 0; q < n * n; ++q) mn = fmin(mn, M[q]);
+    for (int q = 0; q < n * n; ++q) K[q] = exp(-(M[q] - mn) / eta);
+    for (int j = 0; j < n; ++j) v[j] = 1.0;
+    int steps = 0;
+    for (; steps < max_steps; ++steps) {
+        for (int i = 0; i < n; ++i) {
+            double s = 0.0;
+            for (int j = 0; j < n; ++j) s += K[n * i + j] * v[j];
+            u[i] = a[i] / s;
+        }
+        for (int j = 0; j < n; ++j) {
+            double s = 0.0;
+            for (int i = 0; i < n; ++i) s += K[n * i + j] * u[i];
+            v[j] = b[j] / s;
+        }
+        double err = 0.0;
+        for (int i = 0; i < n; ++i) {
+            double s = 0.0;
+            for (int j = 0; j < n; ++j) s += u[i] * K[n * i + j] * v[j];
+            err = fmax(err, fabs(s - a[i]));
+        }
+        if (err <= tol) { ++steps; break; }
+    }
+    for (int i = 0; i < n; ++i)
+        for (int j = 0; j < n; ++j) T[n * i + j] = u[i] * K[n * i + j] * v[j];
+    return steps;
+}
+
+int oraclen_ot_fwd(int n, const double *M, const double *a, const double *b, double eta, double *T,
+                   double *dual, int32_t *iters, int64_t lo, int64_t hi, double tol, int max_iter)
+{
+    if (n < 2 || n > NMAX || !(eta > 0.0)) return -1;
+    for (int64_t q = lo; q < hi; ++q)
+        iters[q] = ot_one(n, M + (int64_t)n * n * q, a + (int64_t)n * q, b + (int64_t)n * q, eta,
+                          T + (int64_t)n * n * q, dual + (int64_t)2 * n * q, tol, max_iter);
+    return 0;
+}
+
+int oraclen_ot_bwd(int n, const double *T, const double *a, double eta, const double *G, double *dM,
+                   int64_t lo, int64_t hi)
+{
+    if (n < 2 || n > NMAX || !(eta > 0.0)) return -1;
+    for (int64_t q = lo; q < hi; ++q)
+        ot_backward_one(n, T + (int64_t)n * n * q, a + (int64_t)n * q, eta, G + (int64_t)n * n * q,
+                        dM + (int64_t)n * n * q);
+    return 0;
+}
+
+int oraclen_ot_sinkhorn(int n, const double *M, const double *a, const double *b, double eta,
+                        double *T, int32_t *steps, int64_t lo, int64_t hi, double tol, int max_steps)
+{
+    if (n < 2 || n > NMAX || !(eta > 0.0)) return -1;
+    for (int64_t q = lo; q < hi; ++q)
+        steps[q] = ot_sinkhorn_one(n, M + (int64_t)n * n * q, a + (int64_t)n * q, b + (int64_t)n * q,
+                                   eta, T + (int64_t)n * n * q, tol, max_steps);
+    return 0;
+}
