@@ -48,7 +48,8 @@ enum {
     BIRKHOFF4_ERR_STEPS = -8,     /* Sinkhorn step count out of range */
     BIRKHOFF4_ERR_DEVICE = -9,    /* HIP device query failed */
     BIRKHOFF4_ERR_LAUNCH = -10,   /* kernel launch failed (hipGetLastError) */
-    BIRKHOFF4_ERR_VARIANT = -11   /* unknown forward variant */
+    BIRKHOFF4_ERR_VARIANT = -11,  /* unknown forward variant */
+    BIRKHOFF4_ERR_ETA = -12       /* eta not positive and finite */
 };
 
 /* Forward kernel variants (birkhoff4_fwd_ex2). Both compute the same projection to the
@@ -160,6 +161,35 @@ int birkhoff8_fwd(const void* H, int h_dtype, float* P, float* dual, int32_t* it
  * reduced dual at P. Rows and columns of dH sum to zero. dH must not overlap P or dP. */
 int birkhoff8_bwd(const float* P, const void* dP, int dp_dtype, float* dH, int64_t B,
                   hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * General entropic OT for 4 x 4 (eq. entropic, Sec. 2.3): for each b,
+ *   T = argmin over { T >= 0, T 1 = a, T^T 1 = b } of <T, M> - eta h(T),
+ * h(T) = -sum T_ij (log T_ij - 1), by the same Newton iteration on the reduced dual
+ * (eq. min_fx with the general eq. grad_hess); the Birkhoff projection is the case
+ * M = -H, a = b = 1, eta = 1.
+ *
+ * M     [B][4][4] fp32 cost, row-major.
+ * a, b  [B][4] fp32 marginals: positive, sum(a[b]) = sum(b[b]) for each b (when the
+ *       sums differ there is no solution and the status is BIRKHOFF4_NOT_CONVERGED).
+ * eta   regulariser > 0 (BIRKHOFF4_ERR_ETA otherwise).
+ * T     [B][4][4] fp32 output: rows sum to a exactly up to rounding, columns to b
+ *       within tol (max_j |c_j - b_j| <= tol, absolute).
+ * dual  NULL or [B][8] fp32 output: (alpha_1..4, beta_1..3, beta_4 = 0) in the units of
+ *       M, with T_ij = exp((alpha_i + beta_j - M_ij) / eta) (eq. dual).
+ * iters NULL or int32 [B]: trial steps taken, BIRKHOFF4_NOT_CONVERGED, or
+ *       BIRKHOFF4_NON_FINITE for a NaN, infinite or non-positive input (T, dual NaN).
+ * tol, max_iter, alignment, overlap rules and asynchrony as in birkhoff4_fwd. */
+int birkhoff4_ot_fwd(const float* M, const float* a, const float* b, float eta, float* T,
+                     float* dual, int32_t* iters, int64_t B, float tol, int max_iter,
+                     hipStream_t stream);
+
+/* Backward of birkhoff4_ot_fwd (eq. derivative): dM [B][4][4] fp32 = dL/dM from the
+ * solution T, the row marginals a [B][4] and dT = dL/dT [B][4][4] fp32, with Delta the
+ * Hessian of the reduced dual at T. Rows and columns of dM sum to zero. dM must not
+ * overlap the inputs. */
+int birkhoff4_ot_bwd(const float* T, const float* a, const float* dT, float eta, float* dM,
+                     int64_t B, hipStream_t stream);
 
 /* Human-readable text for a return code (static storage). */
 const char* birkhoff4_strerror(int code);

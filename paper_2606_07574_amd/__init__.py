@@ -11,6 +11,7 @@ a GPU, the calls raise.
     P = project(H)                    # autograd-aware: backward calls bwd
     P = sk_fwd(H, 20); dH = sk_bwd(H, dP, 20)   # Sinkhorn-Knopp baseline
     P, dual = fwd8(H); dH = bwd8(P, dP); P = project8(H)   # the same for 8 x 8 matrices
+    T, dual = ot_fwd(M, a, b, eta); dM = ot_bwd(T, a, dT, eta)  # general entropic OT, 4 x 4
 """
 from __future__ import annotations
 
@@ -54,6 +55,8 @@ def _load():
         "birkhoff4_sk_fwd": [vp, i32, vp, i64, i32, st],
         "birkhoff4_sk_bwd": [vp, i32, vp, i32, vp, i64, i32, st],
         "birkhoff8_fwd": [vp, i32, vp, vp, vp, i64, f32, i32, st],
+        "birkhoff4_ot_fwd": [vp, vp, vp, f32, vp, vp, vp, i64, f32, i32, st],
+        "birkhoff4_ot_bwd": [vp, vp, vp, f32, vp, i64, st],
         "birkhoff8_bwd": [vp, vp, i32, vp, i64, st],
         "birkhoff4_version": [],
     }
@@ -226,6 +229,68 @@ class Birkhoff8Fn(torch.autograd.Function):
 
 def project8(H: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER) -> torch.Tensor:
     return Birkhoff8Fn.apply(H, tol, max_iter)
+
+
+def _marginals(x: torch.Tensor, lead, name: str) -> None:
+    if not x.is_cuda or x.dtype != torch.float32 or not x.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous float32 GPU tensor")
+    if tuple(x.shape) != (*lead, 4):
+        raise ValueError(f"{name} must have shape {(*lead, 4)}, got {tuple(x.shape)}")
+
+
+def ot_fwd(M: torch.Tensor, a: torch.Tensor, b: torch.Tensor, eta: float = 1.0, tol: float = DEFAULT_TOL,
+           max_iter: int = DEFAULT_MAX_ITER, want_dual: bool = True, want_iters: bool = False):
+    """Entropic OT per trailing 4x4 cost matrix M (float32) with marginals a, b [..., 4]
+    (positive, equal sums) and regulariser eta. Returns (T, dual [..., 8] or None, iters or None)."""
+    B = _batch(M, "M")
+    if M.dtype != torch.float32:
+        raise TypeError("M must be float32")
+    lead = M.shape[:-2]
+    _marginals(a, lead, "a")
+    _marginals(b, lead, "b")
+    T = torch.empty(M.shape, dtype=torch.float32, device=M.device)
+    dual = torch.empty(*lead, 8, dtype=torch.float32, device=M.device) if want_dual else None
+    iters = torch.empty(lead, dtype=torch.int32, device=M.device) if want_iters else None
+    with torch.cuda.device(M.device):
+        _check(_load().birkhoff4_ot_fwd(_ptr(M), _ptr(a), _ptr(b), float(eta), _ptr(T), _ptr(dual), _ptr(iters),
+                                        B, float(tol), int(max_iter), _stream(M)))
+    return T, dual, iters
+
+
+def ot_bwd(T: torch.Tensor, a: torch.Tensor, dT: torch.Tensor, eta: float = 1.0) -> torch.Tensor:
+    """dL/dM of the OT solution T from dL/dT (float32)."""
+    B = _batch(T, "T")
+    if _batch(dT, "dT") != B:
+        raise ValueError("T and dT batch sizes differ")
+    if T.dtype != torch.float32 or dT.dtype != torch.float32:
+        raise TypeError("T and dT must be float32")
+    _marginals(a, T.shape[:-2], "a")
+    dM = torch.empty(T.shape, dtype=torch.float32, device=T.device)
+    with torch.cuda.device(T.device):
+        _check(_load().birkhoff4_ot_bwd(_ptr(T), _ptr(a), _ptr(dT), float(eta), _ptr(dM), B, _stream(T)))
+    return dM
+
+
+class OTFn(torch.autograd.Function):
+    """T = OT(M; a, b, eta); gradient with respect to M only (eq. derivative)."""
+
+    @staticmethod
+    def forward(ctx, M, a, b, eta=1.0, tol=DEFAULT_TOL, max_iter=DEFAULT_MAX_ITER):
+        a = a.contiguous()
+        T, _, _ = ot_fwd(M.contiguous(), a, b.contiguous(), eta, tol, max_iter, want_dual=False)
+        ctx.save_for_backward(T, a)
+        ctx.eta = eta
+        return T
+
+    @staticmethod
+    def backward(ctx, dT):
+        T, a = ctx.saved_tensors
+        return ot_bwd(T, a, dT.contiguous().float(), ctx.eta), None, None, None, None, None
+
+
+def ot(M: torch.Tensor, a: torch.Tensor, b: torch.Tensor, eta: float = 1.0, tol: float = DEFAULT_TOL,
+       max_iter: int = DEFAULT_MAX_ITER) -> torch.Tensor:
+    return OTFn.apply(M, a, b, eta, tol, max_iter)
 
 
 def version() -> int:

@@ -1598,6 +1598,316 @@ __global__ __launch_bounds__(kB8Block, 2) void implicit8_bwd_kernel(const float*
 }
 
 // ---------------------------------------------------------------------------
+// General entropic OT for 4 x 4 (eq. entropic): cost M, marginals a > 0 and b > 0 with
+// equal sums, regulariser eta > 0. With h = -M / eta (log2 units: h log2(e)) and x = beta /
+// eta, T_ij = a_i S_ij where S is the row softmax of h + 1 x^T; the reduced dual over
+// x_{-4} has gradient c - b with c = T^T 1, and Hessian the Laplacian of the column graph
+// with weights W_jk = sum_i a_i S_ij S_ik = sum_i T_ij T_ik / a_i (eq. grad_hess), so the
+// Birkhoff iteration carries over with the row masses and column targets: the same
+// product-form trials (S updated in place), spread cap, Armijo test on
+// f = sum_i a_i lse_i - sum_j b_j x_j, Levenberg-Marquardt shift and re-derivation of
+// flushed entries. One problem per lane; each wave owns a range of problems and refills
+// its lanes from it (as the 8 x 8 kernel does).
+// ---------------------------------------------------------------------------
+constexpr int kOtBlock = 256;
+constexpr int kOtWaves = kOtBlock / 64;
+constexpr int kOtRefillMin = 16;
+constexpr int64_t kOtRanges = 8192;
+
+__device__ __forceinline__ v4f load4(const float* base, int64_t b) { return reinterpret_cast<const v4f*>(base)[b]; }
+
+// Initial point: x_j = mean_i h_i4 - mean_i h_ij + log2(b_j / b_4) (exact for separable
+// h), S the row softmax of h + 1 x^T, la the log2 row normalisers. Returns false for a
+// NaN, infinite or non-positive input (S, la, x are then NaN).
+__device__ __forceinline__ bool ot_init(const float* M, const float* av, const float* bv, int64_t p, float rsc,
+                                        float S[16], float la[4], float x[3], float a[4], float bb[4]) {
+    float h[16];
+    load16_f32(M, p, h);
+    const v4f A = load4(av, p), Bm = load4(bv, p);
+    a[0] = A.x; a[1] = A.y; a[2] = A.z; a[3] = A.w;
+    bb[0] = Bm.x; bb[1] = Bm.y; bb[2] = Bm.z; bb[3] = Bm.w;
+    bool ok = true;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+        ok = ok && __builtin_isfinite(h[q]);
+        h[q] *= rsc;  // -log2(e) / eta
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) ok = ok && __builtin_isfinite(a[k]) && a[k] > 0.f && __builtin_isfinite(bb[k]) && bb[k] > 0.f;
+    const float poison = ok ? 0.f : __builtin_nanf("");
+    float cm[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cm[j] = 0.25f * ((h[j] + h[4 + j]) + (h[8 + j] + h[12 + j]));
+#pragma unroll
+    for (int j = 0; j < 3; ++j) x[j] = (cm[3] - cm[j]) + lg2(bb[j] * rcp(bb[3])) + poison;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        float u[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) u[j] = h[4 * i + j] + (j < 3 ? x[j] : poison);
+        const float m = __builtin_fmaxf(__builtin_fmaxf(u[0], u[1]), __builtin_fmaxf(u[2], u[3])) + poison;
+        float e[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) e[j] = ex2(u[j] - m);
+        const float sum = (e[0] + e[1]) + (e[2] + e[3]);
+        const float r = rcp(sum);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) S[4 * i + j] = e[j] * r;
+        la[i] = m + lg2(sum);
+    }
+    return ok;
+}
+
+// c_j - b_j with c = sum_i a_i S_ij
+__device__ __forceinline__ void ot_grad(const float S[16], const float a[4], const float bb[4], float g[4]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        g[j] = (__builtin_fmaf(a[0], S[j], a[1] * S[4 + j]) + __builtin_fmaf(a[2], S[8 + j], a[3] * S[12 + j])) - bb[j];
+}
+
+__device__ __forceinline__ Weights ot_weights(const float S[16], const float a[4]) {
+    Weights W = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float t0 = a[i] * S[4 * i], t1 = S[4 * i + 1], t2 = S[4 * i + 2], t3 = S[4 * i + 3];
+        const float t1a = a[i] * t1, t2a = a[i] * t2;
+        W.w01 = __builtin_fmaf(t0, t1, W.w01);
+        W.w02 = __builtin_fmaf(t0, t2, W.w02);
+        W.w03 = __builtin_fmaf(t0, t3, W.w03);
+        W.w12 = __builtin_fmaf(t1a, t2, W.w12);
+        W.w13 = __builtin_fmaf(t1a, t3, W.w13);
+        W.w23 = __builtin_fmaf(t2a, t3, W.w23);
+    }
+    return W;
+}
+
+template <bool WRITE_DUAL, bool WRITE_ITERS>
+__device__ __forceinline__ void ot_store(float* __restrict__ T, float* __restrict__ dual, int32_t* __restrict__ iters,
+                                         int64_t p, const float S[16], const float la[4], const float x[3],
+                                         const float a[4], float eta, int status) {
+    v4f* tp = reinterpret_cast<v4f*>(T) + 4 * p;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        tp[i] = v4f{a[i] * S[4 * i], a[i] * S[4 * i + 1], a[i] * S[4 * i + 2], a[i] * S[4 * i + 3]};
+    if constexpr (WRITE_DUAL) {
+        // alpha_i = eta (ln a_i - lse_i), beta_j = eta x_j (natural units; beta_4 = 0)
+        const float e2 = eta * kLn2;
+        v4f* dp = reinterpret_cast<v4f*>(dual) + 2 * p;
+        dp[0] = v4f{e2 * (lg2(a[0]) - la[0]), e2 * (lg2(a[1]) - la[1]), e2 * (lg2(a[2]) - la[2]),
+                    e2 * (lg2(a[3]) - la[3])};
+        dp[1] = v4f{e2 * x[0], e2 * x[1], e2 * x[2], x[0] * 0.f};
+    }
+    if constexpr (WRITE_ITERS) iters[p] = status;
+}
+
+template <bool WRITE_DUAL, bool WRITE_ITERS>
+__global__ __launch_bounds__(kOtBlock) void ot4_fwd_kernel(const float* __restrict__ M, const float* __restrict__ av,
+                                                          const float* __restrict__ bv, float eta,
+                                                          float* __restrict__ T, float* __restrict__ dual,
+                                                          int32_t* __restrict__ iters, int64_t B, float tol,
+                                                          int max_iter, int64_t per_wave) {
+    const int lane = threadIdx.x & 63;
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const int64_t r0 = (static_cast<int64_t>(blockIdx.x) * kOtWaves + (threadIdx.x >> 6)) * per_wave;
+    if (r0 >= B) return;  // uniform across the wave
+    const int64_t r1 = (r0 + per_wave < B) ? r0 + per_wave : B;
+    int64_t cursor = r0;
+    const float rsc = -kLog2e / eta;
+
+    bool active = false;
+    int64_t p = 0;
+    float S[16], la[4], x[3], a[4], bb[4], g[4], ga[3], o[3];
+    Weights W = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    float lam = 0.f, gn2 = 0.f, t = 1.f, fofs = 0.f, gsum = 0.f, fnoise = 0.f, lmfloor = 0.f;
+    int cnt = 0;
+
+    for (;;) {
+        uint64_t idle = __ballot(!active);
+        while (cursor < r1 && (__popcll(idle) >= kOtRefillMin || idle == ~0ull)) {
+            const int64_t left = r1 - cursor;
+            const int n_idle = __popcll(idle);
+            const int take = (left < n_idle) ? static_cast<int>(left) : n_idle;
+            const int rank = __popcll(idle & below);
+            if (!active && rank < take) {
+                p = cursor + rank;
+                const bool ok = ot_init(M, av, bv, p, rsc, S, la, x, a, bb);
+                ot_grad(S, a, bb, g);
+                const float gmax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(g[0]), __builtin_fabsf(g[1])),
+                                                   __builtin_fmaxf(__builtin_fabsf(g[2]), __builtin_fabsf(g[3])));
+                if (!ok || gmax <= tol || max_iter == 0) {
+                    const int st = !ok ? BIRKHOFF4_NON_FINITE : (gmax <= tol ? 0 : BIRKHOFF4_NOT_CONVERGED);
+                    ot_store<WRITE_DUAL, WRITE_ITERS>(T, dual, iters, p, S, la, x, a, eta, st);
+                } else {
+                    const float mass = (a[0] + a[1]) + (a[2] + a[3]);
+                    fnoise = kFNoise * mass;
+                    lmfloor = kLMFloor * 0.25f * mass;
+                    W = ot_weights(S, a);
+                    ga[0] = g[0]; ga[1] = g[1]; ga[2] = g[2];
+                    o[0] = o[1] = o[2] = 0.f;
+                    gn2 = g[0] * g[0] + g[1] * g[1] + g[2] * g[2] + g[3] * g[3];
+                    lam = __builtin_fmaxf(kLM * gmax, lmfloor);
+                    t = 1.f;
+                    fofs = gsum = 0.f;
+                    cnt = 0;
+                    active = true;
+                }
+            }
+            cursor += take;
+            idle = __ballot(!active);
+        }
+        if (idle == ~0ull) break;
+
+        if (active) {
+            float d0, d1, d2;
+            newton_solve(W, ga[0], ga[1], ga[2], lam, d0, d1, d2);
+            t = __builtin_fminf(t, kCap2 * rcp(__builtin_fmaxf(spread(d0, d1, d2), kTiny)));
+            const float s0 = __builtin_fmaf(t, d0, -o[0]), s1 = __builtin_fmaf(t, d1, -o[1]),
+                        s2 = __builtin_fmaf(t, d2, -o[2]);
+            float l[4], gu[4];
+            evaluate(S, s0, s1, s2, l, gu);  // S renormalised; gu unused (unit-mass sums)
+            ot_grad(S, a, bb, g);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) la[i] += l[i];
+            x[0] += s0; x[1] += s1; x[2] += s2;
+            o[0] += s0; o[1] += s1; o[2] += s2;
+            const float df = fofs + (__builtin_fmaf(a[0], l[0], a[1] * l[1]) + __builtin_fmaf(a[2], l[2], a[3] * l[3])) -
+                             __builtin_fmaf(bb[0], s0, __builtin_fmaf(bb[1], s1, bb[2] * s2));
+            fofs = df;
+            gsum += spread(s0, s1, s2);
+            ++cnt;
+            const float gmax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(g[0]), __builtin_fabsf(g[1])),
+                                               __builtin_fmaxf(__builtin_fabsf(g[2]), __builtin_fabsf(g[3])));
+            const float gn2t = g[0] * g[0] + g[1] * g[1] + g[2] * g[2] + g[3] * g[3];
+            const float slope = ga[0] * d0 + ga[1] * d1 + ga[2] * d2;
+            const bool accept = (df <= kArmijo * t * slope) || (__builtin_fabsf(df) < fnoise && gn2t < gn2);
+            const int evals = cnt & 0xffff;
+            const bool conv = accept && gmax <= tol;
+            if (!conv && evals < max_iter) {
+                if (gsum >= kReviveBits) {
+                    gsum = 0.f;
+                    float smin = S[0];
+#pragma unroll
+                    for (int q = 1; q < 16; ++q) smin = __builtin_fminf(smin, S[q]);
+                    if (smin == 0.f) {
+                        float h[16];
+                        load16_f32(M, p, h);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+#pragma unroll
+                            for (int j = 0; j < 4; ++j)
+                                if (S[4 * i + j] == 0.f)
+                                    S[4 * i + j] = ex2(__builtin_fmaf(h[4 * i + j], rsc, j < 3 ? x[j] : 0.f) - la[i]);
+                    }
+                }
+                if (accept) {
+                    const float dd = g[0] * d0 + g[1] * d1 + g[2] * d2;
+                    const int ts = cnt >> 16;
+                    const bool grow = t >= 0.999f * __builtin_ldexpf(1.f, ts) && dd < 0.25f * slope;
+                    cnt = evals | ((grow ? (ts < kMaxExpandLog2 ? ts + 1 : ts) : 0) << 16);
+                    fofs = 0.f;
+                    o[0] = o[1] = o[2] = 0.f;
+                    gn2 = gn2t;
+                    W = ot_weights(S, a);
+                    ga[0] = g[0]; ga[1] = g[1]; ga[2] = g[2];
+                    lam = __builtin_fmaxf(kLM * gmax, lmfloor);
+                    t = __builtin_ldexpf(1.f, cnt >> 16);
+                } else {
+                    t *= 0.5f;
+                    cnt = evals;
+                    lam = __builtin_fminf(16.f * lam, kMaxShift);
+                }
+            } else {
+                if (!accept) {  // max_iter reached on a rejected trial: back to the accepted point
+                    float l2[4], gu2[4];
+                    evaluate(S, -o[0], -o[1], -o[2], l2, gu2);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) la[i] += l2[i];
+                    x[0] -= o[0]; x[1] -= o[1]; x[2] -= o[2];
+                }
+                ot_store<WRITE_DUAL, WRITE_ITERS>(T, dual, iters, p, S, la, x, a, eta,
+                                                  conv ? evals : BIRKHOFF4_NOT_CONVERGED);
+                active = false;
+            }
+        }
+    }
+}
+
+// Backward of the OT solution (eq. derivative): with W_jk = sum_i T_ij T_ik / a_i and
+// flows F_jk = sum_i T_ij T_ik (G_ij - G_ik) / a_i the potentials w solve the grounded
+// Laplacian system by the edge-flow elimination of the Birkhoff backward, and
+// dL/dM_ij = -T_ij (psi_ij - sum_k T_ik psi_ik / a_i) / eta with psi = G - 1 w^T.
+__global__ __launch_bounds__(kOtBlock) void ot4_bwd_kernel(const float* __restrict__ T, const float* __restrict__ av,
+                                                          const float* __restrict__ dT, float eta,
+                                                          float* __restrict__ dM, int64_t B) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kOtBlock;
+    const float ie = 1.f / eta;
+    for (int64_t p = static_cast<int64_t>(blockIdx.x) * kOtBlock + threadIdx.x; p < B; p += stride) {
+        float t[16], G[16];
+        load16_f32(T, p, t);
+        load16_f32(dT, p, G);
+        const v4f A = load4(av, p);
+        const float ia[4] = {rcp(A.x), rcp(A.y), rcp(A.z), rcp(A.w)};
+        float W[4][4], F[4][4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int k = j + 1; k < 4; ++k) {
+                float sw = 0.f, sf = 0.f;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float q = t[4 * i + j] * (t[4 * i + k] * ia[i]);
+                    sw += q;
+                    sf = __builtin_fmaf(q, G[4 * i + j] - G[4 * i + k], sf);
+                }
+                W[j][k] = W[k][j] = sw;
+                F[j][k] = sf;
+                F[k][j] = -sf;
+            }
+        float ip[3], w[4];
+#pragma unroll
+        for (int pn = 0; pn < 3; ++pn) {
+            float piv = 0.f;
+#pragma unroll
+            for (int k = pn + 1; k < 4; ++k) piv += W[pn][k];
+            ip[pn] = (piv > kPivMin) ? rcp(piv) : 0.f;
+#pragma unroll
+            for (int j = pn + 1; j < 4; ++j)
+#pragma unroll
+                for (int k = j + 1; k < 4; ++k) {
+                    const float fj = W[j][pn] * ip[pn], fk = W[pn][k] * ip[pn];
+                    const float Fn = __builtin_fmaf(fk, F[j][pn], __builtin_fmaf(fj, F[pn][k], F[j][k]));
+                    const float Wn = __builtin_fmaf(fj, W[pn][k], W[j][k]);
+                    W[j][k] = W[k][j] = Wn;
+                    F[j][k] = Fn;
+                    F[k][j] = -Fn;
+                }
+        }
+        w[3] = 0.f;
+#pragma unroll
+        for (int pn = 2; pn >= 0; --pn) {
+            float s = 0.f;
+#pragma unroll
+            for (int k = pn + 1; k < 4; ++k) s += __builtin_fmaf(W[pn][k], w[k], F[pn][k]);
+            w[pn] = s * ip[pn];
+        }
+        float out[16];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float psi[4], mu = 0.f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                psi[j] = G[4 * i + j] - w[j];
+                mu = __builtin_fmaf(t[4 * i + j], psi[j], mu);
+            }
+            mu *= ia[i];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) out[4 * i + j] = -t[4 * i + j] * (psi[j] - mu) * ie;
+        }
+        store16(dM, p, out);
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
 constexpr int kMaxDevices = 64;
@@ -1716,6 +2026,21 @@ int dispatch_fwd8(const void* H, float* P, float* dual, int32_t* iters, int64_t 
     return launch_fwd8<DT, false, false>(H, P, dual, iters, B, tol, max_iter, stream);
 }
 
+// General OT: one range of problems per wave (as for n = 8).
+template <bool WD, bool WI>
+int launch_ot_fwd(const float* M, const float* a, const float* b, float eta, float* T, float* dual, int32_t* iters,
+                  int64_t B, float tol, int max_iter, hipStream_t stream) {
+    const int64_t waves_min = (B + kMaxGrid * kOtWaves - 1) / (kMaxGrid * kOtWaves);
+    int64_t per_wave = (B + kOtRanges - 1) / kOtRanges;
+    if (per_wave < 64) per_wave = 64;
+    if (per_wave < waves_min) per_wave = waves_min;
+    const int64_t waves = (B + per_wave - 1) / per_wave;
+    const int64_t grid = (waves + kOtWaves - 1) / kOtWaves;
+    hipLaunchKernelGGL((ot4_fwd_kernel<WD, WI>), dim3(static_cast<unsigned>(grid)), dim3(kOtBlock), 0, stream, M, a,
+                       b, eta, T, dual, iters, B, tol, max_iter, per_wave);
+    return launch_status();
+}
+
 int64_t grid_for(int64_t B, int block, int cus, int per_cu) {
     int64_t blocks = (B + block - 1) / block;
     const int64_t cap = static_cast<int64_t>(cus) * per_cu;
@@ -1762,6 +2087,48 @@ int birkhoff4_fwd_ex(const void* H, int h_dtype, float* P, float* dual, int32_t*
 int birkhoff4_fwd(const float* H, float* P, float* dual, int64_t B, float tol, int max_iter,
                   hipStream_t stream) {
     return birkhoff4_fwd_ex2(H, BIRKHOFF4_F32, P, dual, nullptr, B, tol, max_iter, BIRKHOFF4_AUTO, stream);
+}
+
+int birkhoff4_ot_fwd(const float* M, const float* a, const float* b, float eta, float* T, float* dual,
+                     int32_t* iters, int64_t B, float tol, int max_iter, hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 64)) return BIRKHOFF4_ERR_SIZE;
+    if (!(eta > 0.f) || !(eta <= 3.0e38f)) return BIRKHOFF4_ERR_ETA;
+    if (!(tol >= 0.f)) return BIRKHOFF4_ERR_TOL;
+    if (max_iter < 0 || max_iter > kMaxIterCap) return BIRKHOFF4_ERR_MAX_ITER;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!M || !a || !b || !T) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(M) || misaligned(a) || misaligned(b) || misaligned(T) || misaligned(dual) || misaligned(iters))
+        return BIRKHOFF4_ERR_ALIGN;
+    const size_t nm = static_cast<size_t>(B) * 64, nv = static_cast<size_t>(B) * 16,
+                 nd = dual ? static_cast<size_t>(B) * 32 : 0, ni = iters ? static_cast<size_t>(B) * 4 : 0;
+    const void* ins[3] = {M, a, b};
+    const size_t nins[3] = {nm, nv, nv};
+    for (int k = 0; k < 3; ++k)
+        if (overlaps(ins[k], nins[k], T, nm) || overlaps(ins[k], nins[k], dual, nd) ||
+            overlaps(ins[k], nins[k], iters, ni))
+            return BIRKHOFF4_ERR_OVERLAP;
+    if (overlaps(T, nm, dual, nd) || overlaps(T, nm, iters, ni) || overlaps(dual, nd, iters, ni))
+        return BIRKHOFF4_ERR_OVERLAP;
+    if (dual && iters) return launch_ot_fwd<true, true>(M, a, b, eta, T, dual, iters, B, tol, max_iter, stream);
+    if (dual) return launch_ot_fwd<true, false>(M, a, b, eta, T, dual, iters, B, tol, max_iter, stream);
+    if (iters) return launch_ot_fwd<false, true>(M, a, b, eta, T, dual, iters, B, tol, max_iter, stream);
+    return launch_ot_fwd<false, false>(M, a, b, eta, T, dual, iters, B, tol, max_iter, stream);
+}
+
+int birkhoff4_ot_bwd(const float* T, const float* a, const float* dT, float eta, float* dM, int64_t B,
+                     hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 64)) return BIRKHOFF4_ERR_SIZE;
+    if (!(eta > 0.f) || !(eta <= 3.0e38f)) return BIRKHOFF4_ERR_ETA;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!T || !a || !dT || !dM) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(T) || misaligned(a) || misaligned(dT) || misaligned(dM)) return BIRKHOFF4_ERR_ALIGN;
+    const size_t nm = static_cast<size_t>(B) * 64, nv = static_cast<size_t>(B) * 16;
+    if (overlaps(dM, nm, T, nm) || overlaps(dM, nm, dT, nm) || overlaps(dM, nm, a, nv)) return BIRKHOFF4_ERR_OVERLAP;
+    const int64_t want = (B + kOtBlock - 1) / kOtBlock;
+    const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
+    hipLaunchKernelGGL(ot4_bwd_kernel, dim3(static_cast<unsigned>(grid)), dim3(kOtBlock), 0, stream, T, a, dT, eta,
+                       dM, B);
+    return launch_status();
 }
 
 int birkhoff8_fwd(const void* H, int h_dtype, float* P, float* dual, int32_t* iters, int64_t B, float tol,
@@ -1897,6 +2264,7 @@ const char* birkhoff4_strerror(int code) {
         case BIRKHOFF4_ERR_DEVICE: return "HIP device query failed";
         case BIRKHOFF4_ERR_LAUNCH: return "kernel launch failed";
         case BIRKHOFF4_ERR_VARIANT: return "unknown forward variant";
+        case BIRKHOFF4_ERR_ETA: return "eta must be positive and finite";
         default: return "unknown error";
     }
 }

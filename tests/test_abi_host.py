@@ -19,6 +19,7 @@ HEADER = os.path.join(ROOT, "include", "birkhoff4.h")
 OK, ERR_NULL, ERR_SIZE, ERR_TOL, ERR_MAX_ITER, ERR_DTYPE, ERR_ALIGN, ERR_OVERLAP, ERR_STEPS = (
     0, -1, -2, -3, -4, -5, -6, -7, -8)
 ERR_VARIANT = -11
+ERR_ETA = -12
 
 A = 0x10000000        # fake, 16-byte aligned device addresses far apart
 Bp = 0x20000000
@@ -44,7 +45,7 @@ def test_every_declared_symbol_is_exported():
 def test_version_and_strerror():
     lib = b4.lib()
     assert lib.birkhoff4_version() >= 100
-    for code in range(-11, 1):
+    for code in range(-12, 1):
         assert lib.birkhoff4_strerror(code)
     assert lib.birkhoff4_strerror(-999) == b"unknown error"
 
@@ -99,6 +100,28 @@ def test_n8_argument_errors():
     assert g(A, None, 0, C, 3, None) == ERR_NULL
     assert g(A, Bp, 5, C, 3, None) == ERR_DTYPE
     assert g(A, Bp, 0, A + 256, 3, None) == ERR_OVERLAP
+
+
+def test_ot_argument_errors():
+    lib = b4.lib()
+    f = lib.birkhoff4_ot_fwd
+    E = 0x50000000
+    assert f(A, Bp, C, 1.0, D, None, None, 0, 1e-6, 20, None) == OK
+    assert f(A, Bp, C, 0.0, D, None, None, 5, 1e-6, 20, None) == ERR_ETA
+    assert f(A, Bp, C, -1.0, D, None, None, 5, 1e-6, 20, None) == ERR_ETA
+    assert f(A, Bp, C, float("inf"), D, None, None, 5, 1e-6, 20, None) == ERR_ETA
+    assert f(A, Bp, C, float("nan"), D, None, None, 5, 1e-6, 20, None) == ERR_ETA
+    assert f(A, None, C, 1.0, D, None, None, 5, 1e-6, 20, None) == ERR_NULL
+    assert f(A, Bp, C, 1.0, D, None, None, 5, -1.0, 20, None) == ERR_TOL
+    assert f(A, Bp + 8, C, 1.0, D, None, None, 5, 1e-6, 20, None) == ERR_ALIGN
+    assert f(A, Bp, C, 1.0, A + 64 * 2, None, None, 5, 1e-6, 20, None) == ERR_OVERLAP  # T inside M
+    assert f(A, Bp, C, 1.0, D, Bp + 16, None, 5, 1e-6, 20, None) == ERR_OVERLAP  # dual inside a
+    assert f(A, Bp, C, 1.0, D, E, D + 64, 5, 1e-6, 20, None) == ERR_OVERLAP      # iters inside T
+    g = lib.birkhoff4_ot_bwd
+    assert g(A, Bp, C, 1.0, D, 0, None) == OK
+    assert g(A, Bp, C, 0.0, D, 5, None) == ERR_ETA
+    assert g(A, Bp, None, 1.0, D, 5, None) == ERR_NULL
+    assert g(A, Bp, C, 1.0, C + 16, 5, None) == ERR_OVERLAP
 
 
 def test_backward_and_baseline_argument_errors():
