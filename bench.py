@@ -87,6 +87,8 @@ def main() -> int:
     ap.add_argument("--no-sk", action="store_true")
     ap.add_argument("--no-n8", action="store_true", help="skip the 8x8 measurement")
     ap.add_argument("--n8-only", action="store_true", help="time only the 8x8 path (for profiler runs)")
+    ap.add_argument("--no-ot", action="store_true", help="skip the general-OT measurement")
+    ap.add_argument("--ot-only", action="store_true", help="time only the general-OT path (for profiler runs)")
     ap.add_argument("--no-extras", action="store_true",
                     help="time only the path (for profiler runs)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -121,6 +123,9 @@ def main() -> int:
         return 0
     if args.n8_only:
         print(json.dumps({"n8": bench_n8(args, dev, torch.cuda.current_stream(dev))}), flush=True)
+        return 0
+    if args.ot_only:
+        print(json.dumps({"ot": bench_ot(args, dev, torch.cuda.current_stream(dev))}), flush=True)
         return 0
     w = workloads.WORKLOADS[args.workload]
     B = w.B
@@ -305,9 +310,109 @@ def main() -> int:
 
     if not args.no_n8:
         out["n8"] = bench_n8(args, dev, stream)
+    if not args.no_ot:
+        out["ot"] = bench_ot(args, dev, stream)
 
     print(json.dumps(out), flush=True)
     return 0
+
+
+OT_B = 1 << 22
+OT_ETA = 0.5
+OT_DESC = ("B=2^22 4x4 entropic OT problems, fp32: cost M = 2 N(0,1), marginals a, b ~ U(0.2, 2) with b rescaled "
+           "to sum(a), eta = 0.5; dT ~ N(0,1); fwd + bwd")
+
+
+def ot_inputs(B: int, seed: int, dev):
+    """The general-OT workload, drawn on the device with torch's seeded generator."""
+    import torch
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    M = 2.0 * torch.randn(B, 4, 4, device=dev, generator=g)
+    a = 0.2 + 1.8 * torch.rand(B, 4, device=dev, generator=g)
+    b = 0.2 + 1.8 * torch.rand(B, 4, device=dev, generator=g)
+    b = (b.double() * (a.double().sum(1) / b.double().sum(1))[:, None]).float()
+    G = torch.randn(B, 4, 4, device=dev, generator=g)
+    return M.contiguous(), a.contiguous(), b.contiguous(), G.contiguous()
+
+
+def bench_ot(args, dev, stream) -> dict:
+    """fwd + bwd of 4x4 entropic OT with general marginals (reported beside the 4x4 path)."""
+    import torch
+
+    import paper_2606_07574_amd as b4
+    B = OT_B
+    M, a, b, G = ot_inputs(B, 4, dev)
+    T = torch.empty(B, 4, 4, device=dev)
+    dual = torch.empty(B, 8, device=dev)
+    dM = torch.empty(B, 4, 4, device=dev)
+    lib = b4.lib()
+    sptr = stream.cuda_stream
+
+    def step():
+        rc = lib.birkhoff4_ot_fwd(M.data_ptr(), a.data_ptr(), b.data_ptr(), OT_ETA, T.data_ptr(), dual.data_ptr(),
+                                  None, B, args.tol, args.max_iter, sptr)
+        if rc:
+            raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+        e_mid.record(stream)
+        rc = lib.birkhoff4_ot_bwd(T.data_ptr(), a.data_ptr(), G.data_ptr(), OT_ETA, dM.data_ptr(), B, sptr)
+        if rc:
+            raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+
+    K = max(3, args.steps // 4)
+    e0, e_mid, e1 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    step()
+    torch.cuda.synchronize()
+    f_ms = b_ms = 0.0
+    for _ in range(K):
+        e0.record(stream)
+        step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        f_ms += e0.elapsed_time(e_mid)
+        b_ms += e_mid.elapsed_time(e1)
+    f_ms /= K
+    b_ms /= K
+    fwd_bytes = B * (64 + 16 + 16 + 64 + 32)
+    bwd_bytes = B * (64 + 16 + 64 + 64)
+    res = {"workload": "ot_b2e22", "B": B, "eta": OT_ETA, "desc": OT_DESC, "steps": K,
+           "value": round(B / ((f_ms + b_ms) * 1e-3), 1), "unit": "problems/s",
+           "fwd_ms": round(f_ms, 4), "bwd_ms": round(b_ms, 4),
+           "kernels": {"ot4_fwd": {"alg_bytes_per_launch": fwd_bytes,
+                                   "achieved_GBs": round(fwd_bytes / (f_ms * 1e-3) / 1e9, 1)},
+                       "ot4_bwd": {"alg_bytes_per_launch": bwd_bytes,
+                                   "achieved_GBs": round(bwd_bytes / (b_ms * 1e-3) / 1e9, 1)}},
+           "path_hbm_frac": round((fwd_bytes + bwd_bytes) / ((f_ms + b_ms) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    if args.ot_only:
+        return res
+    _, _, it = b4.ot_fwd(M, a, b, OT_ETA, args.tol, args.max_iter, want_dual=False, want_iters=True)
+    torch.cuda.synchronize()
+    itn = it.cpu().numpy()
+    conv = itn[itn >= 0]
+    T64 = T.double()
+    res["newton_steps"] = {"mean": round(float(conv.mean()), 3), "p99": int(np.percentile(conv, 99)),
+                           "max": int(conv.max()), "not_converged": int((itn == -1).sum()),
+                           "non_finite": int((itn == -2).sum())}
+    res["max_marginal_err"] = float(torch.maximum((T64.sum(-1) - a.double()).abs().amax(),
+                                                  (T64.sum(-2) - b.double()).abs().amax()).item())
+    del T64
+    log(f"ot: {res['value']:.4g} problems/s fwd {f_ms:.3f} ms bwd {b_ms:.3f} ms; steps {res['newton_steps']}; "
+        f"max marginal {res['max_marginal_err']:.3e}")
+    if not args.no_cpu_baseline:
+        from oracle import birkhoffn
+        n = 1 << 20
+        Ms, As, Bs, Gs = (x[:n].double().cpu().numpy() for x in (M, a, b, G))
+        Bs = Bs * (As.sum(1) / Bs.sum(1))[:, None]
+        threads = max(1, min(16, os.cpu_count() or 1))
+        t0 = time.perf_counter()
+        Tr, _, _ = birkhoffn.ot_fwd(Ms, As, Bs, OT_ETA, threads=threads)
+        birkhoffn.ot_bwd(Tr, As, Gs, OT_ETA, threads=threads)
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": round(n / dt, 1), "unit": "problems/s", "cores": threads, "kind": "oracle",
+                               "sample": f"first {n} problems of ot_b2e22; fp64 OT oracle forward (tol "
+                                         f"{birkhoffn.DEFAULT_TOL:g}) + backward, {threads} threads, {dt:.1f} s"}
+        log(f"ot cpu baseline: {res['cpu_baseline']}")
+    return res
 
 
 N8_B = 1 << 22
