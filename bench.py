@@ -40,10 +40,10 @@ def in_bytes(dtype_is_bf16: bool) -> int:
     return 32 if dtype_is_bf16 else 64
 
 
-def valu_from_profiles(workload: str, kernel: str):
+def valu_from_profiles(workload: str, kernel: str, kind: str = "valu"):
     """VALU lane-instructions per launch counted by rocprofv3 (SQ_INSTS_VALU x 64) for the
-    current kernel source (profiles/valu_<workload>.md), else None."""
-    path = os.path.join(ROOT, "profiles", f"valu_{workload}.md")
+    current kernel source (profiles/<kind>_<workload>.md), else None."""
+    path = os.path.join(ROOT, "profiles", f"{kind}_{workload}.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -383,6 +383,12 @@ def bench_ot(args, dev, stream) -> dict:
                        "ot4_bwd": {"alg_bytes_per_launch": bwd_bytes,
                                    "achieved_GBs": round(bwd_bytes / (b_ms * 1e-3) / 1e9, 1)}},
            "path_hbm_frac": round((fwd_bytes + bwd_bytes) / ((f_ms + b_ms) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    valu = valu_from_profiles("ot_b2e22", "ot4_fwd", "kernel_trace")
+    ach = valu / (f_ms * 1e-3) / 1e12 if valu else None
+    res["roofline"] = {"bound": "alu", "kernel": "ot4_fwd",
+                       "achieved": round(ach, 2) if ach else None, "peak": VALU_PEAK_T,
+                       "unit": "T lane-instr/s", "frac": round(ach / VALU_PEAK_T, 4) if ach else None,
+                       "counted_lane_instr_per_launch": valu}
     if args.ot_only:
         return res
     _, _, it = b4.ot_fwd(M, a, b, OT_ETA, args.tol, args.max_iter, want_dual=False, want_iters=True)
