@@ -1096,21 +1096,20 @@ __global__ __launch_bounds__(64) void sk_bwd_kernel(const void* __restrict__ H,
 // n = 8 (Sec. 3.1 and eq. grad_hess / eq. derivative with n = m = 8): one problem per
 // lane. The forward is the 4 x 4 kernel's iteration written for 7 free potentials (the
 // row-softmax state in product form, trial steps capped in spread, Armijo with the
-// rounding-noise test, Levenberg-Marquardt shift, re-derivation of flushed entries),
-// without lane refill: a wave takes 64 consecutive problems and runs until the slowest
-// is done. The Newton system is the column Laplacian with 28 weights, grounded at
-// column 8 and solved by subtraction-free elimination of nodes 1..7.
+// rounding-noise test, Levenberg-Marquardt shift, re-derivation of flushed entries). A
+// wave owns a range of problems; it initialises them 32 at a time with all its lanes (two
+// lanes per problem) into an LDS ring, and a lane whose problem finishes takes the next
+// one from the ring at once. The Newton system is the column Laplacian with 28 weights,
+// grounded at column 8 and solved by subtraction-free elimination of nodes 1..7.
 // ---------------------------------------------------------------------------
 constexpr int kB8Block = 256;
 constexpr int kB8Waves = kB8Block / 64;
-#ifndef B8_REFILL_MIN
-#define B8_REFILL_MIN 32
-#endif
+constexpr int kB8Ring = 32;  // problems per initialisation batch (= ring slots per wave)
+constexpr int kB8Slot = 23;  // v4f per ring slot (22 used; odd, so that slots start in different banks)
 #ifndef B8_RANGES
 #define B8_RANGES 4096
 #endif
-constexpr int kB8RefillMin = B8_REFILL_MIN;  // idle lanes that trigger a refill
-constexpr int64_t kB8Ranges = B8_RANGES;      // wave ranges per launch (blocks are scheduled dynamically)
+constexpr int64_t kB8Ranges = B8_RANGES;  // wave ranges per launch (blocks are scheduled dynamically)
 
 // Index of the weight of column pair (j, k), j < k < 8, in a packed array of 28.
 __host__ __device__ constexpr int pw8(int j, int k) { return j * 8 - (j * (j + 1)) / 2 + (k - j - 1); }
@@ -1228,52 +1227,6 @@ __device__ __forceinline__ void evaluate8(float T[64], const float s[7], float l
     for (int j = 0; j < 8; ++j) g[j] = colgrad8(T, j);
 }
 
-// Initial point: beta_j = mean_i H_i8 - mean_i H_ij (log2 units), T the row softmax of
-// H log2(e) + 1 beta^T with the row maxima subtracted, a the log2 row normalisers,
-// g the column sums minus one. Returns false for a non-finite input (T, a, beta NaN).
-template <int DT>
-__device__ __forceinline__ bool init8(const void* H, int64_t b, float T[64], float a[8], float beta[7],
-                                      float g[8]) {
-    bool finite = true;
-    float cm[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) cm[j] = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        float h[8];
-        load_row8<DT>(H, b, i, h);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            finite = finite && __builtin_isfinite(h[j]);
-            T[8 * i + j] = h[j] * kLog2e;
-            cm[j] += T[8 * i + j];
-        }
-    }
-    const float poison = finite ? 0.f : __builtin_nanf("");
-#pragma unroll
-    for (int j = 0; j < 7; ++j) beta[j] = 0.125f * (cm[7] - cm[j]) + poison;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        float u[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) u[j] = T[8 * i + j] + (j < 7 ? beta[j] : poison);
-        float m = u[0];
-#pragma unroll
-        for (int j = 1; j < 8; ++j) m = __builtin_fmaxf(m, u[j]);
-        m += poison;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) u[j] = ex2(u[j] - m);
-        const float sum = sum8(u);
-        const float r = rcp(sum);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) T[8 * i + j] = u[j] * r;
-        a[i] = m + lg2(sum);
-    }
-#pragma unroll
-    for (int j = 0; j < 8; ++j) g[j] = colgrad8(T, j);
-    return finite;
-}
-
 template <bool WRITE_DUAL, bool WRITE_ITERS>
 __device__ __forceinline__ void store_output8(float* __restrict__ P, float* __restrict__ dual,
                                               int32_t* __restrict__ iters, int64_t b, const float T[64],
@@ -1291,69 +1244,189 @@ __device__ __forceinline__ void store_output8(float* __restrict__ P, float* __re
     if constexpr (WRITE_ITERS) iters[b] = status;
 }
 
+// Raw storage words of four rows of an 8 x 8 problem (16 for bf16, 32 for fp32).
+template <int DT>
+struct RawWords8 {
+    static constexpr int n = (DT == BIRKHOFF4_BF16) ? 16 : 32;
+};
+
+// Rows 4 hf .. 4 hf + 3 of problem b, undecoded.
+template <int DT>
+__device__ __forceinline__ void load_half8(const void* base, int64_t b, int hf, uint32_t w[RawWords8<DT>::n]) {
+    constexpr int NQ = RawWords8<DT>::n / 4;
+    const v4u* p = reinterpret_cast<const v4u*>(base) + NQ * (2 * b + hf);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+        const v4u r = p[q];
+        w[4 * q + 0] = r.x;
+        w[4 * q + 1] = r.y;
+        w[4 * q + 2] = r.z;
+        w[4 * q + 3] = r.w;
+    }
+}
+
+// Row r (0..3) of the four held in raw words, decoded.
+template <int DT>
+__device__ __forceinline__ void decode_row8(const uint32_t w[RawWords8<DT>::n], int r, float h[8]) {
+    if constexpr (DT == BIRKHOFF4_BF16) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            h[2 * k] = __uint_as_float(w[4 * r + k] << 16);
+            h[2 * k + 1] = __uint_as_float(w[4 * r + k] & 0xffff0000u);
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) h[k] = __uint_as_float(w[8 * r + k]);
+    }
+}
+
+// Sum over the two lanes of a pair (2k, 2k + 1); both receive the same value (the add
+// commutes, and contraction is off so that it is not fused into the caller's product).
+__device__ __forceinline__ float psum(float x) {
+#pragma clang fp contract(off)
+    return x + __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, true));
+}
+
 template <int DT, bool WRITE_DUAL, bool WRITE_ITERS>
-__global__ __launch_bounds__(kB8Block) void newton8_fwd_kernel(const void* __restrict__ H, float* __restrict__ P,
+__global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __restrict__ H, float* __restrict__ P,
                                                                 float* __restrict__ dual,
                                                                 int32_t* __restrict__ iters, int64_t B, float tol,
                                                                 int max_iter, int64_t per_wave) {
+    constexpr int NW = RawWords8<DT>::n;
     const int lane = threadIdx.x & 63;
+    const int hf = lane & 1;  // half of the problem this lane initialises (rows 4 hf .. 4 hf + 3)
+    const int pb = lane >> 1;  // its position in an initialisation batch
+    const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    // The wave owns problems r0 .. r1 - 1 and hands them out to its lanes as they free up.
-    const int64_t r0 = (static_cast<int64_t>(blockIdx.x) * kB8Waves + (threadIdx.x >> 6)) * per_wave;
+    // Per-wave ring: slot p holds the initial point of position p of the last batch: row
+    // 4 h + r of T in v4f 4 r + 2 h and 4 r + 2 h + 1 (the two lanes of a pair write
+    // different banks), a (16..17), beta_1..4 (18), beta_5..7 and the offset (19), g
+    // (20..21); order[0 .. nfresh) lists the positions whose problems still need steps.
+    __shared__ v4f ring_all[kB8Waves][kB8Ring * kB8Slot];
+    __shared__ int32_t order_all[kB8Waves][kB8Ring];
+    v4f* const ring = ring_all[wv];
+    int32_t* const order = order_all[wv];
+    // The wave owns problems r0 .. r1 - 1.
+    const int64_t r0 = (static_cast<int64_t>(blockIdx.x) * kB8Waves + wv) * per_wave;
     if (r0 >= B) return;  // uniform across the wave
     const int64_t r1 = (r0 + per_wave < B) ? r0 + per_wave : B;
-    int64_t cursor = r0;  // next unclaimed problem (uniform)
+
+    // Raw words of the batch to initialise next (two lanes per problem), one batch ahead.
+    uint32_t raw[NW];
+#pragma unroll
+    for (int q = 0; q < NW; ++q) raw[q] = 0u;
+    int64_t bnext = r0;  // first problem of that batch (uniform)
+    if (bnext + pb < r1) load_half8<DT>(H, bnext + pb, hf, raw);
+    int nfresh = 0, icur = 0;  // order[icur .. nfresh) not yet taken
 
     bool active = false;  // holds an unfinished problem
-    int64_t b = 0;
+    bool setup = false;   // its Newton system must be formed at the current point
+    int32_t rel = 0;      // problem offset from r0
     float T[64], a[8], beta[7], g[8], W[28], ga[7], o[7];
+#pragma unroll
+    for (int q = 0; q < 64; ++q) T[q] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) a[j] = g[j] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 7; ++j) beta[j] = ga[j] = o[j] = 0.f;
+#pragma unroll
+    for (int k = 0; k < 28; ++k) W[k] = 0.f;
     float lam = 0.f, gn2 = 0.f, t = 1.f, fofs = 0.f, gsum = 0.f;
     int cnt = 0;  // bits 0-15: trial steps; bits 16-18: log2 of the initial trial step
+
+    // Initialise the loaded batch with the whole wave, two lanes per problem: column means
+    // and the finiteness test are combined over the pair, each lane forms the row softmax
+    // of its four rows straight into the problem's ring slot, and the column sums are
+    // combined again. Problems already within tol there (or non-finite, or max_iter = 0)
+    // are written out from the slot; the others are listed for the lanes to take.
+    auto init_batch = [&]() {
 #pragma unroll
-    for (int j = 0; j < 7; ++j) o[j] = 0.f;
+        for (int q = 0; q < NW; ++q) asm volatile("" : "+v"(raw[q])::"memory");
+        const int64_t bp = bnext + pb;
+        const bool valid = bp < r1;
+        float cm[8];
+        bool fin = true;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) cm[j] = 0.f;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            float h[8];
+            decode_row8<DT>(raw, r, h);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                fin = fin && __builtin_isfinite(h[j]);
+                cm[j] += h[j] * kLog2e;
+            }
+        }
+        fin = fin && __builtin_amdgcn_mov_dpp(static_cast<int>(fin), 0xB1, 0xF, 0xF, true);
+        const float poison = fin ? 0.f : __builtin_nanf("");
+#pragma unroll
+        for (int j = 0; j < 8; ++j) cm[j] = psum(cm[j]);
+        float bi[7];
+#pragma unroll
+        for (int j = 0; j < 7; ++j) bi[j] = 0.125f * (cm[7] - cm[j]) + poison;
+        v4f* const sl = ring + pb * kB8Slot;
+        float ai[4], gi[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) gi[j] = 0.f;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            float u[8];
+            decode_row8<DT>(raw, r, u);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) u[j] = __builtin_fmaf(u[j], kLog2e, j < 7 ? bi[j] : poison);
+            float m = u[0];
+#pragma unroll
+            for (int j = 1; j < 8; ++j) m = __builtin_fmaxf(m, u[j]);
+            m += poison;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) u[j] = ex2(u[j] - m);
+            const float sum = sum8(u);
+            const float rc = rcp(sum);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                u[j] *= rc;
+                gi[j] += u[j];
+            }
+            ai[r] = m + lg2(sum);
+            sl[4 * r + 2 * hf] = v4f{u[0], u[1], u[2], u[3]};
+            sl[4 * r + 2 * hf + 1] = v4f{u[4], u[5], u[6], u[7]};
+        }
+        float gmax = 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            gi[j] = psum(gi[j]) - 1.0f;
+            gmax = __builtin_fmaxf(gmax, __builtin_fabsf(gi[j]));
+        }
+        sl[16 + hf] = v4f{ai[0], ai[1], ai[2], ai[3]};
+        sl[18 + hf] = hf ? v4f{bi[4], bi[5], bi[6], __int_as_float(static_cast<int32_t>(bp - r0))}
+                         : v4f{bi[0], bi[1], bi[2], bi[3]};
+        sl[20 + hf] = hf ? v4f{gi[4], gi[5], gi[6], gi[7]} : v4f{gi[0], gi[1], gi[2], gi[3]};
+        const bool conv = gmax <= tol;
+        const bool done = valid && (!fin || conv || max_iter == 0);
+        const bool fresh = valid && !done;
+        const uint64_t fm = __ballot(fresh && hf == 0);
+        if (fresh && hf == 0) order[__popcll(fm & below)] = pb;
+        nfresh = __popcll(fm);
+        icur = 0;
+        if (done) {
+            v4f* pp = reinterpret_cast<v4f*>(P) + 16 * bp + 8 * hf;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) pp[q] = sl[4 * (q >> 1) + 2 * hf + (q & 1)];
+            if constexpr (WRITE_DUAL) {
+                v4f* dp = reinterpret_cast<v4f*>(dual) + 4 * bp;
+                dp[hf] = v4f{-ai[0] * kLn2, -ai[1] * kLn2, -ai[2] * kLn2, -ai[3] * kLn2};
+                dp[2 + hf] = hf ? v4f{bi[4] * kLn2, bi[5] * kLn2, bi[6] * kLn2, bi[0] * 0.f}  // beta_8 = 0
+                                : v4f{bi[0] * kLn2, bi[1] * kLn2, bi[2] * kLn2, bi[3] * kLn2};
+            }
+            if constexpr (WRITE_ITERS)
+                if (hf == 0) iters[bp] = !fin ? BIRKHOFF4_NON_FINITE : (conv ? 0 : BIRKHOFF4_NOT_CONVERGED);
+        }
+        bnext += kB8Ring;
+        if (bnext + pb < r1) load_half8<DT>(H, bnext + pb, hf, raw);
+    };
 
     for (;;) {
-        // Refill: once enough lanes are idle (or none is working), idle lanes take the next
-        // problems of the range and evaluate their initial points; problems already within
-        // tol there (or non-finite, or max_iter = 0) are written at once and the lane takes
-        // another.
-        uint64_t idle = __ballot(!active);
-        while (cursor < r1 && (__popcll(idle) >= kB8RefillMin || idle == ~0ull)) {
-            const int64_t left = r1 - cursor;
-            const int n_idle = __popcll(idle);
-            const int take = (left < n_idle) ? static_cast<int>(left) : n_idle;
-            const int rank = __popcll(idle & below);
-            if (!active && rank < take) {
-                b = cursor + rank;
-                const bool finite = init8<DT>(H, b, T, a, beta, g);
-                float gmax = 0.f;
-#pragma unroll
-                for (int j = 0; j < 8; ++j) gmax = __builtin_fmaxf(gmax, __builtin_fabsf(g[j]));
-                if (!finite || gmax <= tol || max_iter == 0) {
-                    const int st = !finite ? BIRKHOFF4_NON_FINITE : (gmax <= tol ? 0 : BIRKHOFF4_NOT_CONVERGED);
-                    store_output8<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, b, T, a, beta, st);
-                } else {
-                    weights8(T, W);
-                    gn2 = 0.f;
-#pragma unroll
-                    for (int j = 0; j < 7; ++j) {
-                        ga[j] = g[j];
-                        o[j] = 0.f;
-                    }
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) gn2 = __builtin_fmaf(g[j], g[j], gn2);
-                    lam = __builtin_fmaxf(kLM * gmax, kLMFloor);
-                    t = 1.f;
-                    fofs = gsum = 0.f;
-                    cnt = 0;
-                    active = true;
-                }
-            }
-            cursor += take;
-            idle = __ballot(!active);
-        }
-        if (idle == ~0ull) break;  // nothing left in the range and no lane working
-
         if (active) {
             float d[7], s[7], l[8];
             newton_solve8(W, ga, lam, d);
@@ -1398,7 +1471,7 @@ __global__ __launch_bounds__(kB8Block) void newton8_fwd_kernel(const void* __res
 #pragma unroll
                         for (int i = 0; i < 8; ++i) {
                             float h[8];
-                            load_row8<DT>(H, b, i, h);
+                            load_row8<DT>(H, r0 + rel, i, h);
 #pragma unroll
                             for (int j = 0; j < 8; ++j)
                                 if (T[8 * i + j] == 0.f)
@@ -1415,14 +1488,9 @@ __global__ __launch_bounds__(kB8Block) void newton8_fwd_kernel(const void* __res
                     cnt = evals | ((grow ? (ts < kMaxExpandLog2 ? ts + 1 : ts) : 0) << 16);
                     fofs = 0.f;
 #pragma unroll
-                    for (int j = 0; j < 7; ++j) {
-                        o[j] = 0.f;
-                        ga[j] = g[j];
-                    }
-                    gn2 = gn2t;
-                    weights8(T, W);
-                    lam = __builtin_fmaxf(kLM * gmax, kLMFloor);
+                    for (int j = 0; j < 7; ++j) o[j] = 0.f;
                     t = __builtin_ldexpf(1.f, cnt >> 16);
+                    setup = true;
                 } else {
                     t *= 0.5f;
                     cnt = evals;
@@ -1439,11 +1507,68 @@ __global__ __launch_bounds__(kB8Block) void newton8_fwd_kernel(const void* __res
 #pragma unroll
                     for (int j = 0; j < 7; ++j) beta[j] -= o[j];
                 }
-                store_output8<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, b, T, a, beta,
+                store_output8<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, r0 + rel, T, a, beta,
                                                        conv ? evals : BIRKHOFF4_NOT_CONVERGED);
                 active = false;
             }
         }
+        // Hand-off: every idle lane takes the next listed problem of the ring; batches are
+        // initialised as the list runs out.
+        uint64_t wm = __ballot(!active);
+        while (wm != 0) {
+            const int k = __popcll(wm);
+            const int rank = __popcll(wm & below);
+            const int avail = nfresh - icur;
+            if (!active && rank < avail) {
+                const v4f* sl = ring + order[icur + rank] * kB8Slot;
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {  // v4f q holds half (q & 1) of row 4 ((q >> 1) & 1) + (q >> 2)
+                    const v4f r = sl[q];
+                    const int e = 8 * (4 * ((q >> 1) & 1) + (q >> 2)) + 4 * (q & 1);
+                    T[e] = r.x; T[e + 1] = r.y; T[e + 2] = r.z; T[e + 3] = r.w;
+                }
+                const v4f a0 = sl[16], a1 = sl[17], b0 = sl[18], b1 = sl[19], g0 = sl[20], g1 = sl[21];
+                a[0] = a0.x; a[1] = a0.y; a[2] = a0.z; a[3] = a0.w;
+                a[4] = a1.x; a[5] = a1.y; a[6] = a1.z; a[7] = a1.w;
+                beta[0] = b0.x; beta[1] = b0.y; beta[2] = b0.z; beta[3] = b0.w;
+                beta[4] = b1.x; beta[5] = b1.y; beta[6] = b1.z;
+                rel = __float_as_int(b1.w);
+                g[0] = g0.x; g[1] = g0.y; g[2] = g0.z; g[3] = g0.w;
+                g[4] = g1.x; g[5] = g1.y; g[6] = g1.z; g[7] = g1.w;
+#pragma unroll
+                for (int j = 0; j < 7; ++j) o[j] = 0.f;
+                t = 1.f;
+                fofs = gsum = 0.f;
+                cnt = 0;
+                active = true;
+                setup = true;
+            }
+            if (k <= avail) {
+                icur += k;
+                break;
+            }
+            icur = nfresh;
+            if (bnext >= r1) break;  // nothing left to initialise
+            init_batch();
+            wm = __ballot(!active);
+        }
+        // Newton system at the new accepted point, for lanes that accepted a trial and
+        // lanes that took a fresh problem alike.
+        if (setup) {
+            weights8(T, W);
+            float gmax = 0.f, s2 = 0.f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                gmax = __builtin_fmaxf(gmax, __builtin_fabsf(g[j]));
+                s2 = __builtin_fmaf(g[j], g[j], s2);
+            }
+#pragma unroll
+            for (int j = 0; j < 7; ++j) ga[j] = g[j];
+            gn2 = s2;
+            lam = __builtin_fmaxf(kLM * gmax, kLMFloor);
+            setup = false;
+        }
+        if (__ballot(active) == 0) break;
     }
 }
 
@@ -1606,13 +1731,17 @@ __global__ __launch_bounds__(kB8Block, 2) void implicit8_bwd_kernel(const float*
 // Birkhoff iteration carries over with the row masses and column targets: the same
 // product-form trials (S updated in place), spread cap, Armijo test on
 // f = sum_i a_i lse_i - sum_j b_j x_j, Levenberg-Marquardt shift and re-derivation of
-// flushed entries. One problem per lane; each wave owns a range of problems and refills
-// its lanes from it (as the 8 x 8 kernel does).
+// flushed entries. One problem per lane; each wave owns a range of problems, initialises
+// them 64 at a time with all its lanes into an LDS ring, and a lane whose problem finishes
+// takes the next one from the ring at once.
 // ---------------------------------------------------------------------------
 constexpr int kOtBlock = 256;
 constexpr int kOtWaves = kOtBlock / 64;
-constexpr int kOtRefillMin = 16;
-constexpr int64_t kOtRanges = 8192;
+constexpr int kOtSlot = 8;  // v4f per ring slot
+#ifndef OT_RANGES
+#define OT_RANGES 16384
+#endif
+constexpr int64_t kOtRanges = OT_RANGES;  // wave ranges per launch
 
 __device__ __forceinline__ v4f load4(const float* base, int64_t b) { return reinterpret_cast<const v4f*>(base)[b]; }
 
@@ -1707,56 +1836,74 @@ __global__ __launch_bounds__(kOtBlock) void ot4_fwd_kernel(const float* __restri
                                                           int32_t* __restrict__ iters, int64_t B, float tol,
                                                           int max_iter, int64_t per_wave) {
     const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    const int64_t r0 = (static_cast<int64_t>(blockIdx.x) * kOtWaves + (threadIdx.x >> 6)) * per_wave;
+    // Per-wave ring of 64 slots: S rows (v4f 0..3), la (4), x and the problem's offset (5),
+    // a (6), b (7) of a problem not finished at its initial point.
+    __shared__ v4f ring_all[kOtWaves][64 * kOtSlot];
+    v4f* const ring = ring_all[wv];
+    const int64_t r0 = (static_cast<int64_t>(blockIdx.x) * kOtWaves + wv) * per_wave;
     if (r0 >= B) return;  // uniform across the wave
     const int64_t r1 = (r0 + per_wave < B) ? r0 + per_wave : B;
-    int64_t cursor = r0;
+    int64_t bnext = r0;        // first problem of the next batch to initialise (uniform)
+    int nfresh = 0, icur = 0;  // ring slots [icur, nfresh) not yet taken
     const float rsc = -kLog2e / eta;
 
-    bool active = false;
-    int64_t p = 0;
+    bool active = false;  // holds an unfinished problem
+    bool setup = false;   // its Newton system must be formed at the current point
+    int32_t rel = 0;      // problem offset from r0
     float S[16], la[4], x[3], a[4], bb[4], g[4], ga[3], o[3];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) S[q] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) la[j] = a[j] = bb[j] = g[j] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 3; ++j) x[j] = ga[j] = o[j] = 0.f;
     Weights W = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     float lam = 0.f, gn2 = 0.f, t = 1.f, fofs = 0.f, gsum = 0.f, fnoise = 0.f, lmfloor = 0.f;
     int cnt = 0;
 
-    for (;;) {
-        uint64_t idle = __ballot(!active);
-        while (cursor < r1 && (__popcll(idle) >= kOtRefillMin || idle == ~0ull)) {
-            const int64_t left = r1 - cursor;
-            const int n_idle = __popcll(idle);
-            const int take = (left < n_idle) ? static_cast<int>(left) : n_idle;
-            const int rank = __popcll(idle & below);
-            if (!active && rank < take) {
-                p = cursor + rank;
-                const bool ok = ot_init(M, av, bv, p, rsc, S, la, x, a, bb);
-                ot_grad(S, a, bb, g);
-                const float gmax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(g[0]), __builtin_fabsf(g[1])),
-                                                   __builtin_fmaxf(__builtin_fabsf(g[2]), __builtin_fabsf(g[3])));
-                if (!ok || gmax <= tol || max_iter == 0) {
-                    const int st = !ok ? BIRKHOFF4_NON_FINITE : (gmax <= tol ? 0 : BIRKHOFF4_NOT_CONVERGED);
-                    ot_store<WRITE_DUAL, WRITE_ITERS>(T, dual, iters, p, S, la, x, a, eta, st);
-                } else {
-                    const float mass = (a[0] + a[1]) + (a[2] + a[3]);
-                    fnoise = kFNoise * mass;
-                    lmfloor = kLMFloor * 0.25f * mass;
-                    W = ot_weights(S, a);
-                    ga[0] = g[0]; ga[1] = g[1]; ga[2] = g[2];
-                    o[0] = o[1] = o[2] = 0.f;
-                    gn2 = g[0] * g[0] + g[1] * g[1] + g[2] * g[2] + g[3] * g[3];
-                    lam = __builtin_fmaxf(kLM * gmax, lmfloor);
-                    t = 1.f;
-                    fofs = gsum = 0.f;
-                    cnt = 0;
-                    active = true;
-                }
-            }
-            cursor += take;
-            idle = __ballot(!active);
+    // Initialise the next 64 problems with the whole wave (one per lane). Those already
+    // within tol (or invalid, or max_iter = 0) are written out; the others are compacted
+    // into ring slots 0 .. nfresh - 1.
+    auto init_batch = [&]() {
+        const int64_t p = bnext + lane;
+        const bool valid = p < r1;
+        float Si[16], lai[4], xi[3], ai[4], bi[4], gi[4];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) Si[q] = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) lai[j] = ai[j] = bi[j] = 0.f;
+#pragma unroll
+        for (int j = 0; j < 3; ++j) xi[j] = 0.f;
+        bool ok = false;
+        if (valid) ok = ot_init(M, av, bv, p, rsc, Si, lai, xi, ai, bi);
+        ot_grad(Si, ai, bi, gi);
+        const float gmax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(gi[0]), __builtin_fabsf(gi[1])),
+                                           __builtin_fmaxf(__builtin_fabsf(gi[2]), __builtin_fabsf(gi[3])));
+        const bool done = valid && (!ok || gmax <= tol || max_iter == 0);
+        const bool fresh = valid && !done;
+        const uint64_t fm = __ballot(fresh);
+        if (fresh) {
+            v4f* sl = ring + __popcll(fm & below) * kOtSlot;
+            sl[0] = v4f{Si[0], Si[1], Si[2], Si[3]};
+            sl[1] = v4f{Si[4], Si[5], Si[6], Si[7]};
+            sl[2] = v4f{Si[8], Si[9], Si[10], Si[11]};
+            sl[3] = v4f{Si[12], Si[13], Si[14], Si[15]};
+            sl[4] = v4f{lai[0], lai[1], lai[2], lai[3]};
+            sl[5] = v4f{xi[0], xi[1], xi[2], __int_as_float(static_cast<int32_t>(p - r0))};
+            sl[6] = v4f{ai[0], ai[1], ai[2], ai[3]};
+            sl[7] = v4f{bi[0], bi[1], bi[2], bi[3]};
         }
-        if (idle == ~0ull) break;
+        if (done)
+            ot_store<WRITE_DUAL, WRITE_ITERS>(T, dual, iters, p, Si, lai, xi, ai, eta,
+                                              !ok ? BIRKHOFF4_NON_FINITE : (gmax <= tol ? 0 : BIRKHOFF4_NOT_CONVERGED));
+        nfresh = __popcll(fm);
+        icur = 0;
+        bnext += 64;
+    };
 
+    for (;;) {
         if (active) {
             float d0, d1, d2;
             newton_solve(W, ga[0], ga[1], ga[2], lam, d0, d1, d2);
@@ -1790,7 +1937,7 @@ __global__ __launch_bounds__(kOtBlock) void ot4_fwd_kernel(const float* __restri
                     for (int q = 1; q < 16; ++q) smin = __builtin_fminf(smin, S[q]);
                     if (smin == 0.f) {
                         float h[16];
-                        load16_f32(M, p, h);
+                        load16_f32(M, r0 + rel, h);
 #pragma unroll
                         for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -1806,11 +1953,8 @@ __global__ __launch_bounds__(kOtBlock) void ot4_fwd_kernel(const float* __restri
                     cnt = evals | ((grow ? (ts < kMaxExpandLog2 ? ts + 1 : ts) : 0) << 16);
                     fofs = 0.f;
                     o[0] = o[1] = o[2] = 0.f;
-                    gn2 = gn2t;
-                    W = ot_weights(S, a);
-                    ga[0] = g[0]; ga[1] = g[1]; ga[2] = g[2];
-                    lam = __builtin_fmaxf(kLM * gmax, lmfloor);
                     t = __builtin_ldexpf(1.f, cnt >> 16);
+                    setup = true;
                 } else {
                     t *= 0.5f;
                     cnt = evals;
@@ -1824,11 +1968,63 @@ __global__ __launch_bounds__(kOtBlock) void ot4_fwd_kernel(const float* __restri
                     for (int i = 0; i < 4; ++i) la[i] += l2[i];
                     x[0] -= o[0]; x[1] -= o[1]; x[2] -= o[2];
                 }
-                ot_store<WRITE_DUAL, WRITE_ITERS>(T, dual, iters, p, S, la, x, a, eta,
+                ot_store<WRITE_DUAL, WRITE_ITERS>(T, dual, iters, r0 + rel, S, la, x, a, eta,
                                                   conv ? evals : BIRKHOFF4_NOT_CONVERGED);
                 active = false;
             }
         }
+        // Hand-off: every idle lane takes the next problem of the ring; batches are
+        // initialised as the ring runs out.
+        uint64_t wm = __ballot(!active);
+        while (wm != 0) {
+            const int k = __popcll(wm);
+            const int rank = __popcll(wm & below);
+            const int avail = nfresh - icur;
+            if (!active && rank < avail) {
+                const v4f* sl = ring + (icur + rank) * kOtSlot;
+                const v4f q0 = sl[0], q1 = sl[1], q2 = sl[2], q3 = sl[3], lv = sl[4], xv = sl[5], av4 = sl[6],
+                          bv4 = sl[7];
+                S[0] = q0.x; S[1] = q0.y; S[2] = q0.z; S[3] = q0.w;
+                S[4] = q1.x; S[5] = q1.y; S[6] = q1.z; S[7] = q1.w;
+                S[8] = q2.x; S[9] = q2.y; S[10] = q2.z; S[11] = q2.w;
+                S[12] = q3.x; S[13] = q3.y; S[14] = q3.z; S[15] = q3.w;
+                la[0] = lv.x; la[1] = lv.y; la[2] = lv.z; la[3] = lv.w;
+                x[0] = xv.x; x[1] = xv.y; x[2] = xv.z;
+                rel = __float_as_int(xv.w);
+                a[0] = av4.x; a[1] = av4.y; a[2] = av4.z; a[3] = av4.w;
+                bb[0] = bv4.x; bb[1] = bv4.y; bb[2] = bv4.z; bb[3] = bv4.w;
+                ot_grad(S, a, bb, g);
+                const float mass = (a[0] + a[1]) + (a[2] + a[3]);
+                fnoise = kFNoise * mass;
+                lmfloor = kLMFloor * 0.25f * mass;
+                o[0] = o[1] = o[2] = 0.f;
+                t = 1.f;
+                fofs = gsum = 0.f;
+                cnt = 0;
+                active = true;
+                setup = true;
+            }
+            if (k <= avail) {
+                icur += k;
+                break;
+            }
+            icur = nfresh;
+            if (bnext >= r1) break;  // nothing left to initialise
+            init_batch();
+            wm = __ballot(!active);
+        }
+        // Newton system at the new accepted point, for lanes that accepted a trial and
+        // lanes that took a fresh problem alike.
+        if (setup) {
+            W = ot_weights(S, a);
+            const float gmax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(g[0]), __builtin_fabsf(g[1])),
+                                               __builtin_fmaxf(__builtin_fabsf(g[2]), __builtin_fabsf(g[3])));
+            gn2 = g[0] * g[0] + g[1] * g[1] + g[2] * g[2] + g[3] * g[3];
+            ga[0] = g[0]; ga[1] = g[1]; ga[2] = g[2];
+            lam = __builtin_fmaxf(kLM * gmax, lmfloor);
+            setup = false;
+        }
+        if (__ballot(active) == 0) break;
     }
 }
 

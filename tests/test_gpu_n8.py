@@ -61,7 +61,7 @@ def check(H, P, dual, G=None, dH=None, label=""):
         assert e.max() <= TOL_DH
 
 
-@pytest.mark.parametrize("sigma", [0.1, 1.0, 5.0, 20.0, 50.0])
+@pytest.mark.parametrize("sigma", [0.1, 1.0, 5.0, 20.0, 50.0, 100.0])
 def test_scales(sigma):
     say(f"test: n=8 gauss sigma={sigma}")
     H, G = gauss8(6000, sigma, seed=int(10 * sigma) + 1)
@@ -80,11 +80,13 @@ def test_ragged_batches(B):
     check(H, P, dual, G, dH, f"B={B}")
 
 
-def test_near_permutations():
-    say("test: n=8 near-permutations")
-    H = near_perm8(5000, 20.0, 0.1, seed=5)
+@pytest.mark.parametrize("gap,noise", [(20.0, 0.1), (8.0, 1.0), (3.0, 1.0), (60.0, 0.1)])
+def test_near_permutations(gap, noise):
+    say(f"test: n=8 near-permutations gap={gap} noise={noise}")
+    H = near_perm8(5000, gap, noise, seed=int(gap + 10 * noise))
     G = np.random.default_rng(6).standard_normal(H.shape).astype(np.float32)
     P, dual, it, dH = run(H, G)
+    say(f"  iters: mean={it.mean():.2f} max={it.max()} failed={(it < 0).sum()}")
     assert (it >= 0).all()
     check(H, P, dual, G, dH, "near-perm")
 

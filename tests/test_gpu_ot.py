@@ -71,6 +71,24 @@ def test_parity(eta, scale):
     check(M, a, b, eta, T, dual, G, dM, f"eta={eta}")
 
 
+@pytest.mark.parametrize("eta,scale", [(0.1, 1.0), (0.5, 2.0), (0.1, 5.0), (0.02, 1.0)])
+def test_wide_marginals(eta, scale):
+    # a and b log-uniform over three decades (1e-3 .. 1), so rows and columns of T differ in
+    # mass by up to 1000x; cost over eta reaches logit scales of 50
+    say(f"test: OT marginals over three decades, eta={eta} cost scale={scale}")
+    rng = np.random.default_rng(int(1000 * eta + scale))
+    B = 20000
+    M = (scale * rng.standard_normal((B, 4, 4))).astype(np.float32)
+    a = np.exp(rng.uniform(np.log(1e-3), 0.0, (B, 4))).astype(np.float32)
+    b = np.exp(rng.uniform(np.log(1e-3), 0.0, (B, 4)))
+    b = (b * (a.astype(np.float64).sum(1) / b.sum(1))[:, None]).astype(np.float32)
+    G = rng.standard_normal((B, 4, 4)).astype(np.float32)
+    T, dual, it, dM = run(M, a, b, eta, G, max_iter=256)
+    say(f"  iters mean={it.mean():.2f} max={it.max()} failed={(it < 0).sum()}")
+    assert (it >= 0).all()
+    check(M, a, b, eta, T, dual, G, dM, f"wide eta={eta}")
+
+
 def test_birkhoff_special_case():
     say("test: OT with M = -H, a = b = 1, eta = 1 reproduces the projection")
     rng = np.random.default_rng(3)
