@@ -195,21 +195,31 @@ def main() -> int:
     fwd_bytes = B * (in_bytes(bf16) + 64 + 32)
     bwd_bytes = B * (64 + in_bytes(bf16) + 64)
     kernels = {"newton_fwd": {"avg_ms": fwd_ms, "alg_bytes_per_launch": fwd_bytes,
-                              "achieved_GBs": fwd_bytes / (fwd_ms * 1e-3) / 1e9}}
+                              "achieved_GBs": fwd_bytes / (fwd_ms * 1e-3) / 1e9,
+                              "proj_per_s": B / (fwd_ms * 1e-3)}}
     if w.grad:
         kernels["implicit_bwd"] = {"avg_ms": bwd_ms, "alg_bytes_per_launch": bwd_bytes,
-                                   "achieved_GBs": bwd_bytes / (bwd_ms * 1e-3) / 1e9}
+                                   "achieved_GBs": bwd_bytes / (bwd_ms * 1e-3) / 1e9,
+                                   "proj_per_s": B / (bwd_ms * 1e-3)}
     dominant = max(kernels, key=lambda k: kernels[k]["avg_ms"])
     traffic = traffic_from_profiles(w.name)
     ach = kernels[dominant]["achieved_GBs"]
     roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
                 "traffic": (traffic or {}).get(dominant)}
+    # the forward is bound by its write requests and its VALU work together: its VALU issue
+    # rate (lane-instructions counted by rocprofv3 on this source) is reported beside the bytes
+    valu = valu_from_profiles(w.name, dominant, "traffic")
+    if valu:
+        va = valu / (kernels[dominant]["avg_ms"] * 1e-3) / 1e12
+        roofline["valu"] = {"achieved": round(va, 2), "peak": VALU_PEAK_T, "unit": "T lane-instr/s",
+                            "frac": round(va / VALU_PEAK_T, 4), "counted_lane_instr_per_launch": valu}
     path_bytes = fwd_bytes + (bwd_bytes if w.grad else 0)
     out = {
         "metric": METRIC if w.name == "mix_bf16_b2e24" else f"4x4 Birkhoff projections/sec ({w.name})",
         "value": round(value, 1), "unit": "proj/s", "n_gpus": 1, "steps": K, "warmup": W,
-        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "ms_per_step": round(ms_per_step, 4), "fwd_proj_per_s": round(B / (fwd_ms * 1e-3), 1),
+        "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": w.name, "B": B, "storage": w.storage, "tol": args.tol,
                    "max_iter": args.max_iter, "passes": "fwd+bwd" if w.grad else "fwd",
