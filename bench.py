@@ -333,26 +333,14 @@ OT_DESC = ("B=2^22 4x4 entropic OT problems, fp32: cost M = 2 N(0,1), marginals 
            "to sum(a), eta = 0.5; dT ~ N(0,1); fwd + bwd")
 
 
-def ot_inputs(B: int, seed: int, dev):
-    """The general-OT workload, drawn on the device with torch's seeded generator."""
-    import torch
-    g = torch.Generator(device=dev)
-    g.manual_seed(seed)
-    M = 2.0 * torch.randn(B, 4, 4, device=dev, generator=g)
-    a = 0.2 + 1.8 * torch.rand(B, 4, device=dev, generator=g)
-    b = 0.2 + 1.8 * torch.rand(B, 4, device=dev, generator=g)
-    b = (b.double() * (a.double().sum(1) / b.double().sum(1))[:, None]).float()
-    G = torch.randn(B, 4, 4, device=dev, generator=g)
-    return M.contiguous(), a.contiguous(), b.contiguous(), G.contiguous()
-
-
 def bench_ot(args, dev, stream) -> dict:
     """fwd + bwd of 4x4 entropic OT with general marginals (reported beside the 4x4 path)."""
     import torch
 
     import paper_2606_07574_amd as b4
+    import workloads
     B = OT_B
-    M, a, b, G = ot_inputs(B, 4, dev)
+    M, a, b, G = workloads.ot_device(B, 4, dev)
     T = torch.empty(B, 4, 4, device=dev)
     dual = torch.empty(B, 8, device=dev)
     dM = torch.empty(B, 4, 4, device=dev)
@@ -436,28 +424,14 @@ N8_DESC = ("B=2^22 8x8 matrices, bf16 storage, fp32 compute; half sigma*N(0,1) w
            "half 20*Pi + 0.1 N(0,1) (Pi a random permutation); dP ~ N(0,1) bf16; fwd + bwd")
 
 
-def n8_inputs(B: int, seed: int, dev):
-    """The 8x8 mixture, drawn on the device with torch's seeded generator."""
-    import torch
-    g = torch.Generator(device=dev)
-    g.manual_seed(seed)
-    Z = torch.randn(B, 8, 8, device=dev, generator=g)
-    kind = torch.randint(0, 2, (B,), device=dev, generator=g)
-    sig = torch.tensor([1.0, 5.0, 20.0], device=dev)[torch.randint(0, 3, (B,), device=dev, generator=g)]
-    perm = torch.argsort(torch.rand(B, 8, device=dev, generator=g), dim=1)
-    Pi = torch.zeros(B, 8, 8, device=dev).scatter_(2, perm[:, :, None], 1.0)
-    H = torch.where(kind[:, None, None] == 0, sig[:, None, None] * Z, 20.0 * Pi + 0.1 * Z)
-    G = torch.randn(B, 8, 8, device=dev, generator=g)
-    return H.to(torch.bfloat16).contiguous(), G.to(torch.bfloat16).contiguous()
-
-
 def bench_n8(args, dev, stream) -> dict:
     """fwd + bwd of the 8x8 projection on its mixture workload (reported beside the 4x4 path)."""
     import torch
 
     import paper_2606_07574_amd as b4
+    import workloads
     B = N8_B
-    H, G = n8_inputs(B, 8, dev)
+    H, G = workloads.n8_mix_device(B, 8, dev)
     P = torch.empty(B, 8, 8, device=dev)
     dual = torch.empty(B, 16, device=dev)
     dH = torch.empty(B, 8, 8, device=dev)

@@ -8,6 +8,7 @@ import torch
 
 import paper_2606_07574_amd as b4
 from oracle import birkhoffn as on
+import workloads
 from tests._gpu import TOL_DH, TOL_MARGINAL, TOL_P, bits_to_dev, say, to_dev
 
 pytestmark = pytest.mark.gpu
@@ -145,3 +146,30 @@ def test_large_batch_sampled():
     assert marg.max() <= TOL_MARGINAL
     idx = np.random.default_rng(15).choice(B, 3000, replace=False)
     check(H[idx], P[idx], dual[idx], G[idx], dH[idx], "sampled")
+
+
+def test_fullsize_bench_workload():
+    # the benchmark's 8x8 workload and launch (bf16 H and dP, dual written, no step counts);
+    # a second launch with step counts must give the same bits
+    B = 1 << 22
+    say(f"test: n=8 full-size mixture B={B} (bf16), benchmark launch")
+    H, G = workloads.n8_mix_device(B, 8, "cuda")
+    P, dual, _ = b4.fwd8(H, 1e-6, MAX_ITER, want_dual=True)
+    dH = b4.bwd8(P, G)
+    P2, dual2, it = b4.fwd8(H, 1e-6, MAX_ITER, want_dual=True, want_iters=True)
+    torch.cuda.synchronize()
+    assert torch.equal(P, P2) and torch.equal(dual, dual2)
+    itn = it.cpu().numpy()
+    P64 = P.double()
+    marg = torch.maximum((P64.sum(-1) - 1).abs().amax(-1), (P64.sum(-2) - 1).abs().amax(-1)).cpu().numpy()
+    del P64, P2, dual2
+    say(f"  iters mean={itn.mean():.2f} max={itn.max()} not converged={(itn < 0).sum()}; "
+        f"max marginal over all {B}: {marg.max():.3e}")
+    assert (itn >= 0).all()
+    assert marg.max() <= TOL_MARGINAL
+    rng = np.random.default_rng(16)
+    idx = np.unique(np.concatenate([rng.choice(B, 3000, replace=False), np.argsort(marg)[-200:],
+                                    np.argsort(itn)[-200:], np.arange(64), np.arange(B - 64, B)]))
+    it_ = torch.from_numpy(idx).cuda()
+    check(H[it_].float().cpu().numpy(), P[it_].cpu().numpy(), dual[it_].cpu().numpy(),
+          G[it_].float().cpu().numpy(), dH[it_].cpu().numpy(), "full-size sample")

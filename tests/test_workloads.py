@@ -47,3 +47,22 @@ def test_config_table():
     B = {k: w.B for k, w in workloads.WORKLOADS.items()}
     assert B == {"n01_b4096": 4096, "n01_b2e20_fwd": 1 << 20, "n10_b2e22": 1 << 22,
                  "mix_bf16_b2e24": 1 << 24, "logunif_b2e25": 1 << 25}
+
+
+def test_device_generators_on_cpu():
+    import torch
+    H, G = workloads.n8_mix_device(300, 8, "cpu")
+    assert H.shape == (300, 8, 8) and G.shape == (300, 8, 8) and H.dtype == torch.bfloat16
+    H2, _ = workloads.n8_mix_device(300, 8, "cpu")
+    assert torch.equal(H, H2)
+    # about half are near-permutations: one entry per row within 0.6 of 20, at distinct
+    # columns, every other entry within 0.6 of 0
+    Hf = H.float()
+    near20 = (Hf - 20).abs() < 0.6
+    rest_small = torch.where(near20, torch.zeros_like(Hf), Hf).abs().amax(dim=(1, 2)) < 0.6
+    is_perm = (near20.sum(2) == 1).all(1) & (near20.sum(1) == 1).all(1) & rest_small
+    assert 0.35 < is_perm.float().mean().item() < 0.65
+    M, a, b, dT = workloads.ot_device(500, 4, "cpu")
+    assert M.shape == (500, 4, 4) and a.shape == (500, 4) and b.shape == (500, 4) and dT.shape == (500, 4, 4)
+    assert (a >= 0.2).all() and (a <= 2.0).all() and (b > 0).all()
+    assert (a.double().sum(1) - b.double().sum(1)).abs().max() < 1e-5

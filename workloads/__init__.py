@@ -194,3 +194,40 @@ def near_permutation(B: int, gap: float, noise: float, seed: int) -> tuple[np.nd
     H[np.arange(B)[:, None], np.arange(4)[None, :], PERMS4[perm]] += np.float32(gap)
     dP = rng.standard_normal((B, 4, 4), dtype=np.float32)
     return H, dP
+
+
+# ---------------------------------------------------------------------------
+# Larger-problem workloads drawn on the GPU with torch's seeded generator (2^28 values take
+# a while in NumPy); any sample of them is copied back for the oracle.
+# ---------------------------------------------------------------------------
+
+def n8_mix_device(B: int, seed: int, dev):
+    """8x8 mixture: half H = sigma * N(0,1) with sigma drawn from {1, 5, 20}, half
+    H = 20 Pi + 0.1 N(0,1) for a uniformly random permutation Pi of 8 (kinds shuffled),
+    dP ~ N(0,1); both stored as bf16. Returns (H, dP) on ``dev``."""
+    import torch
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    Z = torch.randn(B, 8, 8, device=dev, generator=g)
+    kind = torch.randint(0, 2, (B,), device=dev, generator=g)
+    sig = torch.tensor([1.0, 5.0, 20.0], device=dev)[torch.randint(0, 3, (B,), device=dev, generator=g)]
+    perm = torch.argsort(torch.rand(B, 8, device=dev, generator=g), dim=1)
+    Pi = torch.zeros(B, 8, 8, device=dev).scatter_(2, perm[:, :, None], 1.0)
+    H = torch.where(kind[:, None, None] == 0, sig[:, None, None] * Z, 20.0 * Pi + 0.1 * Z)
+    G = torch.randn(B, 8, 8, device=dev, generator=g)
+    return H.to(torch.bfloat16).contiguous(), G.to(torch.bfloat16).contiguous()
+
+
+def ot_device(B: int, seed: int, dev):
+    """4x4 entropic-OT problems: cost M = 2 N(0,1), marginals a, b ~ U(0.2, 2) with b
+    rescaled (in fp64) to the sum of a, upstream gradient dT ~ N(0,1); fp32. Returns
+    (M, a, b, dT) on ``dev``."""
+    import torch
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    M = 2.0 * torch.randn(B, 4, 4, device=dev, generator=g)
+    a = 0.2 + 1.8 * torch.rand(B, 4, device=dev, generator=g)
+    b = 0.2 + 1.8 * torch.rand(B, 4, device=dev, generator=g)
+    b = (b.double() * (a.double().sum(1) / b.double().sum(1))[:, None]).float()
+    G = torch.randn(B, 4, 4, device=dev, generator=g)
+    return M.contiguous(), a.contiguous(), b.contiguous(), G.contiguous()
