@@ -2032,74 +2032,131 @@ __global__ __launch_bounds__(kOtBlock) void ot4_fwd_kernel(const float* __restri
 // flows F_jk = sum_i T_ij T_ik (G_ij - G_ik) / a_i the potentials w solve the grounded
 // Laplacian system by the edge-flow elimination of the Birkhoff backward, and
 // dL/dM_ij = -T_ij (psi_ij - sum_k T_ik psi_ik / a_i) / eta with psi = G - 1 w^T.
+// dL/dM for one problem from its solution t, the marginal a and dL/dT = G.
+__device__ __forceinline__ void ot_vjp(const float t[16], const float G[16], const v4f A, float ie, float out[16]) {
+    const float ia[4] = {rcp(A.x), rcp(A.y), rcp(A.z), rcp(A.w)};
+    float W[4][4], F[4][4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int k = j + 1; k < 4; ++k) {
+            float sw = 0.f, sf = 0.f;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float q = t[4 * i + j] * (t[4 * i + k] * ia[i]);
+                sw += q;
+                sf = __builtin_fmaf(q, G[4 * i + j] - G[4 * i + k], sf);
+            }
+            W[j][k] = W[k][j] = sw;
+            F[j][k] = sf;
+            F[k][j] = -sf;
+        }
+    float ip[3], w[4];
+#pragma unroll
+    for (int pn = 0; pn < 3; ++pn) {
+        float piv = 0.f;
+#pragma unroll
+        for (int k = pn + 1; k < 4; ++k) piv += W[pn][k];
+        ip[pn] = (piv > kPivMin) ? rcp(piv) : 0.f;
+#pragma unroll
+        for (int j = pn + 1; j < 4; ++j)
+#pragma unroll
+            for (int k = j + 1; k < 4; ++k) {
+                const float fj = W[j][pn] * ip[pn], fk = W[pn][k] * ip[pn];
+                const float Fn = __builtin_fmaf(fk, F[j][pn], __builtin_fmaf(fj, F[pn][k], F[j][k]));
+                const float Wn = __builtin_fmaf(fj, W[pn][k], W[j][k]);
+                W[j][k] = W[k][j] = Wn;
+                F[j][k] = Fn;
+                F[k][j] = -Fn;
+            }
+    }
+    w[3] = 0.f;
+#pragma unroll
+    for (int pn = 2; pn >= 0; --pn) {
+        float s = 0.f;
+#pragma unroll
+        for (int k = pn + 1; k < 4; ++k) s += __builtin_fmaf(W[pn][k], w[k], F[pn][k]);
+        w[pn] = s * ip[pn];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        float psi[4], mu = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            psi[j] = G[4 * i + j] - w[j];
+            mu = __builtin_fmaf(t[4 * i + j], psi[j], mu);
+        }
+        mu *= ia[i];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) out[4 * i + j] = -t[4 * i + j] * (psi[j] - mu) * ie;
+    }
+}
+
+// One 64-problem chunk per wave; T, dT and dM move between HBM and registers in
+// wave-contiguous 16-byte pieces transposed through a per-wave LDS buffer (the 4 x 4
+// backward's memory path), a as one 16-byte piece per lane.
 __global__ __launch_bounds__(kOtBlock) void ot4_bwd_kernel(const float* __restrict__ T, const float* __restrict__ av,
                                                           const float* __restrict__ dT, float eta,
                                                           float* __restrict__ dM, int64_t B) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kOtBlock;
+    __shared__ v4f buf_all[kOtWaves][64 * kBwdStride];
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+    v4f* const buf = buf_all[wv];
+    const v4f* T4 = reinterpret_cast<const v4f*>(T);
+    const v4f* G4 = reinterpret_cast<const v4f*>(dT);
+    const v4f* A4 = reinterpret_cast<const v4f*>(av);
+    v4f* dM4 = reinterpret_cast<v4f*>(dM);
     const float ie = 1.f / eta;
-    for (int64_t p = static_cast<int64_t>(blockIdx.x) * kOtBlock + threadIdx.x; p < B; p += stride) {
+    const int cpos = (lane >> 2) * kBwdStride + (lane & 3);
+    const int64_t nchunk = (B + 63) / 64;
+    for (int64_t c = static_cast<int64_t>(blockIdx.x) * kOtWaves + wv; c < nchunk;
+         c += static_cast<int64_t>(gridDim.x) * kOtWaves) {
+        const int64_t base = c * 64;
+        const int n = (B - base < 64) ? static_cast<int>(B - base) : 64;
+        v4f tc[4], gc[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int k = 64 * q + lane;
+            tc[q] = k < 4 * n ? __builtin_nontemporal_load(T4 + 4 * base + k) : v4f{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int k = 64 * q + lane;
+            gc[q] = k < 4 * n ? __builtin_nontemporal_load(G4 + 4 * base + k) : v4f{0.f, 0.f, 0.f, 0.f};
+        }
+        const v4f A = lane < n ? __builtin_nontemporal_load(A4 + base + lane) : v4f{1.f, 1.f, 1.f, 1.f};
         float t[16], G[16];
-        load16_f32(T, p, t);
-        load16_f32(dT, p, G);
-        const v4f A = load4(av, p);
-        const float ia[4] = {rcp(A.x), rcp(A.y), rcp(A.z), rcp(A.w)};
-        float W[4][4], F[4][4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int q = 0; q < 4; ++q) buf[16 * q * kBwdStride + cpos] = tc[q];
+        __builtin_amdgcn_wave_barrier();
 #pragma unroll
-            for (int k = j + 1; k < 4; ++k) {
-                float sw = 0.f, sf = 0.f;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float q = t[4 * i + j] * (t[4 * i + k] * ia[i]);
-                    sw += q;
-                    sf = __builtin_fmaf(q, G[4 * i + j] - G[4 * i + k], sf);
-                }
-                W[j][k] = W[k][j] = sw;
-                F[j][k] = sf;
-                F[k][j] = -sf;
-            }
-        float ip[3], w[4];
-#pragma unroll
-        for (int pn = 0; pn < 3; ++pn) {
-            float piv = 0.f;
-#pragma unroll
-            for (int k = pn + 1; k < 4; ++k) piv += W[pn][k];
-            ip[pn] = (piv > kPivMin) ? rcp(piv) : 0.f;
-#pragma unroll
-            for (int j = pn + 1; j < 4; ++j)
-#pragma unroll
-                for (int k = j + 1; k < 4; ++k) {
-                    const float fj = W[j][pn] * ip[pn], fk = W[pn][k] * ip[pn];
-                    const float Fn = __builtin_fmaf(fk, F[j][pn], __builtin_fmaf(fj, F[pn][k], F[j][k]));
-                    const float Wn = __builtin_fmaf(fj, W[pn][k], W[j][k]);
-                    W[j][k] = W[k][j] = Wn;
-                    F[j][k] = Fn;
-                    F[k][j] = -Fn;
-                }
+        for (int r = 0; r < 4; ++r) {
+            const v4f u = buf[lane * kBwdStride + r];
+            t[4 * r + 0] = u.x; t[4 * r + 1] = u.y; t[4 * r + 2] = u.z; t[4 * r + 3] = u.w;
         }
-        w[3] = 0.f;
+        __builtin_amdgcn_wave_barrier();
 #pragma unroll
-        for (int pn = 2; pn >= 0; --pn) {
-            float s = 0.f;
+        for (int q = 0; q < 4; ++q) buf[16 * q * kBwdStride + cpos] = gc[q];
+        __builtin_amdgcn_wave_barrier();
 #pragma unroll
-            for (int k = pn + 1; k < 4; ++k) s += __builtin_fmaf(W[pn][k], w[k], F[pn][k]);
-            w[pn] = s * ip[pn];
+        for (int r = 0; r < 4; ++r) {
+            const v4f u = buf[lane * kBwdStride + r];
+            G[4 * r + 0] = u.x; G[4 * r + 1] = u.y; G[4 * r + 2] = u.z; G[4 * r + 3] = u.w;
         }
+        __builtin_amdgcn_wave_barrier();
         float out[16];
+        ot_vjp(t, G, A, ie, out);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            float psi[4], mu = 0.f;
+        for (int r = 0; r < 4; ++r)
+            buf[lane * kBwdStride + r] = v4f{out[4 * r], out[4 * r + 1], out[4 * r + 2], out[4 * r + 3]};
+        __builtin_amdgcn_wave_barrier();
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                psi[j] = G[4 * i + j] - w[j];
-                mu = __builtin_fmaf(t[4 * i + j], psi[j], mu);
-            }
-            mu *= ia[i];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) out[4 * i + j] = -t[4 * i + j] * (psi[j] - mu) * ie;
+        for (int q = 0; q < 4; ++q) {
+            const int k = 64 * q + lane;
+            const v4f o = buf[16 * q * kBwdStride + cpos];
+            if (k < 4 * n) __builtin_nontemporal_store(o, dM4 + 4 * base + k);
         }
-        store16(dM, p, out);
+        __builtin_amdgcn_wave_barrier();
     }
 }
 
@@ -2320,7 +2377,8 @@ int birkhoff4_ot_bwd(const float* T, const float* a, const float* dT, float eta,
     if (misaligned(T) || misaligned(a) || misaligned(dT) || misaligned(dM)) return BIRKHOFF4_ERR_ALIGN;
     const size_t nm = static_cast<size_t>(B) * 64, nv = static_cast<size_t>(B) * 16;
     if (overlaps(dM, nm, T, nm) || overlaps(dM, nm, dT, nm) || overlaps(dM, nm, a, nv)) return BIRKHOFF4_ERR_OVERLAP;
-    const int64_t want = (B + kOtBlock - 1) / kOtBlock;
+    const int64_t chunks = (B + 63) / 64;
+    const int64_t want = (chunks + kOtWaves - 1) / kOtWaves;
     const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
     hipLaunchKernelGGL(ot4_bwd_kernel, dim3(static_cast<unsigned>(grid)), dim3(kOtBlock), 0, stream, T, a, dT, eta,
                        dM, B);
