@@ -79,6 +79,7 @@ constexpr float kTiny = 1e-30f;
 constexpr float kPivMin = 1e-30f;
 constexpr float kFltMin = 1.17549435e-38f;
 constexpr int kMaxSkSteps = 48;   // sk_bwd keeps (n+1) x 4 floats per lane in LDS
+constexpr int kSkRegSteps = 20;   // step count whose backward keeps the iterates in VGPRs
 constexpr int kMaxIterCap = 10000;
 // Batches up to this size take the four-lanes-per-problem forward by default.
 constexpr int64_t kLatencyMaxB = int64_t(1) << 15;
@@ -1005,9 +1006,69 @@ __global__ __launch_bounds__(256) void sk_fwd_kernel(const void* __restrict__ H,
     }
 }
 
-// Reverse mode through the n-step map. The iterates v^(k) are kept in LDS (one
-// 64-lane block, [k][component][lane] so that lanes hit distinct banks); u^(k) is
-// recomputed from v^(k-1). A clamped denominator contributes no gradient.
+// Adjoints of P = diag(u) A diag(v) for dL/dP = G: A-bar = G o u v^T, u-bar, v-bar.
+__device__ __forceinline__ void sk_adjoint_init(const float A[16], const float G[16], const float u[4],
+                                                const float v[4], float Ab[16], float ub[4], float vb[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ub[i] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) vb[j] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float gg = G[4 * i + j];
+            Ab[4 * i + j] = gg * u[i] * v[j];
+            ub[i] = __builtin_fmaf(gg * A[4 * i + j], v[j], ub[i]);
+            vb[j] = __builtin_fmaf(gg * u[i], A[4 * i + j], vb[j]);
+        }
+}
+
+// One step back through u^(k) = 1 / max(A v^(k-1), FLT_MIN), v^(k) = 1 / max(A^T u^(k),
+// FLT_MIN): u^(k) is recomputed from v^(k-1); on entry vb holds dL/dv^(k) and ub the
+// direct part of dL/du^(k) (zero before the last step's), on exit vb holds dL/dv^(k-1),
+// ub is cleared and A-bar has gathered both steps' terms. A clamped denominator
+// contributes no gradient.
+__device__ __forceinline__ void sk_reverse(const float A[16], const float vk[4], const float vp[4], float Ab[16],
+                                           float ub[4], float vb[4]) {
+    float uk[4];
+    sk_u(A, vp, uk);
+    float bb[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const float den = __builtin_fmaf(A[j], uk[0], __builtin_fmaf(A[4 + j], uk[1],
+                          __builtin_fmaf(A[8 + j], uk[2], A[12 + j] * uk[3])));
+        bb[j] = den >= kFltMin ? -vb[j] * vk[j] * vk[j] : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            ub[i] = __builtin_fmaf(A[4 * i + j], bb[j], ub[i]);
+            Ab[4 * i + j] = __builtin_fmaf(uk[i], bb[j], Ab[4 * i + j]);
+        }
+    float ab[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float den = __builtin_fmaf(A[4 * i], vp[0], __builtin_fmaf(A[4 * i + 1], vp[1],
+                          __builtin_fmaf(A[4 * i + 2], vp[2], A[4 * i + 3] * vp[3])));
+        ab[i] = den >= kFltMin ? -ub[i] * uk[i] * uk[i] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) vb[j] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            vb[j] = __builtin_fmaf(A[4 * i + j], ab[i], vb[j]);
+            Ab[4 * i + j] = __builtin_fmaf(ab[i], vp[j], Ab[4 * i + j]);
+        }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ub[i] = 0.f;
+}
+
+// Reverse mode through the n-step map, any n: the iterates v^(k) are kept in LDS (one
+// 64-lane block, [k][component][lane] so that lanes hit distinct banks).
 template <int DT, int DG>
 __global__ __launch_bounds__(64) void sk_bwd_kernel(const void* __restrict__ H,
                                                      const void* __restrict__ dP,
@@ -1029,61 +1090,55 @@ __global__ __launch_bounds__(64) void sk_bwd_kernel(const void* __restrict__ H,
             for (int j = 0; j < 4; ++j) vbuf[(4 * k + j) * 64 + lane] = v[j];
         }
         float Ab[16], ub[4], vb[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) ub[i] = 0.f;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) vb[j] = 0.f;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const float gg = G[4 * i + j];
-                Ab[4 * i + j] = gg * u[i] * v[j];
-                ub[i] = __builtin_fmaf(gg * A[4 * i + j], v[j], ub[i]);
-                vb[j] = __builtin_fmaf(gg * u[i], A[4 * i + j], vb[j]);
-            }
+        sk_adjoint_init(A, G, u, v, Ab, ub, vb);
         for (int k = n_steps; k >= 1; --k) {
-            float vk[4], vp[4], uk[4];
+            float vk[4], vp[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 vk[j] = vbuf[(4 * k + j) * 64 + lane];
                 vp[j] = vbuf[(4 * (k - 1) + j) * 64 + lane];
             }
-            sk_u(A, vp, uk);
-            // v^(k) = 1 / max(A^T u^(k), FLT_MIN)
-            float bb[4];
+            sk_reverse(A, vk, vp, Ab, ub, vb);
+        }
+        float out[16];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const float den = __builtin_fmaf(A[j], uk[0], __builtin_fmaf(A[4 + j], uk[1],
-                                  __builtin_fmaf(A[8 + j], uk[2], A[12 + j] * uk[3])));
-                bb[j] = den >= kFltMin ? -vb[j] * vk[j] * vk[j] : 0.f;
-            }
+        for (int q = 0; q < 16; ++q) out[q] = Ab[q] * A[q];
+        store16(dH, b, out);
+    }
+}
+
+// The same for a step count fixed at compile time: the iterates stay in VGPRs (the
+// loops are unrolled), so occupancy is set by registers, not by the LDS the iterates
+// would take. Same arithmetic in the same order as the LDS kernel.
+template <int DT, int DG, int NS>
+__global__ __launch_bounds__(256, 3) void sk_bwd_reg_kernel(const void* __restrict__ H,
+                                                          const void* __restrict__ dP,
+                                                          float* __restrict__ dH, int64_t B) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t b = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; b < B; b += stride) {
+        float h[16], G[16], A[16], u[4], vs[NS + 1][4];
+        load16<DT>(H, b, h);
+        sk_kernel_matrix(h, A);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 4; ++j) vs[0][j] = 1.f;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    ub[i] = __builtin_fmaf(A[4 * i + j], bb[j], ub[i]);
-                    Ab[4 * i + j] = __builtin_fmaf(uk[i], bb[j], Ab[4 * i + j]);
-                }
-            // u^(k) = 1 / max(A v^(k-1), FLT_MIN)
-            float ab[4];
+        for (int k = 1; k <= NS; ++k) {
+            sk_u(A, vs[k - 1], u);
+            sk_v(A, u, vs[k]);
+        }
+        load16<DG>(dP, b, G);  // needed from here on only
+        float Ab[16], ub[4], vb[4];
+        sk_adjoint_init(A, G, u, vs[NS], Ab, ub, vb);
+        // Each reverse step recomputes u^(k) from v^(k-1); tying the step's inputs to the
+        // adjoint it receives keeps that work in its own step (hoisted ahead, or shared with
+        // the forward steps, it would keep ~20 values per step live at once).
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float den = __builtin_fmaf(A[4 * i], vp[0], __builtin_fmaf(A[4 * i + 1], vp[1],
-                                  __builtin_fmaf(A[4 * i + 2], vp[2], A[4 * i + 3] * vp[3])));
-                ab[i] = den >= kFltMin ? -ub[i] * uk[i] * uk[i] : 0.f;
-            }
-#pragma unroll
-            for (int j = 0; j < 4; ++j) vb[j] = 0.f;
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    vb[j] = __builtin_fmaf(A[4 * i + j], ab[i], vb[j]);
-                    Ab[4 * i + j] = __builtin_fmaf(ab[i], vp[j], Ab[4 * i + j]);
-                }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) ub[i] = 0.f;
+        for (int k = NS; k >= 1; --k) {
+            float vk[4] = {vs[k][0], vs[k][1], vs[k][2], vs[k][3]};
+            float vp[4] = {vs[k - 1][0], vs[k - 1][1], vs[k - 1][2], vs[k - 1][3]};
+            asm volatile("" : "+v"(vk[0]), "+v"(vk[1]), "+v"(vk[2]), "+v"(vk[3]), "+v"(vp[0]), "+v"(vp[1]),
+                              "+v"(vp[2]), "+v"(vp[3]) : "v"(vb[0]), "v"(vb[1]), "v"(vb[2]), "v"(vb[3]));
+            sk_reverse(A, vk, vp, Ab, ub, vb);
         }
         float out[16];
 #pragma unroll
@@ -2487,6 +2542,22 @@ int birkhoff4_sk_bwd(const void* H, int h_dtype, const void* dP, int dp_dtype, f
         return BIRKHOFF4_ERR_OVERLAP;
     int cus = 0;
     if (int e = device_cus(&cus)) return e;
+    if (n_steps == kSkRegSteps) {
+        const int64_t grid = grid_for(B, 256, cus, 64);
+        const dim3 g(static_cast<unsigned>(grid)), blk(256);
+        if (h_dtype == BIRKHOFF4_BF16) {
+            if (dp_dtype == BIRKHOFF4_BF16)
+                hipLaunchKernelGGL((sk_bwd_reg_kernel<BIRKHOFF4_BF16, BIRKHOFF4_BF16, kSkRegSteps>), g, blk, 0, stream, H, dP, dH, B);
+            else
+                hipLaunchKernelGGL((sk_bwd_reg_kernel<BIRKHOFF4_BF16, BIRKHOFF4_F32, kSkRegSteps>), g, blk, 0, stream, H, dP, dH, B);
+        } else {
+            if (dp_dtype == BIRKHOFF4_BF16)
+                hipLaunchKernelGGL((sk_bwd_reg_kernel<BIRKHOFF4_F32, BIRKHOFF4_BF16, kSkRegSteps>), g, blk, 0, stream, H, dP, dH, B);
+            else
+                hipLaunchKernelGGL((sk_bwd_reg_kernel<BIRKHOFF4_F32, BIRKHOFF4_F32, kSkRegSteps>), g, blk, 0, stream, H, dP, dH, B);
+        }
+        return launch_status();
+    }
     const int64_t grid = grid_for(B, 64, cus, 64);
     const size_t lds = static_cast<size_t>(n_steps + 1) * 4 * 64 * sizeof(float);
     const dim3 g(static_cast<unsigned>(grid)), blk(64);

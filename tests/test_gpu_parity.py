@@ -190,6 +190,29 @@ def test_sinkhorn_baseline(sigma):
     assert np.abs(P.cpu().numpy().astype(np.float64).sum(axis=1) - 1).max() < 2e-6
 
 
+@pytest.mark.parametrize("n_steps", [1, 7, 19, 21, 48])
+def test_sinkhorn_step_counts(n_steps):
+    # 20 steps run the register-resident backward; every other count the LDS one
+    say(f"test: SK-{n_steps} baseline")
+    H, dP = workloads.gauss(5000, 3.0, seed=30 + n_steps)
+    P = b4.sk_fwd(to_dev(H), n_steps)
+    dH = b4.sk_bwd(to_dev(H), to_dev(dP), n_steps)
+    torch.cuda.synchronize()
+    assert np.abs(P.cpu().numpy() - oracle.sk_fwd(H, n_steps)).max() <= 1e-5
+    assert dh_rel_err(dH.cpu().numpy().astype(np.float64), oracle.sk_bwd(H, dP, n_steps)).max() <= TOL_DH
+
+
+def test_sinkhorn_bf16():
+    say("test: SK-20 baseline on bf16 H and dP")
+    ch = workloads.make_chunk(workloads.WORKLOADS["mix_bf16_b2e24"], 0, B=20000)
+    Hd, dPd = bits_to_dev(ch.H_bits), bits_to_dev(ch.dP_bits)
+    P = b4.sk_fwd(Hd, 20)
+    dH = b4.sk_bwd(Hd, dPd, 20)
+    torch.cuda.synchronize()
+    assert np.abs(P.cpu().numpy() - oracle.sk_fwd(ch.H, 20)).max() <= 1e-5
+    assert dh_rel_err(dH.cpu().numpy().astype(np.float64), oracle.sk_bwd(ch.H, ch.dP, 20)).max() <= TOL_DH
+
+
 def test_variants_agree():
     say("test: throughput and latency variants give the same projection")
     H, _ = workloads.gauss(50000, 6.0, seed=21)
