@@ -293,7 +293,11 @@ def main() -> int:
                                     "max": float(sl1.max().item())},
             }
             log(f"sk20: {out['sk20_baseline']}")
+            sk_marg = smarg.cpu().numpy()
             del Psk, S64
+        else:
+            sk_marg = None
+        out["buckets"] = bucket_report(w, ch, itn, marg.cpu().numpy(), sk_marg)
         del P, P64
 
     if not args.no_cpu_baseline:
@@ -325,6 +329,39 @@ def main() -> int:
 
     print(json.dumps(out), flush=True)
     return 0
+
+
+def bucket_report(w, ch, itn, marg, sk_marg):
+    """Newton steps and max marginal error (and the SK-20 baseline's) per input bucket: the
+    mixture's four kinds, deciles of the log-uniform scale, or the one Gaussian scale."""
+    if w.kind == "mixture":
+        sel = [(f"gauss sigma={sg:g}", (ch.kind == 0) & (ch.scale == np.float32(sg))) for sg in (1.0, 5.0, 20.0)]
+        sel.append(("near-permutation 20 Pi + 0.1 N", ch.kind == 1))
+    elif w.kind == "logunif":
+        edges = np.quantile(ch.scale, np.linspace(0.0, 1.0, 11))
+        sel = []
+        for d in range(10):
+            lo, hi = edges[d], edges[d + 1]
+            m = (ch.scale >= lo) & ((ch.scale < hi) if d < 9 else (ch.scale <= hi))
+            sel.append((f"alpha decile {d + 1}: [{lo:.3g}, {hi:.3g}]", m))
+    else:
+        sel = [(f"sigma={w.sigma:g}", np.ones(len(itn), bool))]
+    rows = []
+    for name, m in sel:
+        it = itn[m]
+        conv = it[it >= 0]
+        row = {"bucket": name, "n": int(m.sum()),
+               "newton_steps": {"mean": round(float(conv.mean()), 3) if len(conv) else None,
+                                "p99": int(np.percentile(conv, 99)) if len(conv) else None,
+                                "max": int(conv.max()) if len(conv) else None,
+                                "not_converged": int((it == -1).sum()),
+                                "hist": np.bincount(np.clip(conv, 0, 40), minlength=41).tolist()},
+               "max_marginal_err": float(marg[m].max()) if m.any() else None}
+        if sk_marg is not None and m.any():
+            row["sk20_max_marginal_err"] = float(sk_marg[m].max())
+            row["sk20_median_marginal_err"] = float(np.median(sk_marg[m]))
+        rows.append(row)
+    return rows
 
 
 OT_B = 1 << 22
