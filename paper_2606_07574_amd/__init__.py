@@ -107,6 +107,23 @@ def _ptr(t: torch.Tensor | None) -> int | None:
     return None if t is None else t.data_ptr()
 
 
+def _same_device(first: torch.Tensor, *others: torch.Tensor) -> None:
+    for t in others:
+        if t.device != first.device:
+            raise ValueError(f"all tensors must be on {first.device}, got one on {t.device}")
+
+
+def _out(out: torch.Tensor | None, shape, device, name: str = "out") -> torch.Tensor:
+    """A new float32 tensor of the given shape, or the caller's after checking that the
+    kernel may write exactly that many float32 values into it."""
+    if out is None:
+        return torch.empty(shape, dtype=torch.float32, device=device)
+    if (tuple(out.shape) != tuple(shape) or out.dtype != torch.float32 or out.device != device
+            or not out.is_contiguous()):
+        raise ValueError(f"{name} must be a contiguous float32 tensor of shape {tuple(shape)} on {device}")
+    return out
+
+
 def fwd(H: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER,
         want_dual: bool = True, want_iters: bool = False, out: torch.Tensor | None = None,
         variant: int = AUTO):
@@ -118,7 +135,7 @@ def fwd(H: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_I
     """
     B = _batch(H, "H")
     lead = H.shape[:-2]
-    P = torch.empty(H.shape, dtype=torch.float32, device=H.device) if out is None else out
+    P = _out(out, H.shape, H.device)
     dual = torch.empty(*lead, 8, dtype=torch.float32, device=H.device) if want_dual else None
     iters = torch.empty(lead, dtype=torch.int32, device=H.device) if want_iters else None
     with torch.cuda.device(H.device):
@@ -134,7 +151,8 @@ def bwd(P: torch.Tensor, dP: torch.Tensor, out: torch.Tensor | None = None) -> t
         raise ValueError("P and dP batch sizes differ")
     if P.dtype != torch.float32:
         raise TypeError("P must be float32")
-    dH = torch.empty(P.shape, dtype=torch.float32, device=P.device) if out is None else out
+    _same_device(P, dP)
+    dH = _out(out, P.shape, P.device)
     with torch.cuda.device(P.device):
         _check(_load().birkhoff4_bwd_ex(_ptr(P), _ptr(dP), _dtype_code(dP), _ptr(dH), B, _stream(P)))
     return dH
@@ -154,6 +172,7 @@ def sk_bwd(H: torch.Tensor, dP: torch.Tensor, n_steps: int = 20) -> torch.Tensor
     B = _batch(H, "H")
     if _batch(dP, "dP") != B:
         raise ValueError("H and dP batch sizes differ")
+    _same_device(H, dP)
     dH = torch.empty(H.shape, dtype=torch.float32, device=H.device)
     with torch.cuda.device(H.device):
         _check(_load().birkhoff4_sk_bwd(_ptr(H), _dtype_code(H), _ptr(dP), _dtype_code(dP), _ptr(dH),
@@ -188,7 +207,7 @@ def fwd8(H: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_
     """fwd for trailing 8x8 matrices: returns (P, dual [..., 16] or None, iters or None)."""
     B = _batch(H, "H", 8)
     lead = H.shape[:-2]
-    P = torch.empty(H.shape, dtype=torch.float32, device=H.device) if out is None else out
+    P = _out(out, H.shape, H.device)
     dual = torch.empty(*lead, 16, dtype=torch.float32, device=H.device) if want_dual else None
     iters = torch.empty(lead, dtype=torch.int32, device=H.device) if want_iters else None
     with torch.cuda.device(H.device):
@@ -204,7 +223,8 @@ def bwd8(P: torch.Tensor, dP: torch.Tensor, out: torch.Tensor | None = None) -> 
         raise ValueError("P and dP batch sizes differ")
     if P.dtype != torch.float32:
         raise TypeError("P must be float32")
-    dH = torch.empty(P.shape, dtype=torch.float32, device=P.device) if out is None else out
+    _same_device(P, dP)
+    dH = _out(out, P.shape, P.device)
     with torch.cuda.device(P.device):
         _check(_load().birkhoff8_bwd(_ptr(P), _ptr(dP), _dtype_code(dP), _ptr(dH), B, _stream(P)))
     return dH
@@ -248,6 +268,7 @@ def ot_fwd(M: torch.Tensor, a: torch.Tensor, b: torch.Tensor, eta: float = 1.0, 
     lead = M.shape[:-2]
     _marginals(a, lead, "a")
     _marginals(b, lead, "b")
+    _same_device(M, a, b)
     T = torch.empty(M.shape, dtype=torch.float32, device=M.device)
     dual = torch.empty(*lead, 8, dtype=torch.float32, device=M.device) if want_dual else None
     iters = torch.empty(lead, dtype=torch.int32, device=M.device) if want_iters else None
@@ -265,6 +286,7 @@ def ot_bwd(T: torch.Tensor, a: torch.Tensor, dT: torch.Tensor, eta: float = 1.0)
     if T.dtype != torch.float32 or dT.dtype != torch.float32:
         raise TypeError("T and dT must be float32")
     _marginals(a, T.shape[:-2], "a")
+    _same_device(T, a, dT)
     dM = torch.empty(T.shape, dtype=torch.float32, device=T.device)
     with torch.cuda.device(T.device):
         _check(_load().birkhoff4_ot_bwd(_ptr(T), _ptr(a), _ptr(dT), float(eta), _ptr(dM), B, _stream(T)))

@@ -153,3 +153,18 @@ def test_binding_refuses_cpu_tensors():
         b4.fwd(H)
     with pytest.raises(b4.Birkhoff4Error):
         b4.bwd(H, H)
+
+
+def test_binding_output_and_device_checks():
+    import torch
+    dev = torch.device("cpu")
+    assert b4._out(None, (3, 4, 4), dev).shape == (3, 4, 4)
+    good = torch.empty(3, 4, 4)
+    assert b4._out(good, (3, 4, 4), dev) is good
+    for bad in (torch.empty(3, 4, 5), torch.empty(2, 4, 4), torch.empty(3, 4, 4, dtype=torch.float64),
+                torch.empty(3, 4, 8)[..., ::2]):
+        with pytest.raises(ValueError):
+            b4._out(bad, (3, 4, 4), dev)
+    b4._same_device(good, torch.empty(1))
+    with pytest.raises(ValueError):
+        b4._same_device(good, torch.empty(1, device="meta"))

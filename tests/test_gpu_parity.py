@@ -223,3 +223,17 @@ def test_variants_agree():
     say(f"  max |P_throughput - P_latency| = {diff:.2e}")
     assert diff <= 2 * TOL_P
     assert (i1 >= 0).all() and (i2 >= 0).all()
+
+
+def test_binding_rejects_mismatched_outputs():
+    say("test: binding rejects an out tensor the kernel could overrun")
+    H = to_dev(workloads.gauss(100, 1.0, seed=40)[0])
+    for bad in (torch.empty(99, 4, 4, device="cuda"), torch.empty(100, 4, 4, device="cuda", dtype=torch.float16),
+                torch.empty(100, 4, 8, device="cuda")[..., ::2]):
+        with pytest.raises(ValueError):
+            b4.fwd(H, out=bad)
+    P, _, _ = b4.fwd(H)
+    with pytest.raises(ValueError):
+        b4.bwd(P, H, out=torch.empty(50, 4, 4, device="cuda"))
+    with pytest.raises(ValueError):
+        b4.fwd8(torch.zeros(10, 8, 8, device="cuda"), out=torch.empty(10, 4, 4, device="cuda"))
