@@ -85,6 +85,7 @@ def main() -> int:
                     help="matrices in the oracle's CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sk", action="store_true")
+    ap.add_argument("--no-hess", action="store_true", help="skip the saved-Hessian variant's timing")
     ap.add_argument("--no-n8", action="store_true", help="skip the 8x8 measurement")
     ap.add_argument("--n8-only", action="store_true", help="time only the 8x8 path (for profiler runs)")
     ap.add_argument("--no-ot", action="store_true", help="skip the general-OT measurement")
@@ -299,6 +300,10 @@ def main() -> int:
             sk_marg = None
         out["buckets"] = bucket_report(w, ch, itn, marg.cpu().numpy(), sk_marg)
         del P, P64
+        if w.grad and not args.no_hess:
+            out["saved_hessian"] = bench_saved_hessian(args, lib, sets, n_sets, B, hcode, bf16, stream,
+                                                       in_bytes(bf16), ms_per_step)
+            log(f"saved hessian: {out['saved_hessian']}")
 
     if not args.no_cpu_baseline:
         # the oracle as it stands (fp64, its own tolerance 1e-13), then at the GPU's tolerance
@@ -329,6 +334,56 @@ def main() -> int:
 
     print(json.dumps(out), flush=True)
     return 0
+
+
+def bench_saved_hessian(args, lib, sets, n_sets, B, hcode, bf16, stream, inb, default_ms):
+    """The saved-Hessian variant (Sec. 4.2) on the benchmark's buffers: the forward also writes
+    the 32-byte column weights of P, the backward reads them instead of recomputing them."""
+    import torch
+
+    import paper_2606_07574_amd as b4
+    dev = sets[0]["H"].device
+    hs = [torch.empty(B, 8, device=dev) for _ in range(n_sets)]
+    sptr = stream.cuda_stream
+    gcode = hcode if bf16 else b4.F32
+    ks = max(3, args.steps // 2)
+    e0 = [torch.cuda.Event(enable_timing=True) for _ in range(ks)]
+    e1 = [torch.cuda.Event(enable_timing=True) for _ in range(ks)]
+    e2 = [torch.cuda.Event(enable_timing=True) for _ in range(ks)]
+
+    def step(k, ev):
+        st, h = sets[k % n_sets], hs[k % n_sets]
+        if ev:
+            e0[k].record(stream)
+        rc = lib.birkhoff4_fwd_hess(st["H"].data_ptr(), hcode, st["P"].data_ptr(), st["dual"].data_ptr(),
+                                    h.data_ptr(), None, B, args.tol, args.max_iter, sptr)
+        if rc:
+            raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+        if ev:
+            e1[k].record(stream)
+        rc = lib.birkhoff4_bwd_hess(st["P"].data_ptr(), h.data_ptr(), st["G"].data_ptr(), gcode,
+                                    st["dH"].data_ptr(), B, sptr)
+        if rc:
+            raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+        if ev:
+            e2[k].record(stream)
+
+    for k in range(2):
+        step(k, False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(ks):
+        step(k, True)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / ks
+    f_ms = float(np.mean([e0[k].elapsed_time(e1[k]) for k in range(ks)]))
+    b_ms = float(np.mean([e1[k].elapsed_time(e2[k]) for k in range(ks)]))
+    fwd_bytes, bwd_bytes = B * (inb + 64 + 32 + 32), B * (64 + 32 + inb + 64)
+    return {"ms_per_step": round(wall * 1e3, 4), "value": round(B / wall, 1), "unit": "proj/s",
+            "fwd_ms": round(f_ms, 4), "bwd_ms": round(b_ms, 4),
+            "alg_bytes_per_projection": (fwd_bytes + bwd_bytes) // B,
+            "fwd_GBs": round(fwd_bytes / (f_ms * 1e-3) / 1e9, 1), "bwd_GBs": round(bwd_bytes / (b_ms * 1e-3) / 1e9, 1),
+            "default_ms_per_step": round(default_ms, 4)}
 
 
 def bucket_report(w, ch, itn, marg, sk_marg):

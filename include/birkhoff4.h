@@ -125,6 +125,22 @@ int birkhoff4_fwd_ex2(const void* H, int h_dtype, float* P, float* dual, int32_t
 int birkhoff4_bwd_ex(const float* P, const void* dP, int dp_dtype, float* dH, int64_t B,
                      hipStream_t stream);
 
+/* Saved-Hessian variant (Sec. 4.2: at the solution the Hessian of the reduced dual equals
+ * the Delta of eq. derivative, so the forward's Hessian can be kept for the backward).
+ * birkhoff4_fwd_hess is birkhoff4_fwd_ex (one problem per lane, any B) that also writes,
+ * per matrix, the six column weights W_jk = sum_i P_ij P_ik of its output P, whose
+ * Laplacian grounded at column 4 is that Hessian: hess [B][8] fp32 =
+ * (W_12, W_13, W_14, W_23, W_24, W_34, 0, 0), 32 bytes per matrix, caller-owned, 16-byte
+ * aligned, not overlapping the other arrays; dual and iters may be NULL.
+ * birkhoff4_bwd_hess is birkhoff4_bwd_ex taking those weights instead of recomputing them
+ * from P. Both return the codes of the calls they extend; hess NULL gives
+ * BIRKHOFF4_ERR_NULL. This trades 32 bytes of writes and of reads per matrix for the six
+ * weight sums of the backward; the default pair above does not use it. */
+int birkhoff4_fwd_hess(const void* H, int h_dtype, float* P, float* dual, float* hess, int32_t* iters,
+                       int64_t B, float tol, int max_iter, hipStream_t stream);
+int birkhoff4_bwd_hess(const float* P, const float* hess, const void* dP, int dp_dtype, float* dH,
+                       int64_t B, hipStream_t stream);
+
 /* Baseline: n_steps iterations of Sinkhorn-Knopp (eq. sinkhorn_knopp) from
  * v^(0) = 1 on A = exp(H) (each row shifted by its maximum, which leaves every
  * iterate diag(u) A diag(v) unchanged); P = diag(u^(n)) A diag(v^(n)), whose

@@ -9,6 +9,7 @@ a GPU, the calls raise.
     P, dual = fwd(H)                  # eq. birkhoff_projection via Newton (Sec. 3)
     dH = bwd(P, dP)                   # implicit differentiation (Sec. 4, eq. derivative)
     P = project(H)                    # autograd-aware: backward calls bwd
+    P, dual, hess, _ = fwd_hess(H); dH = bwd_hess(P, hess, dP)   # saved-Hessian variant (Sec. 4.2)
     P = sk_fwd(H, 20); dH = sk_bwd(H, dP, 20)   # Sinkhorn-Knopp baseline
     P, dual = fwd8(H); dH = bwd8(P, dP); P = project8(H)   # the same for 8 x 8 matrices
     T, dual = ot_fwd(M, a, b, eta); dM = ot_bwd(T, a, dT, eta)  # general entropic OT, 4 x 4
@@ -52,6 +53,8 @@ def _load():
         "birkhoff4_fwd_ex": [vp, i32, vp, vp, vp, i64, f32, i32, st],
         "birkhoff4_fwd_ex2": [vp, i32, vp, vp, vp, i64, f32, i32, i32, st],
         "birkhoff4_bwd_ex": [vp, vp, i32, vp, i64, st],
+        "birkhoff4_fwd_hess": [vp, i32, vp, vp, vp, vp, i64, f32, i32, st],
+        "birkhoff4_bwd_hess": [vp, vp, vp, i32, vp, i64, st],
         "birkhoff4_sk_fwd": [vp, i32, vp, i64, i32, st],
         "birkhoff4_sk_bwd": [vp, i32, vp, i32, vp, i64, i32, st],
         "birkhoff8_fwd": [vp, i32, vp, vp, vp, i64, f32, i32, st],
@@ -155,6 +158,38 @@ def bwd(P: torch.Tensor, dP: torch.Tensor, out: torch.Tensor | None = None) -> t
     dH = _out(out, P.shape, P.device)
     with torch.cuda.device(P.device):
         _check(_load().birkhoff4_bwd_ex(_ptr(P), _ptr(dP), _dtype_code(dP), _ptr(dH), B, _stream(P)))
+    return dH
+
+
+def fwd_hess(H: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER,
+             want_dual: bool = True, want_iters: bool = False):
+    """fwd that also returns the column weights of P (the Hessian at the solution, Sec. 4.2):
+    (P, dual or None, hess float32 [..., 8] = (W12, W13, W14, W23, W24, W34, 0, 0), iters or None)."""
+    B = _batch(H, "H")
+    lead = H.shape[:-2]
+    P = torch.empty(H.shape, dtype=torch.float32, device=H.device)
+    dual = torch.empty(*lead, 8, dtype=torch.float32, device=H.device) if want_dual else None
+    hess = torch.empty(*lead, 8, dtype=torch.float32, device=H.device)
+    iters = torch.empty(lead, dtype=torch.int32, device=H.device) if want_iters else None
+    with torch.cuda.device(H.device):
+        _check(_load().birkhoff4_fwd_hess(_ptr(H), _dtype_code(H), _ptr(P), _ptr(dual), _ptr(hess), _ptr(iters),
+                                          B, float(tol), int(max_iter), _stream(H)))
+    return P, dual, hess, iters
+
+
+def bwd_hess(P: torch.Tensor, hess: torch.Tensor, dP: torch.Tensor) -> torch.Tensor:
+    """bwd taking the column weights saved by fwd_hess instead of recomputing them from P."""
+    B = _batch(P, "P")
+    if _batch(dP, "dP") != B:
+        raise ValueError("P and dP batch sizes differ")
+    if P.dtype != torch.float32:
+        raise TypeError("P must be float32")
+    if (tuple(hess.shape) != (*P.shape[:-2], 8) or hess.dtype != torch.float32 or not hess.is_contiguous()):
+        raise ValueError(f"hess must be a contiguous float32 tensor of shape {(*P.shape[:-2], 8)}")
+    _same_device(P, hess, dP)
+    dH = torch.empty(P.shape, dtype=torch.float32, device=P.device)
+    with torch.cuda.device(P.device):
+        _check(_load().birkhoff4_bwd_hess(_ptr(P), _ptr(hess), _ptr(dP), _dtype_code(dP), _ptr(dH), B, _stream(P)))
     return dH
 
 

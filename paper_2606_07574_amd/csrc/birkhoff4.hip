@@ -305,12 +305,20 @@ __device__ __forceinline__ void init_problem(const uint32_t w[RawWords<DT>::n], 
 }
 
 // Output of one problem: P = T, dual = (alpha*(beta), beta) in natural-log units with
-// beta_4 = 0 (NaN for a poisoned input), and the status word.
-template <bool WRITE_DUAL, bool WRITE_ITERS>
+// beta_4 = 0 (NaN for a poisoned input), the status word, and (saved-Hessian variant) the
+// column weights of P.
+template <bool WRITE_DUAL, bool WRITE_ITERS, bool WRITE_HESS>
 __device__ __forceinline__ void store_output(float* __restrict__ P, float* __restrict__ dual,
-                                             int32_t* __restrict__ iters, int64_t gi, const float T[16],
-                                             const float a[4], float b0, float b1, float b2, int status) {
+                                             int32_t* __restrict__ iters, float* __restrict__ hess, int64_t gi,
+                                             const float T[16], const float a[4], float b0, float b1, float b2,
+                                             int status) {
     store16(P, gi, T);
+    if constexpr (WRITE_HESS) {
+        const Weights W = column_weights(T);
+        v4f* hp = reinterpret_cast<v4f*>(hess) + 2 * gi;
+        hp[0] = v4f{W.w01, W.w02, W.w03, W.w12};
+        hp[1] = v4f{W.w13, W.w23, 0.f, 0.f};
+    }
     if constexpr (WRITE_DUAL) {
         v4f* dp = reinterpret_cast<v4f*>(dual) + 2 * gi;
         dp[0] = v4f{-a[0] * kLn2, -a[1] * kLn2, -a[2] * kLn2, -a[3] * kLn2};
@@ -319,11 +327,12 @@ __device__ __forceinline__ void store_output(float* __restrict__ P, float* __res
     if constexpr (WRITE_ITERS) iters[gi] = status;
 }
 
-template <int DT, bool WRITE_DUAL, bool WRITE_ITERS>
+template <int DT, bool WRITE_DUAL, bool WRITE_ITERS, bool WRITE_HESS>
 __global__ __launch_bounds__(kFwdBlock) void newton_fwd_kernel(const void* __restrict__ H,
                                                                 float* __restrict__ P,
                                                                 float* __restrict__ dual,
-                                                                int32_t* __restrict__ iters, int64_t B,
+                                                                int32_t* __restrict__ iters,
+                                                                float* __restrict__ hess, int64_t B,
                                                                 int64_t chunk, float tol, int max_iter) {
     constexpr int NW = RawWords<DT>::n;
     const int lane = threadIdx.x & 63;
@@ -333,7 +342,8 @@ __global__ __launch_bounds__(kFwdBlock) void newton_fwd_kernel(const void* __res
     // initialised and not finished at its initial point: T rows (v4f 0..3), a (4),
     // beta_1..3 and the problem's offset (5), the column weights and gradient at the
     // initial point (6..8). The lane that takes it leaves the output of its previous
-    // problem in its place: P rows (0..3), dual (4..5), (offset or -1, status) (6).
+    // problem in its place: P rows (0..3), dual (4..5), (offset or -1, status) (6), and in
+    // the saved-Hessian variant the column weights of P (7..8).
     __shared__ v4f ring_all[kFwdWaves][64 * kSlot];
     __shared__ int32_t next_batch;  // next unclaimed batch of the block's range
     v4f* const ring = ring_all[wv];
@@ -402,11 +412,10 @@ __global__ __launch_bounds__(kFwdBlock) void newton_fwd_kernel(const void* __res
             const int32_t ip = __float_as_int(sp[6].x);
             const v4f pv = sp[lane & 3];
             int32_t id = -1;
-            v4f dv = {0.f, 0.f, 0.f, 0.f};
-            if constexpr (WRITE_DUAL) {
-                id = __float_as_int(sd[6].x);
-                dv = sd[4 + (lane & 1)];
-            }
+            v4f dv = {0.f, 0.f, 0.f, 0.f}, hv = {0.f, 0.f, 0.f, 0.f};
+            if constexpr (WRITE_DUAL || WRITE_HESS) id = __float_as_int(sd[6].x);
+            if constexpr (WRITE_DUAL) dv = sd[4 + (lane & 1)];
+            if constexpr (WRITE_HESS) hv = sd[7 + (lane & 1)];
             int32_t ii = -1, st = 0;
             if constexpr (WRITE_ITERS) {
                 const v4f sv = si[6];
@@ -418,6 +427,8 @@ __global__ __launch_bounds__(kFwdBlock) void newton_fwd_kernel(const void* __res
             if (ep < m && ip >= 0) __builtin_nontemporal_store(pv, reinterpret_cast<v4f*>(P) + 4 * (lo + ip) + (lane & 3));
             if constexpr (WRITE_DUAL)
                 if (ed < m && id >= 0) reinterpret_cast<v4f*>(dual)[2 * (lo + id) + (lane & 1)] = dv;
+            if constexpr (WRITE_HESS)
+                if (ed < m && id >= 0) reinterpret_cast<v4f*>(hess)[2 * (lo + id) + (lane & 1)] = hv;
             if constexpr (WRITE_ITERS)
                 if (lane < m && ii >= 0) iters[lo + ii] = st;
         }
@@ -436,6 +447,11 @@ __global__ __launch_bounds__(kFwdBlock) void newton_fwd_kernel(const void* __res
             sl[5] = v4f{c0 * kLn2, c1 * kLn2, c2 * kLn2, c0 * 0.f};  // beta_4 = 0, NaN if poisoned
         }
         sl[6] = v4f{__int_as_float(idx), __int_as_float(st), 0.f, 0.f};
+        if constexpr (WRITE_HESS) {
+            const Weights W = column_weights(To);
+            sl[7] = v4f{W.w01, W.w02, W.w03, W.w12};
+            sl[8] = v4f{W.w13, W.w23, 0.f, 0.f};
+        }
     };
 
     // Initialise the batch whose raw words are loaded, one problem per lane with the whole
@@ -619,7 +635,8 @@ __global__ __launch_bounds__(kFwdBlock) void newton_fwd_kernel(const void* __res
             if (nxt >= nbatch) {
                 // nothing left to initialise: lanes still holding an output write it and idle
                 if (has_out)
-                    store_output<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, lo + rel, T, a, b0, b1, b2, status);
+                    store_output<WRITE_DUAL, WRITE_ITERS, WRITE_HESS>(P, dual, iters, hess, lo + rel, T, a, b0, b1,
+                                                                      b2, status);
                 has_out = false;
                 want = false;
                 break;
@@ -812,8 +829,12 @@ __global__ __launch_bounds__(256) void newton_fwd_quad_kernel(const void* __rest
 // ---------------------------------------------------------------------------
 // Backward (Sec. 4.2)
 // ---------------------------------------------------------------------------
-// dH for one problem from T (= P) and G (= dP): -D of eq. derivative, Sec. 4.2.
-__device__ __forceinline__ void implicit_vjp(const float T[16], const float G[16], float out[16]) {
+// dH for one problem from T (= P) and G (= dP): -D of eq. derivative, Sec. 4.2. With
+// GIVEN_W the column weights come from the forward (the Hessian at the solution, which is
+// the Delta of eq. derivative: the saved-Hessian reading of Sec. 4.2) instead of from T.
+template <bool GIVEN_W = false>
+__device__ __forceinline__ void implicit_vjp(const float T[16], const float G[16], float out[16],
+                                             const float* Wg = nullptr) {
     // W_jk = sum_i T_ij T_ik; F_jk = sum_i T_ij T_ik (G_ij - G_ik): the right-hand
     // side mu_c,j - sum_i T_ij mu_r,i of eq. derivative is sum_{k != j} F_jk.
     float W01 = 0.f, W02 = 0.f, W03 = 0.f, W12 = 0.f, W13 = 0.f, W23 = 0.f;
@@ -823,12 +844,15 @@ __device__ __forceinline__ void implicit_vjp(const float T[16], const float G[16
         const float t0 = T[4 * i], t1 = T[4 * i + 1], t2 = T[4 * i + 2], t3 = T[4 * i + 3];
         const float g0 = G[4 * i], g1 = G[4 * i + 1], g2 = G[4 * i + 2], g3 = G[4 * i + 3];
         float p;
-        p = t0 * t1; W01 += p; F01 = __builtin_fmaf(p, g0 - g1, F01);
-        p = t0 * t2; W02 += p; F02 = __builtin_fmaf(p, g0 - g2, F02);
-        p = t0 * t3; W03 += p; F03 = __builtin_fmaf(p, g0 - g3, F03);
-        p = t1 * t2; W12 += p; F12 = __builtin_fmaf(p, g1 - g2, F12);
-        p = t1 * t3; W13 += p; F13 = __builtin_fmaf(p, g1 - g3, F13);
-        p = t2 * t3; W23 += p; F23 = __builtin_fmaf(p, g2 - g3, F23);
+        p = t0 * t1; if constexpr (!GIVEN_W) W01 += p; F01 = __builtin_fmaf(p, g0 - g1, F01);
+        p = t0 * t2; if constexpr (!GIVEN_W) W02 += p; F02 = __builtin_fmaf(p, g0 - g2, F02);
+        p = t0 * t3; if constexpr (!GIVEN_W) W03 += p; F03 = __builtin_fmaf(p, g0 - g3, F03);
+        p = t1 * t2; if constexpr (!GIVEN_W) W12 += p; F12 = __builtin_fmaf(p, g1 - g2, F12);
+        p = t1 * t3; if constexpr (!GIVEN_W) W13 += p; F13 = __builtin_fmaf(p, g1 - g3, F13);
+        p = t2 * t3; if constexpr (!GIVEN_W) W23 += p; F23 = __builtin_fmaf(p, g2 - g3, F23);
+    }
+    if constexpr (GIVEN_W) {
+        W01 = Wg[0]; W02 = Wg[1]; W03 = Wg[2]; W12 = Wg[3]; W13 = Wg[4]; W23 = Wg[5];
     }
     // Delta w = rhs, Delta = Hessian at T (Laplacian of W grounded at column 4).
     // Eliminating a node joins its neighbours j,k by W_jp W_pk / piv and moves its
@@ -879,10 +903,11 @@ constexpr int kBwdBlock = 256;
 constexpr int kBwdWaves = kBwdBlock / 64;
 constexpr int kBwdStride = 5;  // v4f per problem in the LDS buffer (4 rows + 1 pad: no bank conflicts on reads)
 
-template <int DT>
+template <int DT, bool HESS = false>
 __global__ __launch_bounds__(kBwdBlock) void implicit_bwd_kernel(const float* __restrict__ P,
                                                                   const void* __restrict__ dP,
-                                                                  float* __restrict__ dH, int64_t B) {
+                                                                  float* __restrict__ dH, int64_t B,
+                                                                  const float* __restrict__ hess) {
     __shared__ v4f buf_all[kBwdWaves][64 * kBwdStride];
     const int lane = threadIdx.x & 63;
     const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
@@ -911,6 +936,15 @@ __global__ __launch_bounds__(kBwdBlock) void implicit_bwd_kernel(const float* __
         for (int q = 0; q < NG; ++q) {
             const int k = 64 * q + lane;
             gc[q] = k < GP * n ? __builtin_nontemporal_load(G4 + GP * base + k) : v4u{0u, 0u, 0u, 0u};
+        }
+        [[maybe_unused]] v4f hc[2];  // saved column weights (saved-Hessian variant), two pieces per problem
+        if constexpr (HESS) {
+            const v4f* W4 = reinterpret_cast<const v4f*>(hess);
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                const int k = 64 * q + lane;
+                hc[q] = k < 2 * n ? __builtin_nontemporal_load(W4 + 2 * base + k) : v4f{0.f, 0.f, 0.f, 0.f};
+            }
         }
         // P: pieces to one problem per lane
 #pragma unroll
@@ -942,7 +976,21 @@ __global__ __launch_bounds__(kBwdBlock) void implicit_bwd_kernel(const float* __
         }
         __builtin_amdgcn_wave_barrier();
         float out[16];
-        implicit_vjp(T, G, out);
+        if constexpr (HESS) {
+            // saved column weights: two 16-byte pieces per problem, through the same buffer
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                const int k = 64 * q + lane;
+                buf[(k >> 1) * kBwdStride + (k & 1)] = hc[q];
+            }
+            __builtin_amdgcn_wave_barrier();
+            const v4f w0 = buf[lane * kBwdStride], w1 = buf[lane * kBwdStride + 1];
+            __builtin_amdgcn_wave_barrier();
+            const float Wg[6] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y};
+            implicit_vjp<true>(T, G, out, Wg);
+        } else {
+            implicit_vjp(T, G, out);
+        }
         // dH: one problem per lane to pieces
 #pragma unroll
         for (int r = 0; r < 4; ++r)
@@ -2251,12 +2299,12 @@ int launch_status() {
 
 // Blocks of the forward kernel resident at once on one CU (VGPR-limited),
 // from the occupancy calculator; queried once per instantiation.
-template <int DT, bool WD, bool WI>
+template <int DT, bool WD, bool WI, bool WH>
 int fwd_blocks_per_cu() {
     static int cached = 0;
     if (cached == 0) {
         int nb = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, newton_fwd_kernel<DT, WD, WI>, kFwdBlock, 0) !=
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, newton_fwd_kernel<DT, WD, WI, WH>, kFwdBlock, 0) !=
                 hipSuccess || nb <= 0)
             nb = 1;
         cached = nb;
@@ -2266,17 +2314,17 @@ int fwd_blocks_per_cu() {
 
 // Launch one resident workgroup per CU (as many as the occupancy calculator allows),
 // each owning a contiguous range of whole 64-problem batches that its waves share.
-template <int DT, bool WD, bool WI>
+template <int DT, bool WD, bool WI, bool WH = false>
 int launch_fwd(const void* H, float* P, float* dual, int32_t* iters, int64_t B, float tol,
-               int max_iter, hipStream_t stream, int cus) {
+               int max_iter, hipStream_t stream, int cus, float* hess = nullptr) {
     const int64_t batches = (B + 63) / 64;
-    int64_t blocks = static_cast<int64_t>(cus) * fwd_blocks_per_cu<DT, WD, WI>();
+    int64_t blocks = static_cast<int64_t>(cus) * fwd_blocks_per_cu<DT, WD, WI, WH>();
     if (blocks > batches) blocks = batches;
     const int64_t chunk = ((batches + blocks - 1) / blocks) * 64;
     if (chunk > INT32_MAX / 2) return BIRKHOFF4_ERR_SIZE;  // problems are 32-bit offsets in a range
     blocks = (B + chunk - 1) / chunk;
-    hipLaunchKernelGGL((newton_fwd_kernel<DT, WD, WI>), dim3(static_cast<unsigned>(blocks)),
-                       dim3(kFwdBlock), 0, stream, H, P, dual, iters, B, chunk, tol, max_iter);
+    hipLaunchKernelGGL((newton_fwd_kernel<DT, WD, WI, WH>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(kFwdBlock), 0, stream, H, P, dual, iters, hess, B, chunk, tol, max_iter);
     return launch_status();
 }
 
@@ -2307,6 +2355,15 @@ int dispatch_fwd(const void* H, float* P, float* dual, int32_t* iters, int64_t B
     if (dual) return launch_fwd<DT, true, false>(H, P, dual, iters, B, tol, max_iter, stream, cus);
     if (iters) return launch_fwd<DT, false, true>(H, P, dual, iters, B, tol, max_iter, stream, cus);
     return launch_fwd<DT, false, false>(H, P, dual, iters, B, tol, max_iter, stream, cus);
+}
+
+template <int DT>
+int dispatch_fwd_hess(const void* H, float* P, float* dual, int32_t* iters, float* hess, int64_t B, float tol,
+                      int max_iter, hipStream_t stream, int cus) {
+    if (dual && iters) return launch_fwd<DT, true, true, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, hess);
+    if (dual) return launch_fwd<DT, true, false, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, hess);
+    if (iters) return launch_fwd<DT, false, true, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, hess);
+    return launch_fwd<DT, false, false, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, hess);
 }
 
 // n = 8: one range of problems per wave, blocks scheduled by the hardware.
@@ -2385,6 +2442,31 @@ int birkhoff4_fwd_ex2(const void* H, int h_dtype, float* P, float* dual, int32_t
     if (h_dtype == BIRKHOFF4_BF16)
         return dispatch_fwd<BIRKHOFF4_BF16>(H, P, dual, iters, B, tol, max_iter, stream, cus);
     return dispatch_fwd<BIRKHOFF4_F32>(H, P, dual, iters, B, tol, max_iter, stream, cus);
+}
+
+int birkhoff4_fwd_hess(const void* H, int h_dtype, float* P, float* dual, float* hess, int32_t* iters,
+                       int64_t B, float tol, int max_iter, hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 64)) return BIRKHOFF4_ERR_SIZE;
+    if (!dtype_ok(h_dtype)) return BIRKHOFF4_ERR_DTYPE;
+    if (!(tol >= 0.f)) return BIRKHOFF4_ERR_TOL;
+    if (max_iter < 0 || max_iter > kMaxIterCap) return BIRKHOFF4_ERR_MAX_ITER;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!H || !P || !hess) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(H) || misaligned(P) || misaligned(dual) || misaligned(hess) || misaligned(iters))
+        return BIRKHOFF4_ERR_ALIGN;
+    const size_t nh = static_cast<size_t>(B) * 16 * dtype_bytes(h_dtype);
+    const size_t np = static_cast<size_t>(B) * 64, nd = dual ? static_cast<size_t>(B) * 32 : 0,
+                 nw = static_cast<size_t>(B) * 32, ni = iters ? static_cast<size_t>(B) * 4 : 0;
+    if (overlaps(H, nh, P, np) || overlaps(H, nh, dual, nd) || overlaps(H, nh, iters, ni) ||
+        overlaps(H, nh, hess, nw) || overlaps(P, np, dual, nd) || overlaps(P, np, iters, ni) ||
+        overlaps(P, np, hess, nw) || overlaps(dual, nd, iters, ni) || overlaps(dual, nd, hess, nw) ||
+        overlaps(hess, nw, iters, ni))
+        return BIRKHOFF4_ERR_OVERLAP;
+    int cus = 0;
+    if (int e = device_cus(&cus)) return e;
+    if (h_dtype == BIRKHOFF4_BF16)
+        return dispatch_fwd_hess<BIRKHOFF4_BF16>(H, P, dual, iters, hess, B, tol, max_iter, stream, cus);
+    return dispatch_fwd_hess<BIRKHOFF4_F32>(H, P, dual, iters, hess, B, tol, max_iter, stream, cus);
 }
 
 int birkhoff4_fwd_ex(const void* H, int h_dtype, float* P, float* dual, int32_t* iters, int64_t B,
@@ -2494,10 +2576,32 @@ int birkhoff4_bwd_ex(const float* P, const void* dP, int dp_dtype, float* dH, in
     const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
     if (dp_dtype == BIRKHOFF4_BF16)
         hipLaunchKernelGGL(implicit_bwd_kernel<BIRKHOFF4_BF16>, dim3(static_cast<unsigned>(grid)), dim3(kBwdBlock),
-                           0, stream, P, dP, dH, B);
+                           0, stream, P, dP, dH, B, nullptr);
     else
         hipLaunchKernelGGL(implicit_bwd_kernel<BIRKHOFF4_F32>, dim3(static_cast<unsigned>(grid)), dim3(kBwdBlock),
-                           0, stream, P, dP, dH, B);
+                           0, stream, P, dP, dH, B, nullptr);
+    return launch_status();
+}
+
+int birkhoff4_bwd_hess(const float* P, const float* hess, const void* dP, int dp_dtype, float* dH, int64_t B,
+                       hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 64)) return BIRKHOFF4_ERR_SIZE;
+    if (!dtype_ok(dp_dtype)) return BIRKHOFF4_ERR_DTYPE;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!P || !hess || !dP || !dH) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(P) || misaligned(hess) || misaligned(dP) || misaligned(dH)) return BIRKHOFF4_ERR_ALIGN;
+    const size_t n = static_cast<size_t>(B) * 64, ng = static_cast<size_t>(B) * 16 * dtype_bytes(dp_dtype),
+                 nw = static_cast<size_t>(B) * 32;
+    if (overlaps(dH, n, P, n) || overlaps(dH, n, dP, ng) || overlaps(dH, n, hess, nw)) return BIRKHOFF4_ERR_OVERLAP;
+    const int64_t chunks = (B + 63) / 64;
+    const int64_t want = (chunks + kBwdWaves - 1) / kBwdWaves;
+    const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
+    if (dp_dtype == BIRKHOFF4_BF16)
+        hipLaunchKernelGGL((implicit_bwd_kernel<BIRKHOFF4_BF16, true>), dim3(static_cast<unsigned>(grid)),
+                           dim3(kBwdBlock), 0, stream, P, dP, dH, B, hess);
+    else
+        hipLaunchKernelGGL((implicit_bwd_kernel<BIRKHOFF4_F32, true>), dim3(static_cast<unsigned>(grid)),
+                           dim3(kBwdBlock), 0, stream, P, dP, dH, B, hess);
     return launch_status();
 }
 

@@ -168,3 +168,24 @@ def test_binding_output_and_device_checks():
     b4._same_device(good, torch.empty(1))
     with pytest.raises(ValueError):
         b4._same_device(good, torch.empty(1, device="meta"))
+
+
+def test_saved_hessian_argument_errors():
+    lib = b4.lib()
+    f = lib.birkhoff4_fwd_hess  # (H, h_dtype, P, dual, hess, iters, B, tol, max_iter, stream)
+    assert f(A, 0, Bp, None, C, None, 0, 1e-6, 20, None) == OK
+    assert f(A, 0, Bp, None, C, None, -1, 1e-6, 20, None) == ERR_SIZE
+    assert f(A, 0, Bp, None, None, None, 10, 1e-6, 20, None) == ERR_NULL
+    assert f(A, 3, Bp, None, C, None, 10, 1e-6, 20, None) == ERR_DTYPE
+    assert f(A, 0, Bp, None, C, None, 10, -1.0, 20, None) == ERR_TOL
+    assert f(A, 0, Bp, None, C, None, 10, 1e-6, -2, None) == ERR_MAX_ITER
+    assert f(A, 0, Bp, None, C + 4, None, 10, 1e-6, 20, None) == ERR_ALIGN
+    assert f(A, 0, Bp, None, Bp + 64 * 5, None, 10, 1e-6, 20, None) == ERR_OVERLAP  # hess inside P
+    assert f(A, 0, Bp, D, D + 32 * 3, None, 10, 1e-6, 20, None) == ERR_OVERLAP    # hess inside dual
+    g = lib.birkhoff4_bwd_hess  # (P, hess, dP, dp_dtype, dH, B, stream)
+    assert g(A, Bp, C, 0, D, 0, None) == OK
+    assert g(A, Bp, C, 0, D, -5, None) == ERR_SIZE
+    assert g(A, None, C, 0, D, 5, None) == ERR_NULL
+    assert g(A, Bp, C, 7, D, 5, None) == ERR_DTYPE
+    assert g(A, Bp + 8, C, 0, D, 5, None) == ERR_ALIGN
+    assert g(A, Bp, C, 0, Bp + 32, 5, None) == ERR_OVERLAP  # dH over hess
