@@ -98,8 +98,8 @@ def main() -> int:
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build runs on one GPU only; the projection shards by batch with "
-              "no communication (see the design notes), so only --gpus 1 is measured.",
+        print("bench.py: measures one GPU only; the projection shards by contiguous batch ranges with "
+              "no communication between GPUs, so only --gpus 1 is measured.",
               file=sys.stderr)
         return 2
 
