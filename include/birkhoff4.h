@@ -190,7 +190,11 @@ int birkhoff8_bwd(const float* P, const void* dP, int dp_dtype, float* dH, int64
  *       sums differ there is no solution and the status is BIRKHOFF4_NOT_CONVERGED).
  * eta   regulariser > 0 (BIRKHOFF4_ERR_ETA otherwise).
  * T     [B][4][4] fp32 output: rows sum to a exactly up to rounding, columns to b
- *       within tol (max_j |c_j - b_j| <= tol, absolute).
+ *       within tol: |c_j - b_j| <= tol max(1, b_j) for every column (absolute for
+ *       marginals up to one, relative above, where the fp32 resolution of a column sum
+ *       grows with it; for a = b = 1 this is the Birkhoff test); the last column, whose
+ *       potential is fixed, may in addition differ by |sum a - sum b| as computed in fp32,
+ *       since marginals given in fp32 rarely have exactly equal sums.
  * dual  NULL or [B][8] fp32 output: (alpha_1..4, beta_1..3, beta_4 = 0) in the units of
  *       M, with T_ij = exp((alpha_i + beta_j - M_ij) / eta) (eq. dual).
  * iters NULL or int32 [B]: trial steps taken, BIRKHOFF4_NOT_CONVERGED, or
@@ -206,6 +210,16 @@ int birkhoff4_ot_fwd(const float* M, const float* a, const float* b, float eta, 
  * overlap the inputs. */
 int birkhoff4_ot_bwd(const float* T, const float* a, const float* dT, float eta, float* dM,
                      int64_t B, hipStream_t stream);
+
+/* General entropic OT for 8 x 8 problems: birkhoff4_ot_fwd / birkhoff4_ot_bwd with n = m = 8
+ * (eq. entropic, eq. grad_hess, eq. derivative). M, T, dT, dM are [B][8][8] fp32 (256 bytes per
+ * problem), a and b [B][8] fp32, dual [B][16] = (alpha_1..8, beta_1..7, beta_8 = 0) with
+ * T_ij = exp((alpha_i + beta_j - M_ij) / eta); iters as for birkhoff8_fwd. Arguments, return
+ * codes, status words and ownership as for the 4 x 4 calls. */
+int birkhoff8_ot_fwd(const float* M, const float* a, const float* b, float eta, float* T, float* dual,
+                     int32_t* iters, int64_t B, float tol, int max_iter, hipStream_t stream);
+int birkhoff8_ot_bwd(const float* T, const float* a, const float* dT, float eta, float* dM, int64_t B,
+                     hipStream_t stream);
 
 /* Human-readable text for a return code (static storage). */
 const char* birkhoff4_strerror(int code);

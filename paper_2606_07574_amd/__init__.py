@@ -13,6 +13,7 @@ a GPU, the calls raise.
     P = sk_fwd(H, 20); dH = sk_bwd(H, dP, 20)   # Sinkhorn-Knopp baseline
     P, dual = fwd8(H); dH = bwd8(P, dP); P = project8(H)   # the same for 8 x 8 matrices
     T, dual = ot_fwd(M, a, b, eta); dM = ot_bwd(T, a, dT, eta)  # general entropic OT, 4 x 4
+    T, dual = ot8_fwd(M, a, b, eta); dM = ot8_bwd(T, a, dT, eta)  # the same for 8 x 8
 """
 from __future__ import annotations
 
@@ -61,6 +62,8 @@ def _load():
         "birkhoff4_ot_fwd": [vp, vp, vp, f32, vp, vp, vp, i64, f32, i32, st],
         "birkhoff4_ot_bwd": [vp, vp, vp, f32, vp, i64, st],
         "birkhoff8_bwd": [vp, vp, i32, vp, i64, st],
+        "birkhoff8_ot_fwd": [vp, vp, vp, f32, vp, vp, vp, i64, f32, i32, st],
+        "birkhoff8_ot_bwd": [vp, vp, vp, f32, vp, i64, st],
         "birkhoff4_version": [],
     }
     for name, args in sigs.items():
@@ -286,11 +289,11 @@ def project8(H: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_
     return Birkhoff8Fn.apply(H, tol, max_iter)
 
 
-def _marginals(x: torch.Tensor, lead, name: str) -> None:
+def _marginals(x: torch.Tensor, lead, name: str, n: int = 4) -> None:
     if not x.is_cuda or x.dtype != torch.float32 or not x.is_contiguous():
         raise ValueError(f"{name} must be a contiguous float32 GPU tensor")
-    if tuple(x.shape) != (*lead, 4):
-        raise ValueError(f"{name} must have shape {(*lead, 4)}, got {tuple(x.shape)}")
+    if tuple(x.shape) != (*lead, n):
+        raise ValueError(f"{name} must have shape {(*lead, n)}, got {tuple(x.shape)}")
 
 
 def ot_fwd(M: torch.Tensor, a: torch.Tensor, b: torch.Tensor, eta: float = 1.0, tol: float = DEFAULT_TOL,
@@ -348,6 +351,62 @@ class OTFn(torch.autograd.Function):
 def ot(M: torch.Tensor, a: torch.Tensor, b: torch.Tensor, eta: float = 1.0, tol: float = DEFAULT_TOL,
        max_iter: int = DEFAULT_MAX_ITER) -> torch.Tensor:
     return OTFn.apply(M, a, b, eta, tol, max_iter)
+
+
+def ot8_fwd(M: torch.Tensor, a: torch.Tensor, b: torch.Tensor, eta: float = 1.0, tol: float = DEFAULT_TOL,
+            max_iter: int = DEFAULT_MAX_ITER, want_dual: bool = True, want_iters: bool = False):
+    """ot_fwd for trailing 8x8 cost matrices and marginals [..., 8]: (T, dual [..., 16] or None, iters)."""
+    B = _batch(M, "M", 8)
+    if M.dtype != torch.float32:
+        raise TypeError("M must be float32")
+    lead = M.shape[:-2]
+    _marginals(a, lead, "a", 8)
+    _marginals(b, lead, "b", 8)
+    _same_device(M, a, b)
+    T = torch.empty(M.shape, dtype=torch.float32, device=M.device)
+    dual = torch.empty(*lead, 16, dtype=torch.float32, device=M.device) if want_dual else None
+    iters = torch.empty(lead, dtype=torch.int32, device=M.device) if want_iters else None
+    with torch.cuda.device(M.device):
+        _check(_load().birkhoff8_ot_fwd(_ptr(M), _ptr(a), _ptr(b), float(eta), _ptr(T), _ptr(dual), _ptr(iters),
+                                        B, float(tol), int(max_iter), _stream(M)))
+    return T, dual, iters
+
+
+def ot8_bwd(T: torch.Tensor, a: torch.Tensor, dT: torch.Tensor, eta: float = 1.0) -> torch.Tensor:
+    """ot_bwd for trailing 8x8 problems."""
+    B = _batch(T, "T", 8)
+    if _batch(dT, "dT", 8) != B:
+        raise ValueError("T and dT batch sizes differ")
+    if T.dtype != torch.float32 or dT.dtype != torch.float32:
+        raise TypeError("T and dT must be float32")
+    _marginals(a, T.shape[:-2], "a", 8)
+    _same_device(T, a, dT)
+    dM = torch.empty(T.shape, dtype=torch.float32, device=T.device)
+    with torch.cuda.device(T.device):
+        _check(_load().birkhoff8_ot_bwd(_ptr(T), _ptr(a), _ptr(dT), float(eta), _ptr(dM), B, _stream(T)))
+    return dM
+
+
+class OT8Fn(torch.autograd.Function):
+    """OTFn for 8x8 problems."""
+
+    @staticmethod
+    def forward(ctx, M, a, b, eta=1.0, tol=DEFAULT_TOL, max_iter=DEFAULT_MAX_ITER):
+        a = a.contiguous()
+        T, _, _ = ot8_fwd(M.contiguous(), a, b.contiguous(), eta, tol, max_iter, want_dual=False)
+        ctx.save_for_backward(T, a)
+        ctx.eta = eta
+        return T
+
+    @staticmethod
+    def backward(ctx, dT):
+        T, a = ctx.saved_tensors
+        return ot8_bwd(T, a, dT.contiguous().float(), ctx.eta), None, None, None, None, None
+
+
+def ot8(M: torch.Tensor, a: torch.Tensor, b: torch.Tensor, eta: float = 1.0, tol: float = DEFAULT_TOL,
+        max_iter: int = DEFAULT_MAX_ITER) -> torch.Tensor:
+    return OT8Fn.apply(M, a, b, eta, tol, max_iter)
 
 
 def version() -> int:

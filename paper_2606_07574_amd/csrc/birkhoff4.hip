@@ -1209,6 +1209,7 @@ constexpr int kB8Block = 256;
 constexpr int kB8Waves = kB8Block / 64;
 constexpr int kB8Ring = 32;  // problems per initialisation batch (= ring slots per wave)
 constexpr int kB8Slot = 23;  // v4f per ring slot (22 used; odd, so that slots start in different banks)
+constexpr int kB8SlotOT = 27;  // the same with the two marginals (26 used)
 #ifndef B8_RANGES
 #define B8_RANGES 4096
 #endif
@@ -1256,6 +1257,23 @@ __device__ __forceinline__ void weights8(const float T[64], float W[28]) {
             for (int i = 1; i < 8; ++i) s = __builtin_fmaf(T[8 * i + j], T[8 * i + k], s);
             W[pw8(j, k)] = s;
         }
+}
+
+// W_jk = sum_i w_i T_ij T_ik (general marginals, eq. grad_hess: w = a for S, 1/a for T).
+__device__ __forceinline__ void weights8w(const float T[64], const float w[8], float W[28]) {
+#pragma unroll
+    for (int j = 0; j < 7; ++j) {
+        float c[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) c[i] = T[8 * i + j] * w[i];
+#pragma unroll
+        for (int k = j + 1; k < 8; ++k) {
+            float s = c[0] * T[k];
+#pragma unroll
+            for (int i = 1; i < 8; ++i) s = __builtin_fmaf(c[i], T[8 * i + k], s);
+            W[pw8(j, k)] = s;
+        }
+    }
 }
 
 // Newton direction in log2 units, d = -log2(e) (Lap(W) + lam I)^{-1} g over nodes 0..6
@@ -1390,12 +1408,64 @@ __device__ __forceinline__ float psum(float x) {
     return x + __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, true));
 }
 
-template <int DT, bool WRITE_DUAL, bool WRITE_ITERS>
+// The OT stopping test: |c_j - b_j| <= tol max(1, b_j) for every column (absolute for
+// marginals up to one, relative above: the fp32 resolution of a column sum grows with it).
+// The last column, whose potential is fixed, also absorbs `slack` = |sum a - sum b|, which
+// marginals given in fp32 cannot make exactly zero.
+__device__ __forceinline__ bool ot_within_tol8(const float g[8], const float b[8], float tol, float slack) {
+    float x = -1.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        x = __builtin_fmaxf(x, __builtin_fabsf(g[j]) - tol * __builtin_fmaxf(1.f, b[j]) - (j == 7 ? slack : 0.f));
+    return x <= 0.f;
+}
+
+// |sum a - sum b| in fp32 (for the stopping test)
+__device__ __forceinline__ float mass_slack8(const float a[8], const float b[8]) {
+    return __builtin_fabsf((((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]))) -
+                           (((b[0] + b[1]) + (b[2] + b[3])) + ((b[4] + b[5]) + (b[6] + b[7]))));
+}
+
+// Output of one 8 x 8 OT problem: T = diag(a) S, dual alpha_i = eta (ln a_i - lse_i), beta_j =
+// eta x_j (natural units, beta_8 = 0), and the status word.
+template <bool WRITE_DUAL, bool WRITE_ITERS>
+__device__ __forceinline__ void store_output8_ot(float* __restrict__ P, float* __restrict__ dual,
+                                                 int32_t* __restrict__ iters, int64_t b, const float S[64],
+                                                 const float la[8], const float x[7], const float ma[8], float eta,
+                                                 int status) {
+    v4f* pp = reinterpret_cast<v4f*>(P) + 16 * b;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+        const float m = ma[q >> 1];
+        pp[q] = v4f{m * S[4 * q], m * S[4 * q + 1], m * S[4 * q + 2], m * S[4 * q + 3]};
+    }
+    if constexpr (WRITE_DUAL) {
+        const float e2 = eta * kLn2;
+        v4f* dp = reinterpret_cast<v4f*>(dual) + 4 * b;
+        dp[0] = v4f{e2 * (lg2(ma[0]) - la[0]), e2 * (lg2(ma[1]) - la[1]), e2 * (lg2(ma[2]) - la[2]),
+                    e2 * (lg2(ma[3]) - la[3])};
+        dp[1] = v4f{e2 * (lg2(ma[4]) - la[4]), e2 * (lg2(ma[5]) - la[5]), e2 * (lg2(ma[6]) - la[6]),
+                    e2 * (lg2(ma[7]) - la[7])};
+        dp[2] = v4f{e2 * x[0], e2 * x[1], e2 * x[2], e2 * x[3]};
+        dp[3] = v4f{e2 * x[4], e2 * x[5], e2 * x[6], x[0] * 0.f};
+    }
+    if constexpr (WRITE_ITERS) iters[b] = status;
+}
+
+// With OT the kernel solves general entropic OT (eq. entropic) instead: H is the cost M
+// (fp32), av and bv the marginals, eta the regulariser; the state is S = diag(a)^-1 T in
+// product form (the 4 x 4 OT kernel's substitution), the gradient sum_i a_i S_ij - b_j, the
+// weights sum_i a_i S_ij S_ik and the f change sum_i a_i l_i - sum_j b_j s_j.
+template <int DT, bool WRITE_DUAL, bool WRITE_ITERS, bool OT>
 __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __restrict__ H, float* __restrict__ P,
                                                                 float* __restrict__ dual,
                                                                 int32_t* __restrict__ iters, int64_t B, float tol,
-                                                                int max_iter, int64_t per_wave) {
+                                                                int max_iter, int64_t per_wave,
+                                                                const float* __restrict__ av,
+                                                                const float* __restrict__ bv, float eta) {
     constexpr int NW = RawWords8<DT>::n;
+    constexpr int SLOT = OT ? kB8SlotOT : kB8Slot;
+    const float hsc = OT ? -kLog2e / eta : kLog2e;  // log2-unit logits per unit of H (or of M)
     const int lane = threadIdx.x & 63;
     const int hf = lane & 1;  // half of the problem this lane initialises (rows 4 hf .. 4 hf + 3)
     const int pb = lane >> 1;  // its position in an initialisation batch
@@ -1404,11 +1474,15 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
     // Per-wave ring: slot p holds the initial point of position p of the last batch: row
     // 4 h + r of T in v4f 4 r + 2 h and 4 r + 2 h + 1 (the two lanes of a pair write
     // different banks), a (16..17), beta_1..4 (18), beta_5..7 and the offset (19), g
-    // (20..21); order[0 .. nfresh) lists the positions whose problems still need steps.
-    __shared__ v4f ring_all[kB8Waves][kB8Ring * kB8Slot];
+    // (20..21), with OT the marginals a (22..23) and b (24..25); order[0 .. nfresh) lists the
+    // positions whose problems still need steps. With OT each lane also keeps the marginals of
+    // its current problem in LDS (a in v4f 0..1, b in 2..3 of its four).
+    __shared__ v4f ring_all[kB8Waves][kB8Ring * SLOT];
     __shared__ int32_t order_all[kB8Waves][kB8Ring];
+    __shared__ v4f marg_all[OT ? kB8Waves : 1][OT ? 64 * 4 : 1];
     v4f* const ring = ring_all[wv];
     int32_t* const order = order_all[wv];
+    v4f* const marg = marg_all[OT ? wv : 0] + (OT ? 4 * lane : 0);
     // The wave owns problems r0 .. r1 - 1.
     const int64_t r0 = (static_cast<int64_t>(blockIdx.x) * kB8Waves + wv) * per_wave;
     if (r0 >= B) return;  // uniform across the wave
@@ -1419,7 +1493,20 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
 #pragma unroll
     for (int q = 0; q < NW; ++q) raw[q] = 0u;
     int64_t bnext = r0;  // first problem of that batch (uniform)
-    if (bnext + pb < r1) load_half8<DT>(H, bnext + pb, hf, raw);
+    v4f pa = {1.f, 1.f, 1.f, 1.f}, pb0 = pa, pb1 = pa;  // OT: its marginals (this lane's four a_i, all b_j)
+    auto prefetch = [&]() {
+        if (bnext + pb < r1) {
+            load_half8<DT>(H, bnext + pb, hf, raw);
+            if constexpr (OT) {
+                const v4f* a4 = reinterpret_cast<const v4f*>(av) + 2 * (bnext + pb);
+                const v4f* b4 = reinterpret_cast<const v4f*>(bv) + 2 * (bnext + pb);
+                pa = a4[hf];
+                pb0 = b4[0];
+                pb1 = b4[1];
+            }
+        }
+    };
+    prefetch();
     int nfresh = 0, icur = 0;  // order[icur .. nfresh) not yet taken
 
     bool active = false;  // holds an unfinished problem
@@ -1435,6 +1522,9 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
 #pragma unroll
     for (int k = 0; k < 28; ++k) W[k] = 0.f;
     float lam = 0.f, gn2 = 0.f, t = 1.f, fofs = 0.f, gsum = 0.f;
+    // rounding-noise threshold of f and floor of the Levenberg-Marquardt shift (OT: scaled by
+    // the problem's mass / 8, so that unit marginals give the Birkhoff values)
+    float fnoise = kFNoise, lmfloor = kLMFloor;
     int cnt = 0;  // bits 0-15: trial steps; bits 16-18: log2 of the initial trial step
 
     // Initialise the loaded batch with the whole wave, two lanes per problem: column means
@@ -1449,6 +1539,15 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
         const bool valid = bp < r1;
         float cm[8];
         bool fin = true;
+        // OT: this lane's four row masses and all eight column masses
+        const float ma[4] = {pa.x, pa.y, pa.z, pa.w};
+        const float mb[8] = {pb0.x, pb0.y, pb0.z, pb0.w, pb1.x, pb1.y, pb1.z, pb1.w};
+        if constexpr (OT) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) fin = fin && __builtin_isfinite(ma[r]) && ma[r] > 0.f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) fin = fin && __builtin_isfinite(mb[j]) && mb[j] > 0.f;
+        }
 #pragma unroll
         for (int j = 0; j < 8; ++j) cm[j] = 0.f;
 #pragma unroll
@@ -1458,7 +1557,7 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 fin = fin && __builtin_isfinite(h[j]);
-                cm[j] += h[j] * kLog2e;
+                cm[j] += h[j] * hsc;
             }
         }
         fin = fin && __builtin_amdgcn_mov_dpp(static_cast<int>(fin), 0xB1, 0xF, 0xF, true);
@@ -1468,7 +1567,12 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
         float bi[7];
 #pragma unroll
         for (int j = 0; j < 7; ++j) bi[j] = 0.125f * (cm[7] - cm[j]) + poison;
-        v4f* const sl = ring + pb * kB8Slot;
+        if constexpr (OT) {  // x_j + log2(b_j / b_8): exact for separable costs
+            const float ib7 = rcp(mb[7]);
+#pragma unroll
+            for (int j = 0; j < 7; ++j) bi[j] += lg2(mb[j] * ib7);
+        }
+        v4f* const sl = ring + pb * SLOT;
         float ai[4], gi[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) gi[j] = 0.f;
@@ -1477,7 +1581,7 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
             float u[8];
             decode_row8<DT>(raw, r, u);
 #pragma unroll
-            for (int j = 0; j < 8; ++j) u[j] = __builtin_fmaf(u[j], kLog2e, j < 7 ? bi[j] : poison);
+            for (int j = 0; j < 8; ++j) u[j] = __builtin_fmaf(u[j], hsc, j < 7 ? bi[j] : poison);
             float m = u[0];
 #pragma unroll
             for (int j = 1; j < 8; ++j) m = __builtin_fmaxf(m, u[j]);
@@ -1489,7 +1593,10 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 u[j] *= rc;
-                gi[j] += u[j];
+                if constexpr (OT)
+                    gi[j] = __builtin_fmaf(ma[r], u[j], gi[j]);
+                else
+                    gi[j] += u[j];
             }
             ai[r] = m + lg2(sum);
             sl[4 * r + 2 * hf] = v4f{u[0], u[1], u[2], u[3]};
@@ -1498,14 +1605,23 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
         float gmax = 0.f;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            gi[j] = psum(gi[j]) - 1.0f;
+            gi[j] = psum(gi[j]) - (OT ? mb[j] : 1.0f);
             gmax = __builtin_fmaxf(gmax, __builtin_fabsf(gi[j]));
         }
         sl[16 + hf] = v4f{ai[0], ai[1], ai[2], ai[3]};
+        if constexpr (OT) {
+            sl[22 + hf] = pa;
+            sl[24 + hf] = hf ? pb1 : pb0;
+        }
         sl[18 + hf] = hf ? v4f{bi[4], bi[5], bi[6], __int_as_float(static_cast<int32_t>(bp - r0))}
                          : v4f{bi[0], bi[1], bi[2], bi[3]};
         sl[20 + hf] = hf ? v4f{gi[4], gi[5], gi[6], gi[7]} : v4f{gi[0], gi[1], gi[2], gi[3]};
-        const bool conv = gmax <= tol;
+        bool conv = gmax <= tol;
+        if constexpr (OT) {
+            const float sa = psum((ma[0] + ma[1]) + (ma[2] + ma[3]));
+            const float sb = ((mb[0] + mb[1]) + (mb[2] + mb[3])) + ((mb[4] + mb[5]) + (mb[6] + mb[7]));
+            conv = ot_within_tol8(gi, mb, tol, __builtin_fabsf(sa - sb));
+        }
         const bool done = valid && (!fin || conv || max_iter == 0);
         const bool fresh = valid && !done;
         const uint64_t fm = __ballot(fresh && hf == 0);
@@ -1515,18 +1631,38 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
         if (done) {
             v4f* pp = reinterpret_cast<v4f*>(P) + 16 * bp + 8 * hf;
 #pragma unroll
-            for (int q = 0; q < 8; ++q) pp[q] = sl[4 * (q >> 1) + 2 * hf + (q & 1)];
+            for (int q = 0; q < 8; ++q) {
+                const v4f u = sl[4 * (q >> 1) + 2 * hf + (q & 1)];
+                pp[q] = OT ? u * ma[q >> 1] : u;
+            }
             if constexpr (WRITE_DUAL) {
                 v4f* dp = reinterpret_cast<v4f*>(dual) + 4 * bp;
-                dp[hf] = v4f{-ai[0] * kLn2, -ai[1] * kLn2, -ai[2] * kLn2, -ai[3] * kLn2};
-                dp[2 + hf] = hf ? v4f{bi[4] * kLn2, bi[5] * kLn2, bi[6] * kLn2, bi[0] * 0.f}  // beta_8 = 0
-                                : v4f{bi[0] * kLn2, bi[1] * kLn2, bi[2] * kLn2, bi[3] * kLn2};
+                if constexpr (OT) {
+                    const float e2 = eta * kLn2;
+                    dp[hf] = v4f{e2 * (lg2(ma[0]) - ai[0]), e2 * (lg2(ma[1]) - ai[1]), e2 * (lg2(ma[2]) - ai[2]),
+                                 e2 * (lg2(ma[3]) - ai[3])};
+                    dp[2 + hf] = hf ? v4f{bi[4] * e2, bi[5] * e2, bi[6] * e2, bi[0] * 0.f}
+                                    : v4f{bi[0] * e2, bi[1] * e2, bi[2] * e2, bi[3] * e2};
+                } else {
+                    dp[hf] = v4f{-ai[0] * kLn2, -ai[1] * kLn2, -ai[2] * kLn2, -ai[3] * kLn2};
+                    dp[2 + hf] = hf ? v4f{bi[4] * kLn2, bi[5] * kLn2, bi[6] * kLn2, bi[0] * 0.f}  // beta_8 = 0
+                                    : v4f{bi[0] * kLn2, bi[1] * kLn2, bi[2] * kLn2, bi[3] * kLn2};
+                }
             }
             if constexpr (WRITE_ITERS)
                 if (hf == 0) iters[bp] = !fin ? BIRKHOFF4_NON_FINITE : (conv ? 0 : BIRKHOFF4_NOT_CONVERGED);
         }
         bnext += kB8Ring;
-        if (bnext + pb < r1) load_half8<DT>(H, bnext + pb, hf, raw);
+        prefetch();
+    };
+
+    // OT: the marginals of this lane's current problem, from its LDS side slot
+    auto load_marg = [&](float ma8[8], float mb8[8]) {
+        const v4f a0 = marg[0], a1 = marg[1], b0 = marg[2], b1 = marg[3];
+        ma8[0] = a0.x; ma8[1] = a0.y; ma8[2] = a0.z; ma8[3] = a0.w;
+        ma8[4] = a1.x; ma8[5] = a1.y; ma8[6] = a1.z; ma8[7] = a1.w;
+        mb8[0] = b0.x; mb8[1] = b0.y; mb8[2] = b0.z; mb8[3] = b0.w;
+        mb8[4] = b1.x; mb8[5] = b1.y; mb8[6] = b1.z; mb8[7] = b1.w;
     };
 
     for (;;) {
@@ -1538,16 +1674,41 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
             for (int j = 0; j < 7; ++j) s[j] = __builtin_fmaf(t, d[j], -o[j]);
             evaluate8(T, s, l, g);
             float ls = 0.f, ss = 0.f;
+            bool within = false;  // OT: every column within its tolerance
+            if constexpr (OT) {  // gradient sum_i a_i S_ij - b_j, f change sum_i a_i l_i - sum_j b_j s_j
+                float ma8[8], mb8[8];
+                load_marg(ma8, mb8);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                a[i] += l[i];
-                ls += l[i];
-            }
+                for (int j = 0; j < 8; ++j) {
+                    float c = ma8[0] * T[j];
 #pragma unroll
-            for (int j = 0; j < 7; ++j) {
-                beta[j] += s[j];
-                o[j] += s[j];
-                ss += s[j];
+                    for (int i = 1; i < 8; ++i) c = __builtin_fmaf(ma8[i], T[8 * i + j], c);
+                    g[j] = c - mb8[j];
+                }
+                within = ot_within_tol8(g, mb8, tol, mass_slack8(ma8, mb8));
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    a[i] += l[i];
+                    ls = __builtin_fmaf(ma8[i], l[i], ls);
+                }
+#pragma unroll
+                for (int j = 0; j < 7; ++j) {
+                    beta[j] += s[j];
+                    o[j] += s[j];
+                    ss = __builtin_fmaf(mb8[j], s[j], ss);
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    a[i] += l[i];
+                    ls += l[i];
+                }
+#pragma unroll
+                for (int j = 0; j < 7; ++j) {
+                    beta[j] += s[j];
+                    o[j] += s[j];
+                    ss += s[j];
+                }
             }
             const float df = fofs + (ls - ss);
             fofs = df;
@@ -1561,9 +1722,9 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
             }
 #pragma unroll
             for (int j = 0; j < 7; ++j) slope = __builtin_fmaf(ga[j], d[j], slope);
-            const bool accept = (df <= kArmijo * t * slope) || (__builtin_fabsf(df) < kFNoise && gn2t < gn2);
+            const bool accept = (df <= kArmijo * t * slope) || (__builtin_fabsf(df) < fnoise && gn2t < gn2);
             const int evals = cnt & 0xffff;
-            const bool conv = accept && gmax <= tol;
+            const bool conv = accept && (OT ? within : gmax <= tol);
             if (!conv && evals < max_iter) {
                 if (gsum >= kReviveBits) {
                     gsum = 0.f;
@@ -1578,7 +1739,7 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
 #pragma unroll
                             for (int j = 0; j < 8; ++j)
                                 if (T[8 * i + j] == 0.f)
-                                    T[8 * i + j] = ex2(__builtin_fmaf(h[j], kLog2e, j < 7 ? beta[j] : 0.f) - a[i]);
+                                    T[8 * i + j] = ex2(__builtin_fmaf(h[j], hsc, j < 7 ? beta[j] : 0.f) - a[i]);
                         }
                     }
                 }
@@ -1610,8 +1771,15 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
 #pragma unroll
                     for (int j = 0; j < 7; ++j) beta[j] -= o[j];
                 }
-                store_output8<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, r0 + rel, T, a, beta,
-                                                       conv ? evals : BIRKHOFF4_NOT_CONVERGED);
+                if constexpr (OT) {
+                    float ma8[8], mb8[8];
+                    load_marg(ma8, mb8);
+                    store_output8_ot<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, r0 + rel, T, a, beta, ma8, eta,
+                                                              conv ? evals : BIRKHOFF4_NOT_CONVERGED);
+                } else {
+                    store_output8<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, r0 + rel, T, a, beta,
+                                                           conv ? evals : BIRKHOFF4_NOT_CONVERGED);
+                }
                 active = false;
             }
         }
@@ -1623,7 +1791,7 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
             const int rank = __popcll(wm & below);
             const int avail = nfresh - icur;
             if (!active && rank < avail) {
-                const v4f* sl = ring + order[icur + rank] * kB8Slot;
+                const v4f* sl = ring + order[icur + rank] * SLOT;
 #pragma unroll
                 for (int q = 0; q < 16; ++q) {  // v4f q holds half (q & 1) of row 4 ((q >> 1) & 1) + (q >> 2)
                     const v4f r = sl[q];
@@ -1638,6 +1806,16 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
                 rel = __float_as_int(b1.w);
                 g[0] = g0.x; g[1] = g0.y; g[2] = g0.z; g[3] = g0.w;
                 g[4] = g1.x; g[5] = g1.y; g[6] = g1.z; g[7] = g1.w;
+                if constexpr (OT) {
+                    const v4f m0 = sl[22], m1 = sl[23], m2 = sl[24], m3 = sl[25];
+                    marg[0] = m0;
+                    marg[1] = m1;
+                    marg[2] = m2;
+                    marg[3] = m3;
+                    const float mass = ((m0.x + m0.y) + (m0.z + m0.w)) + ((m1.x + m1.y) + (m1.z + m1.w));
+                    fnoise = kFNoise * 0.125f * mass;
+                    lmfloor = kLMFloor * 0.125f * mass;
+                }
 #pragma unroll
                 for (int j = 0; j < 7; ++j) o[j] = 0.f;
                 t = 1.f;
@@ -1658,7 +1836,13 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
         // Newton system at the new accepted point, for lanes that accepted a trial and
         // lanes that took a fresh problem alike.
         if (setup) {
-            weights8(T, W);
+            if constexpr (OT) {
+                float ma8[8], mb8[8];
+                load_marg(ma8, mb8);
+                weights8w(T, ma8, W);
+            } else {
+                weights8(T, W);
+            }
             float gmax = 0.f, s2 = 0.f;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
@@ -1668,7 +1852,7 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
 #pragma unroll
             for (int j = 0; j < 7; ++j) ga[j] = g[j];
             gn2 = s2;
-            lam = __builtin_fmaxf(kLM * gmax, kLMFloor);
+            lam = __builtin_fmaxf(kLM * gmax, lmfloor);
             setup = false;
         }
         if (__ballot(active) == 0) break;
@@ -1687,10 +1871,14 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
 // non-temporal accesses, and each lane works on its own problem from the tile.
 constexpr int kB8Stride = 17;  // v4f per problem in the LDS tile
 
-template <int DT>
+// With OT it is the backward of 8 x 8 entropic OT (eq. derivative): P is the solution T, av
+// the row marginal, dP = dL/dT (fp32) and dH = dL/dM; weights and flows carry 1/a_i, and
+// dM_ij = -T_ij (psi_ij - sum_k T_ik psi_ik / a_i) / eta.
+template <int DT, bool OT>
 __global__ __launch_bounds__(kB8Block, 2) void implicit8_bwd_kernel(const float* __restrict__ P,
                                                                      const void* __restrict__ dP,
-                                                                     float* __restrict__ dH, int64_t B) {
+                                                                     float* __restrict__ dH, int64_t B,
+                                                                     const float* __restrict__ av, float eta) {
     __shared__ v4f tile_all[kB8Waves][64 * kB8Stride];
     const int lane = threadIdx.x & 63;
     const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
@@ -1758,8 +1946,17 @@ __global__ __launch_bounds__(kB8Block, 2) void implicit8_bwd_kernel(const float*
                 G[4] = r1.x; G[5] = r1.y; G[6] = r1.z; G[7] = r1.w;
             }
         };
-        float W[28], F[28], w[8], ip[7];
-        weights8(T, W);
+        float W[28], F[28], w[8], ip[7], ia[8];
+        if constexpr (OT) {
+            const v4f* a4 = reinterpret_cast<const v4f*>(av) + 2 * (base + lane);
+            const v4f A0 = lane < n ? a4[0] : v4f{1.f, 1.f, 1.f, 1.f};
+            const v4f A1 = lane < n ? a4[1] : v4f{1.f, 1.f, 1.f, 1.f};
+            ia[0] = rcp(A0.x); ia[1] = rcp(A0.y); ia[2] = rcp(A0.z); ia[3] = rcp(A0.w);
+            ia[4] = rcp(A1.x); ia[5] = rcp(A1.y); ia[6] = rcp(A1.z); ia[7] = rcp(A1.w);
+            weights8w(T, ia, W);
+        } else {
+            weights8(T, W);
+        }
 #pragma unroll
         for (int k = 0; k < 28; ++k) F[k] = 0.f;
 #pragma unroll
@@ -1769,8 +1966,10 @@ __global__ __launch_bounds__(kB8Block, 2) void implicit8_bwd_kernel(const float*
 #pragma unroll
             for (int j = 0; j < 8; ++j)
 #pragma unroll
-                for (int k = j + 1; k < 8; ++k)
-                    F[pw8(j, k)] = __builtin_fmaf(T[8 * i + j] * T[8 * i + k], G[j] - G[k], F[pw8(j, k)]);
+                for (int k = j + 1; k < 8; ++k) {
+                    const float q = OT ? T[8 * i + j] * (T[8 * i + k] * ia[i]) : T[8 * i + j] * T[8 * i + k];
+                    F[pw8(j, k)] = __builtin_fmaf(q, G[j] - G[k], F[pw8(j, k)]);
+                }
         }
 #pragma unroll
         for (int p = 0; p < 7; ++p) {
@@ -1809,8 +2008,15 @@ __global__ __launch_bounds__(kB8Block, 2) void implicit8_bwd_kernel(const float*
                 mu = __builtin_fmaf(T[8 * i + j], psi[j], mu);
             }
             float o[8];
+            if constexpr (OT) {
+                mu *= ia[i];
+                const float nie = -1.f / eta;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) o[j] = T[8 * i + j] * (psi[j] - mu);
+                for (int j = 0; j < 8; ++j) o[j] = T[8 * i + j] * (psi[j] - mu) * nie;
+            } else {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) o[j] = T[8 * i + j] * (psi[j] - mu);
+            }
             tile[lane * kB8Stride + 2 * i] = v4f{o[0], o[1], o[2], o[3]};
             tile[lane * kB8Stride + 2 * i + 1] = v4f{o[4], o[5], o[6], o[7]};
         }
@@ -1888,6 +2094,19 @@ __device__ __forceinline__ bool ot_init(const float* M, const float* av, const f
         la[i] = m + lg2(sum);
     }
     return ok;
+}
+
+// The OT stopping test: |c_j - b_j| <= tol max(1, b_j) for every column (absolute for
+// marginals up to one, relative above: the fp32 resolution of a column sum grows with it).
+// The last column, whose potential is fixed, also absorbs |sum a - sum b|, which marginals
+// given in fp32 cannot make exactly zero.
+__device__ __forceinline__ bool ot_within_tol4(const float g[4], const float a[4], const float b[4], float tol) {
+    const float slack = __builtin_fabsf(((a[0] + a[1]) + (a[2] + a[3])) - ((b[0] + b[1]) + (b[2] + b[3])));
+    float x = -1.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        x = __builtin_fmaxf(x, __builtin_fabsf(g[j]) - tol * __builtin_fmaxf(1.f, b[j]) - (j == 3 ? slack : 0.f));
+    return x <= 0.f;
 }
 
 // c_j - b_j with c = sum_i a_i S_ij
@@ -1982,9 +2201,8 @@ __global__ __launch_bounds__(kOtBlock) void ot4_fwd_kernel(const float* __restri
         bool ok = false;
         if (valid) ok = ot_init(M, av, bv, p, rsc, Si, lai, xi, ai, bi);
         ot_grad(Si, ai, bi, gi);
-        const float gmax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(gi[0]), __builtin_fabsf(gi[1])),
-                                           __builtin_fmaxf(__builtin_fabsf(gi[2]), __builtin_fabsf(gi[3])));
-        const bool done = valid && (!ok || gmax <= tol || max_iter == 0);
+        const bool within = ot_within_tol4(gi, ai, bi, tol);
+        const bool done = valid && (!ok || within || max_iter == 0);
         const bool fresh = valid && !done;
         const uint64_t fm = __ballot(fresh);
         if (fresh) {
@@ -2000,7 +2218,7 @@ __global__ __launch_bounds__(kOtBlock) void ot4_fwd_kernel(const float* __restri
         }
         if (done)
             ot_store<WRITE_DUAL, WRITE_ITERS>(T, dual, iters, p, Si, lai, xi, ai, eta,
-                                              !ok ? BIRKHOFF4_NON_FINITE : (gmax <= tol ? 0 : BIRKHOFF4_NOT_CONVERGED));
+                                              !ok ? BIRKHOFF4_NON_FINITE : (within ? 0 : BIRKHOFF4_NOT_CONVERGED));
         nfresh = __popcll(fm);
         icur = 0;
         bnext += 64;
@@ -2025,13 +2243,11 @@ __global__ __launch_bounds__(kOtBlock) void ot4_fwd_kernel(const float* __restri
             fofs = df;
             gsum += spread(s0, s1, s2);
             ++cnt;
-            const float gmax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(g[0]), __builtin_fabsf(g[1])),
-                                               __builtin_fmaxf(__builtin_fabsf(g[2]), __builtin_fabsf(g[3])));
             const float gn2t = g[0] * g[0] + g[1] * g[1] + g[2] * g[2] + g[3] * g[3];
             const float slope = ga[0] * d0 + ga[1] * d1 + ga[2] * d2;
             const bool accept = (df <= kArmijo * t * slope) || (__builtin_fabsf(df) < fnoise && gn2t < gn2);
             const int evals = cnt & 0xffff;
-            const bool conv = accept && gmax <= tol;
+            const bool conv = accept && ot_within_tol4(g, a, bb, tol);
             if (!conv && evals < max_iter) {
                 if (gsum >= kReviveBits) {
                     gsum = 0.f;
@@ -2367,9 +2583,9 @@ int dispatch_fwd_hess(const void* H, float* P, float* dual, int32_t* iters, floa
 }
 
 // n = 8: one range of problems per wave, blocks scheduled by the hardware.
-template <int DT, bool WD, bool WI>
+template <int DT, bool WD, bool WI, bool OT = false>
 int launch_fwd8(const void* H, float* P, float* dual, int32_t* iters, int64_t B, float tol, int max_iter,
-                hipStream_t stream) {
+                hipStream_t stream, const float* a = nullptr, const float* b = nullptr, float eta = 1.f) {
     // about kB8Ranges ranges in all (several per resident wave slot), at least 64 problems each
     const int64_t waves_min = (B + kMaxGrid * kB8Waves - 1) / (kMaxGrid * kB8Waves);
     int64_t per_wave = (B + kB8Ranges - 1) / kB8Ranges;
@@ -2377,8 +2593,8 @@ int launch_fwd8(const void* H, float* P, float* dual, int32_t* iters, int64_t B,
     if (per_wave < waves_min) per_wave = waves_min;
     const int64_t waves = (B + per_wave - 1) / per_wave;
     const int64_t grid = (waves + kB8Waves - 1) / kB8Waves;
-    hipLaunchKernelGGL((newton8_fwd_kernel<DT, WD, WI>), dim3(static_cast<unsigned>(grid)), dim3(kB8Block), 0,
-                       stream, H, P, dual, iters, B, tol, max_iter, per_wave);
+    hipLaunchKernelGGL((newton8_fwd_kernel<DT, WD, WI, OT>), dim3(static_cast<unsigned>(grid)), dim3(kB8Block), 0,
+                       stream, H, P, dual, iters, B, tol, max_iter, per_wave, a, b, eta);
     return launch_status();
 }
 
@@ -2389,6 +2605,15 @@ int dispatch_fwd8(const void* H, float* P, float* dual, int32_t* iters, int64_t 
     if (dual) return launch_fwd8<DT, true, false>(H, P, dual, iters, B, tol, max_iter, stream);
     if (iters) return launch_fwd8<DT, false, true>(H, P, dual, iters, B, tol, max_iter, stream);
     return launch_fwd8<DT, false, false>(H, P, dual, iters, B, tol, max_iter, stream);
+}
+
+int dispatch_ot8_fwd(const float* M, const float* a, const float* b, float eta, float* T, float* dual,
+                     int32_t* iters, int64_t B, float tol, int max_iter, hipStream_t stream) {
+    constexpr int F = BIRKHOFF4_F32;
+    if (dual && iters) return launch_fwd8<F, true, true, true>(M, T, dual, iters, B, tol, max_iter, stream, a, b, eta);
+    if (dual) return launch_fwd8<F, true, false, true>(M, T, dual, iters, B, tol, max_iter, stream, a, b, eta);
+    if (iters) return launch_fwd8<F, false, true, true>(M, T, dual, iters, B, tol, max_iter, stream, a, b, eta);
+    return launch_fwd8<F, false, false, true>(M, T, dual, iters, B, tol, max_iter, stream, a, b, eta);
 }
 
 // General OT: one range of problems per wave (as for n = 8).
@@ -2522,6 +2747,46 @@ int birkhoff4_ot_bwd(const float* T, const float* a, const float* dT, float eta,
     return launch_status();
 }
 
+int birkhoff8_ot_fwd(const float* M, const float* a, const float* b, float eta, float* T, float* dual,
+                     int32_t* iters, int64_t B, float tol, int max_iter, hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 256)) return BIRKHOFF4_ERR_SIZE;
+    if (!(eta > 0.f) || !(eta <= 3.0e38f)) return BIRKHOFF4_ERR_ETA;
+    if (!(tol >= 0.f)) return BIRKHOFF4_ERR_TOL;
+    if (max_iter < 0 || max_iter > kMaxIterCap) return BIRKHOFF4_ERR_MAX_ITER;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!M || !a || !b || !T) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(M) || misaligned(a) || misaligned(b) || misaligned(T) || misaligned(dual) || misaligned(iters))
+        return BIRKHOFF4_ERR_ALIGN;
+    const size_t nm = static_cast<size_t>(B) * 256, nv = static_cast<size_t>(B) * 32,
+                 nd = dual ? static_cast<size_t>(B) * 64 : 0, ni = iters ? static_cast<size_t>(B) * 4 : 0;
+    const void* ins[3] = {M, a, b};
+    const size_t nins[3] = {nm, nv, nv};
+    for (int k = 0; k < 3; ++k)
+        if (overlaps(ins[k], nins[k], T, nm) || overlaps(ins[k], nins[k], dual, nd) ||
+            overlaps(ins[k], nins[k], iters, ni))
+            return BIRKHOFF4_ERR_OVERLAP;
+    if (overlaps(T, nm, dual, nd) || overlaps(T, nm, iters, ni) || overlaps(dual, nd, iters, ni))
+        return BIRKHOFF4_ERR_OVERLAP;
+    return dispatch_ot8_fwd(M, a, b, eta, T, dual, iters, B, tol, max_iter, stream);
+}
+
+int birkhoff8_ot_bwd(const float* T, const float* a, const float* dT, float eta, float* dM, int64_t B,
+                     hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 256)) return BIRKHOFF4_ERR_SIZE;
+    if (!(eta > 0.f) || !(eta <= 3.0e38f)) return BIRKHOFF4_ERR_ETA;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!T || !a || !dT || !dM) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(T) || misaligned(a) || misaligned(dT) || misaligned(dM)) return BIRKHOFF4_ERR_ALIGN;
+    const size_t nm = static_cast<size_t>(B) * 256, nv = static_cast<size_t>(B) * 32;
+    if (overlaps(dM, nm, T, nm) || overlaps(dM, nm, dT, nm) || overlaps(dM, nm, a, nv)) return BIRKHOFF4_ERR_OVERLAP;
+    const int64_t chunks = (B + 63) / 64;
+    const int64_t want = (chunks + kB8Waves - 1) / kB8Waves;
+    const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
+    hipLaunchKernelGGL((implicit8_bwd_kernel<BIRKHOFF4_F32, true>), dim3(static_cast<unsigned>(grid)),
+                       dim3(kB8Block), 0, stream, T, dT, dM, B, a, eta);
+    return launch_status();
+}
+
 int birkhoff8_fwd(const void* H, int h_dtype, float* P, float* dual, int32_t* iters, int64_t B, float tol,
                   int max_iter, hipStream_t stream) {
     if (B < 0 || B > (INT64_MAX / 256)) return BIRKHOFF4_ERR_SIZE;
@@ -2553,11 +2818,11 @@ int birkhoff8_bwd(const float* P, const void* dP, int dp_dtype, float* dH, int64
     const int64_t want = (chunks + kB8Waves - 1) / kB8Waves;
     const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
     if (dp_dtype == BIRKHOFF4_BF16)
-        hipLaunchKernelGGL(implicit8_bwd_kernel<BIRKHOFF4_BF16>, dim3(static_cast<unsigned>(grid)),
-                           dim3(kB8Block), 0, stream, P, dP, dH, B);
+        hipLaunchKernelGGL((implicit8_bwd_kernel<BIRKHOFF4_BF16, false>), dim3(static_cast<unsigned>(grid)),
+                           dim3(kB8Block), 0, stream, P, dP, dH, B, nullptr, 1.f);
     else
-        hipLaunchKernelGGL(implicit8_bwd_kernel<BIRKHOFF4_F32>, dim3(static_cast<unsigned>(grid)),
-                           dim3(kB8Block), 0, stream, P, dP, dH, B);
+        hipLaunchKernelGGL((implicit8_bwd_kernel<BIRKHOFF4_F32, false>), dim3(static_cast<unsigned>(grid)),
+                           dim3(kB8Block), 0, stream, P, dP, dH, B, nullptr, 1.f);
     return launch_status();
 }
 

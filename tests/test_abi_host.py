@@ -189,3 +189,22 @@ def test_saved_hessian_argument_errors():
     assert g(A, Bp, C, 7, D, 5, None) == ERR_DTYPE
     assert g(A, Bp + 8, C, 0, D, 5, None) == ERR_ALIGN
     assert g(A, Bp, C, 0, Bp + 32, 5, None) == ERR_OVERLAP  # dH over hess
+
+
+def test_ot8_argument_errors():
+    lib = b4.lib()
+    f = lib.birkhoff8_ot_fwd  # (M, a, b, eta, T, dual, iters, B, tol, max_iter, stream)
+    assert f(A, Bp, C, 1.0, D, None, None, 0, 1e-6, 20, None) == OK
+    assert f(A, Bp, C, 1.0, D, None, None, -1, 1e-6, 20, None) == ERR_SIZE
+    assert f(A, Bp, C, 0.0, D, None, None, 5, 1e-6, 20, None) == ERR_ETA
+    assert f(A, Bp, C, float("nan"), D, None, None, 5, 1e-6, 20, None) == ERR_ETA
+    assert f(A, Bp, C, 1.0, D, None, None, 5, -1.0, 20, None) == ERR_TOL
+    assert f(A, None, C, 1.0, D, None, None, 5, 1e-6, 20, None) == ERR_NULL
+    assert f(A, Bp + 4, C, 1.0, D, None, None, 5, 1e-6, 20, None) == ERR_ALIGN
+    assert f(A, Bp, C, 1.0, A + 256 * 3, None, None, 5, 1e-6, 20, None) == ERR_OVERLAP  # T inside M
+    assert f(A, Bp, C, 1.0, D, Bp + 32 * 2, None, 5, 1e-6, 20, None) == ERR_OVERLAP    # dual inside a
+    g = lib.birkhoff8_ot_bwd  # (T, a, dT, eta, dM, B, stream)
+    assert g(A, Bp, C, 1.0, D, 0, None) == OK
+    assert g(A, Bp, C, -1.0, D, 5, None) == ERR_ETA
+    assert g(A, None, C, 1.0, D, 5, None) == ERR_NULL
+    assert g(A, Bp, C, 1.0, A + 256, 5, None) == ERR_OVERLAP

@@ -1,0 +1,170 @@
+"""GPU parity for general entropic OT on 8 x 8 problems: birkhoff8_ot_fwd / birkhoff8_ot_bwd
+against the size-generic fp64 OT oracle, element by element. Bars as for 4 x 4 OT: max
+|T - T_ref| <= 1e-5 max(1, max a), marginals within 1e-5, per-matrix dM error <= 1e-4
+relative to max(1, |dM_ref|_inf)."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_07574_amd as b4
+from oracle import birkhoffn as on
+from tests._gpu import say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+TOL_T = 1e-5
+TOL_MARG = 1e-5
+TOL_DM = 1e-4
+
+
+def problem(B, scale, seed, lo=0.2, hi=2.0, logu=False):
+    rng = np.random.default_rng(seed)
+    M = (scale * rng.standard_normal((B, 8, 8))).astype(np.float32)
+    if logu:
+        a = np.exp(rng.uniform(np.log(lo), np.log(hi), (B, 8))).astype(np.float32)
+        b = np.exp(rng.uniform(np.log(lo), np.log(hi), (B, 8)))
+    else:
+        a = rng.uniform(lo, hi, (B, 8)).astype(np.float32)
+        b = rng.uniform(lo, hi, (B, 8))
+    b = (b * (a.astype(np.float64).sum(1) / b.sum(1))[:, None]).astype(np.float32)
+    G = rng.standard_normal((B, 8, 8)).astype(np.float32)
+    return M, a, b, G
+
+
+def run(M, a, b, eta, G=None, tol=1e-6, max_iter=64):
+    T, dual, it = b4.ot8_fwd(to_dev(M), to_dev(a), to_dev(b), eta, tol, max_iter, want_dual=True, want_iters=True)
+    dM = b4.ot8_bwd(T, to_dev(a), to_dev(G), eta) if G is not None else None
+    torch.cuda.synchronize()
+    return (T.cpu().numpy(), dual.cpu().numpy(), it.cpu().numpy(), None if dM is None else dM.cpu().numpy())
+
+
+def check(M, a, b, eta, T, dual, G=None, dM=None, label=""):
+    a64, b64 = a.astype(np.float64), b.astype(np.float64)
+    b64 = b64 * (a64.sum(1) / b64.sum(1))[:, None]
+    Tr, _, itr = on.ot_fwd(M.astype(np.float64), a64, b64, eta)
+    assert (itr >= 0).all(), f"{label}: oracle failed"
+    scale = np.maximum(1.0, a64.max(axis=1))[:, None, None]
+    terr = (np.abs(T - Tr) / scale).max()
+    cerr = np.abs(T.astype(np.float64).sum(1) - b64).max()
+    rerr = np.abs(T.astype(np.float64).sum(2) - a64).max()
+    say(f"  [{label}] max|T-Tref|/scale={terr:.3e} col marginal={cerr:.3e} row marginal={rerr:.3e}")
+    assert terr <= TOL_T and cerr <= TOL_MARG and rerr <= TOL_MARG
+    if dual is not None:
+        T64 = T.astype(np.float64)
+        mask = T64 > 1e-4 * scale
+        kkt = eta * np.log(np.where(mask, T64, 1.0)) - (dual[:, :8, None] + dual[:, None, 8:] - M)
+        rel = np.abs(kkt) / (eta + np.abs(M).max(axis=(1, 2), keepdims=True))
+        kerr = rel[mask].max()
+        say(f"  [{label}] dual kkt rel err={kerr:.3e}")
+        assert kerr < 2e-4 and (dual[:, 15] == 0).all()
+    if G is not None:
+        ref = on.ot_bwd(Tr, a64, G.astype(np.float64), eta).reshape(-1, 64)
+        e = np.abs(dM.reshape(-1, 64) - ref).max(axis=1) / np.maximum(1.0, np.abs(ref).max(axis=1))
+        say(f"  [{label}] max dM rel err={e.max():.3e}")
+        assert e.max() <= TOL_DM
+
+
+@pytest.mark.parametrize("eta,scale", [(1.0, 1.0), (1.0, 5.0), (0.1, 2.0), (0.05, 1.0), (5.0, 20.0), (0.5, 10.0)])
+def test_parity(eta, scale):
+    say(f"test: OT8 eta={eta} cost scale={scale}")
+    M, a, b, G = problem(6000, scale, seed=int(100 * eta + scale))
+    T, dual, it, dM = run(M, a, b, eta, G)
+    say(f"  iters mean={it.mean():.2f} max={it.max()} failed={(it < 0).sum()}")
+    assert (it >= 0).all()
+    check(M, a, b, eta, T, dual, G, dM, f"eta={eta}")
+
+
+@pytest.mark.parametrize("eta,scale", [(0.1, 1.0), (0.5, 2.0), (0.1, 5.0)])
+def test_wide_marginals(eta, scale):
+    say(f"test: OT8 marginals over three decades, eta={eta} cost scale={scale}")
+    M, a, b, G = problem(6000, scale, seed=int(1000 * eta + scale), lo=1e-3, hi=1.0, logu=True)
+    T, dual, it, dM = run(M, a, b, eta, G, max_iter=256)
+    say(f"  iters mean={it.mean():.2f} max={it.max()} failed={(it < 0).sum()}")
+    assert (it >= 0).all()
+    check(M, a, b, eta, T, dual, G, dM, f"wide eta={eta}")
+
+
+def test_birkhoff_special_case():
+    say("test: OT8 with M = -H, a = b = 1, eta = 1 reproduces the 8x8 projection")
+    rng = np.random.default_rng(3)
+    H = (5 * rng.standard_normal((3000, 8, 8))).astype(np.float32)
+    G = rng.standard_normal(H.shape).astype(np.float32)
+    ones = np.ones((3000, 8), np.float32)
+    T, dual, it, dM = run(-H, ones, ones, 1.0, G)
+    P, _, _ = b4.fwd8(to_dev(H))
+    dH = b4.bwd8(P, to_dev(G))
+    torch.cuda.synchronize()
+    assert (it >= 0).all()
+    assert np.abs(T - P.cpu().numpy()).max() < 2e-5
+    assert np.abs(dM + dH.cpu().numpy()).max() / max(1.0, np.abs(dH.cpu().numpy()).max()) < 1e-4
+    check(-H, ones, ones, 1.0, T, dual, G, dM, "birkhoff")
+
+
+def test_separable_cost():
+    say("test: OT8 separable cost gives a b^T / sum(a)")
+    rng = np.random.default_rng(4)
+    B = 2000
+    M = (3 * rng.standard_normal((B, 8, 1)) + 3 * rng.standard_normal((B, 1, 8))).astype(np.float32)
+    a = rng.uniform(0.5, 3.0, (B, 8)).astype(np.float32)
+    b = rng.uniform(0.5, 3.0, (B, 8))
+    b = (b * (a.astype(np.float64).sum(1) / b.sum(1))[:, None]).astype(np.float32)
+    T, _, it, _ = run(M, a, b, 0.7)
+    expect = a[:, :, None].astype(np.float64) * b[:, None, :] / a.astype(np.float64).sum(1)[:, None, None]
+    assert (it >= 0).all()
+    assert np.abs(T - expect).max() < 1e-5
+
+
+@pytest.mark.parametrize("B", [1, 2, 31, 32, 33, 63, 64, 65, 1000, 4097])
+def test_ragged(B):
+    say(f"test: OT8 ragged B={B}")
+    M, a, b, G = problem(B, 3.0, seed=B)
+    T, dual, it, dM = run(M, a, b, 0.8, G)
+    assert (it >= 0).all()
+    check(M, a, b, 0.8, T, dual, G, dM, f"B={B}")
+
+
+def test_edge_cases():
+    say("test: OT8 edge cases (B=0, non-finite and non-positive inputs, max_iter=0)")
+    z = torch.empty(0, 8, 8, device="cuda")
+    zv = torch.empty(0, 8, device="cuda")
+    T, _, _ = b4.ot8_fwd(z, zv, zv, 1.0)
+    assert T.shape == (0, 8, 8)
+    M, a, b, _ = problem(70, 2.0, seed=7)
+    M[3, 1, 2] = np.nan
+    a[10, 5] = 0.0
+    b[20, 7] = -1.0
+    M[30, 0, 0] = np.inf
+    b[40, 2] = np.inf
+    T, dual, it, _ = run(M, a, b, 1.0)
+    bad = [3, 10, 20, 30, 40]
+    assert (it[bad] == b4.NON_FINITE).all()
+    assert np.isnan(T[bad]).all()
+    ok = np.setdiff1d(np.arange(70), bad)
+    assert (it[ok] >= 0).all()
+    check(M[ok], a[ok], b[ok], 1.0, T[ok], dual[ok], label="valid rows")
+    _, _, it0, _ = run(M[ok], a[ok], b[ok], 1.0, max_iter=0)
+    assert ((it0 == 0) | (it0 == b4.NOT_CONVERGED)).all()
+
+
+def test_autograd():
+    say("test: OT8 autograd")
+    M, a, b, G = problem(600, 2.0, seed=9)
+    Md = to_dev(M).requires_grad_(True)
+    T = b4.ot8(Md, to_dev(a), to_dev(b), 0.6)
+    (T * to_dev(G)).sum().backward()
+    torch.cuda.synchronize()
+    check(M, a, b, 0.6, T.detach().cpu().numpy(), None, G, Md.grad.cpu().numpy(), "autograd")
+
+
+def test_large_batch_sampled():
+    B = 1 << 20
+    say(f"test: OT8 B={B}, sampled parity")
+    M, a, b, G = problem(B, 2.0, seed=14)
+    T, dual, it, dM = run(M, a, b, 0.5, G)
+    assert (it >= 0).all()
+    T64 = T.astype(np.float64)
+    marg = np.maximum(np.abs(T64.sum(2) - a).max(1), np.abs(T64.sum(1) - b).max(1))
+    say(f"  iters mean={it.mean():.2f} max={it.max()}; max marginal over all {B}: {marg.max():.3e}")
+    assert marg.max() <= 2 * TOL_MARG
+    idx = np.unique(np.concatenate([np.random.default_rng(15).choice(B, 3000, replace=False), np.argsort(marg)[-100:]]))
+    check(M[idx], a[idx], b[idx], 0.5, T[idx], dual[idx], G[idx], dM[idx], "sampled")
