@@ -89,6 +89,7 @@ def main() -> int:
     ap.add_argument("--no-n8", action="store_true", help="skip the 8x8 measurement")
     ap.add_argument("--n8-only", action="store_true", help="time only the 8x8 path (for profiler runs)")
     ap.add_argument("--no-ot", action="store_true", help="skip the general-OT measurement")
+    ap.add_argument("--ot8-only", action="store_true", help="time only the 8x8 general-OT path (for profiler runs)")
     ap.add_argument("--ot-only", action="store_true", help="time only the general-OT path (for profiler runs)")
     ap.add_argument("--no-extras", action="store_true",
                     help="time only the path (for profiler runs)")
@@ -127,6 +128,9 @@ def main() -> int:
         return 0
     if args.ot_only:
         print(json.dumps({"ot": bench_ot(args, dev, torch.cuda.current_stream(dev))}), flush=True)
+        return 0
+    if args.ot8_only:
+        print(json.dumps({"ot8": bench_ot(args, dev, torch.cuda.current_stream(dev), n=8)}), flush=True)
         return 0
     w = workloads.WORKLOADS[args.workload]
     B = w.B
@@ -331,6 +335,7 @@ def main() -> int:
         out["n8"] = bench_n8(args, dev, stream)
     if not args.no_ot:
         out["ot"] = bench_ot(args, dev, stream)
+        out["ot8"] = bench_ot(args, dev, stream, n=8)
 
     print(json.dumps(out), flush=True)
     return 0
@@ -425,27 +430,32 @@ OT_DESC = ("B=2^22 4x4 entropic OT problems, fp32: cost M = 2 N(0,1), marginals 
            "to sum(a), eta = 0.5; dT ~ N(0,1); fwd + bwd")
 
 
-def bench_ot(args, dev, stream) -> dict:
-    """fwd + bwd of 4x4 entropic OT with general marginals (reported beside the 4x4 path)."""
+def bench_ot(args, dev, stream, n: int = 4) -> dict:
+    """fwd + bwd of n x n entropic OT with general marginals (n = 4 or 8; reported beside the
+    4x4 path)."""
     import torch
 
     import paper_2606_07574_amd as b4
     import workloads
     B = OT_B
-    M, a, b, G = workloads.ot_device(B, 4, dev)
-    T = torch.empty(B, 4, 4, device=dev)
-    dual = torch.empty(B, 8, device=dev)
-    dM = torch.empty(B, 4, 4, device=dev)
+    name = "ot_b2e22" if n == 4 else "ot8_b2e22"
+    kf, kb = ("ot4_fwd", "ot4_bwd") if n == 4 else ("ot8_fwd", "ot8_bwd")
+    M, a, b, G = workloads.ot_device(B, 4 if n == 4 else 48, dev, n)
+    T = torch.empty(B, n, n, device=dev)
+    dual = torch.empty(B, 2 * n, device=dev)
+    dM = torch.empty(B, n, n, device=dev)
     lib = b4.lib()
+    fwd_fn = lib.birkhoff4_ot_fwd if n == 4 else lib.birkhoff8_ot_fwd
+    bwd_fn = lib.birkhoff4_ot_bwd if n == 4 else lib.birkhoff8_ot_bwd
     sptr = stream.cuda_stream
 
     def step():
-        rc = lib.birkhoff4_ot_fwd(M.data_ptr(), a.data_ptr(), b.data_ptr(), OT_ETA, T.data_ptr(), dual.data_ptr(),
-                                  None, B, args.tol, args.max_iter, sptr)
+        rc = fwd_fn(M.data_ptr(), a.data_ptr(), b.data_ptr(), OT_ETA, T.data_ptr(), dual.data_ptr(),
+                    None, B, args.tol, args.max_iter, sptr)
         if rc:
             raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
         e_mid.record(stream)
-        rc = lib.birkhoff4_ot_bwd(T.data_ptr(), a.data_ptr(), G.data_ptr(), OT_ETA, dM.data_ptr(), B, sptr)
+        rc = bwd_fn(T.data_ptr(), a.data_ptr(), G.data_ptr(), OT_ETA, dM.data_ptr(), B, sptr)
         if rc:
             raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
 
@@ -463,25 +473,27 @@ def bench_ot(args, dev, stream) -> dict:
         b_ms += e_mid.elapsed_time(e1)
     f_ms /= K
     b_ms /= K
-    fwd_bytes = B * (64 + 16 + 16 + 64 + 32)
-    bwd_bytes = B * (64 + 16 + 64 + 64)
-    res = {"workload": "ot_b2e22", "B": B, "eta": OT_ETA, "desc": OT_DESC, "steps": K,
+    nn, nv = 4 * n * n, 4 * n  # bytes of a matrix and of a marginal
+    fwd_bytes = B * (nn + 2 * nv + nn + 2 * nv)
+    bwd_bytes = B * (nn + nv + nn + nn)
+    res = {"workload": name, "B": B, "n": n, "eta": OT_ETA, "desc": OT_DESC.replace("4x4", f"{n}x{n}"), "steps": K,
            "value": round(B / ((f_ms + b_ms) * 1e-3), 1), "unit": "problems/s",
            "fwd_ms": round(f_ms, 4), "bwd_ms": round(b_ms, 4),
-           "kernels": {"ot4_fwd": {"alg_bytes_per_launch": fwd_bytes,
-                                   "achieved_GBs": round(fwd_bytes / (f_ms * 1e-3) / 1e9, 1)},
-                       "ot4_bwd": {"alg_bytes_per_launch": bwd_bytes,
-                                   "achieved_GBs": round(bwd_bytes / (b_ms * 1e-3) / 1e9, 1)}},
+           "kernels": {kf: {"alg_bytes_per_launch": fwd_bytes,
+                            "achieved_GBs": round(fwd_bytes / (f_ms * 1e-3) / 1e9, 1)},
+                       kb: {"alg_bytes_per_launch": bwd_bytes,
+                            "achieved_GBs": round(bwd_bytes / (b_ms * 1e-3) / 1e9, 1)}},
            "path_hbm_frac": round((fwd_bytes + bwd_bytes) / ((f_ms + b_ms) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
-    valu = valu_from_profiles("ot_b2e22", "ot4_fwd", "kernel_trace")
+    valu = valu_from_profiles(name, kf, "kernel_trace")
     ach = valu / (f_ms * 1e-3) / 1e12 if valu else None
-    res["roofline"] = {"bound": "alu", "kernel": "ot4_fwd",
+    res["roofline"] = {"bound": "alu", "kernel": kf,
                        "achieved": round(ach, 2) if ach else None, "peak": VALU_PEAK_T,
                        "unit": "T lane-instr/s", "frac": round(ach / VALU_PEAK_T, 4) if ach else None,
                        "counted_lane_instr_per_launch": valu}
-    if args.ot_only:
+    if args.ot_only or args.ot8_only:
         return res
-    _, _, it = b4.ot_fwd(M, a, b, OT_ETA, args.tol, args.max_iter, want_dual=False, want_iters=True)
+    _, _, it = (b4.ot_fwd if n == 4 else b4.ot8_fwd)(M, a, b, OT_ETA, args.tol, args.max_iter, want_dual=False,
+                                                       want_iters=True)
     torch.cuda.synchronize()
     itn = it.cpu().numpy()
     conv = itn[itn >= 0]
@@ -492,22 +504,22 @@ def bench_ot(args, dev, stream) -> dict:
     res["max_marginal_err"] = float(torch.maximum((T64.sum(-1) - a.double()).abs().amax(),
                                                   (T64.sum(-2) - b.double()).abs().amax()).item())
     del T64
-    log(f"ot: {res['value']:.4g} problems/s fwd {f_ms:.3f} ms bwd {b_ms:.3f} ms; steps {res['newton_steps']}; "
+    log(f"{name}: {res['value']:.4g} problems/s fwd {f_ms:.3f} ms bwd {b_ms:.3f} ms; steps {res['newton_steps']}; "
         f"max marginal {res['max_marginal_err']:.3e}")
     if not args.no_cpu_baseline:
         from oracle import birkhoffn
-        n = 1 << 20
-        Ms, As, Bs, Gs = (x[:n].double().cpu().numpy() for x in (M, a, b, G))
+        ns = 1 << 20 if n == 4 else 1 << 18
+        Ms, As, Bs, Gs = (x[:ns].double().cpu().numpy() for x in (M, a, b, G))
         Bs = Bs * (As.sum(1) / Bs.sum(1))[:, None]
         threads = max(1, min(16, os.cpu_count() or 1))
         t0 = time.perf_counter()
         Tr, _, _ = birkhoffn.ot_fwd(Ms, As, Bs, OT_ETA, threads=threads)
         birkhoffn.ot_bwd(Tr, As, Gs, OT_ETA, threads=threads)
         dt = time.perf_counter() - t0
-        res["cpu_baseline"] = {"value": round(n / dt, 1), "unit": "problems/s", "cores": threads, "kind": "oracle",
-                               "sample": f"first {n} problems of ot_b2e22; fp64 OT oracle forward (tol "
+        res["cpu_baseline"] = {"value": round(ns / dt, 1), "unit": "problems/s", "cores": threads, "kind": "oracle",
+                               "sample": f"first {ns} problems of {name}; fp64 OT oracle forward (tol "
                                          f"{birkhoffn.DEFAULT_TOL:g}) + backward, {threads} threads, {dt:.1f} s"}
-        log(f"ot cpu baseline: {res['cpu_baseline']}")
+        log(f"{name} cpu baseline: {res['cpu_baseline']}")
     return res
 
 

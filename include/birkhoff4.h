@@ -190,11 +190,11 @@ int birkhoff8_bwd(const float* P, const void* dP, int dp_dtype, float* dH, int64
  *       sums differ there is no solution and the status is BIRKHOFF4_NOT_CONVERGED).
  * eta   regulariser > 0 (BIRKHOFF4_ERR_ETA otherwise).
  * T     [B][4][4] fp32 output: rows sum to a exactly up to rounding, columns to b
- *       within tol: |c_j - b_j| <= tol max(1, b_j) for every column (absolute for
- *       marginals up to one, relative above, where the fp32 resolution of a column sum
- *       grows with it; for a = b = 1 this is the Birkhoff test); the last column, whose
- *       potential is fixed, may in addition differ by |sum a - sum b| as computed in fp32,
- *       since marginals given in fp32 rarely have exactly equal sums.
+ *       within tol: |c_j - b_j| <= tol max(1, sum(a) / n, b_j) for every column (n = 4
+ *       here): absolute for unit-sized marginals, relative above, where the fp32 resolution
+ *       of the column sums grows with the masses; for a = b = 1 this is the Birkhoff test.
+ *       The last column, whose potential is fixed, may in addition differ by
+ *       |sum a - sum b| as computed in fp32, since fp32 marginals rarely have equal sums.
  * dual  NULL or [B][8] fp32 output: (alpha_1..4, beta_1..3, beta_4 = 0) in the units of
  *       M, with T_ij = exp((alpha_i + beta_j - M_ij) / eta) (eq. dual).
  * iters NULL or int32 [B]: trial steps taken, BIRKHOFF4_NOT_CONVERGED, or

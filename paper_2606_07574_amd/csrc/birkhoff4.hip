@@ -1408,22 +1408,21 @@ __device__ __forceinline__ float psum(float x) {
     return x + __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, true));
 }
 
-// The OT stopping test: |c_j - b_j| <= tol max(1, b_j) for every column (absolute for
-// marginals up to one, relative above: the fp32 resolution of a column sum grows with it).
-// The last column, whose potential is fixed, also absorbs `slack` = |sum a - sum b|, which
-// marginals given in fp32 cannot make exactly zero.
-__device__ __forceinline__ bool ot_within_tol8(const float g[8], const float b[8], float tol, float slack) {
+// The OT stopping test: |c_j - b_j| <= tol max(1, sum a / 8, b_j) for every column: absolute
+// for unit-sized marginals (the Birkhoff test), relative above, where the fp32 resolution of
+// the column sums grows with the masses. The last column, whose potential is fixed, also
+// absorbs |sum a - sum b|, which marginals given in fp32 cannot make exactly zero.
+__device__ __forceinline__ bool ot_within_tol8(const float g[8], const float b[8], float tol, float sa, float sb) {
+    const float slack = __builtin_fabsf(sa - sb), ms = __builtin_fmaxf(1.f, 0.125f * sa);
     float x = -1.f;
 #pragma unroll
     for (int j = 0; j < 8; ++j)
-        x = __builtin_fmaxf(x, __builtin_fabsf(g[j]) - tol * __builtin_fmaxf(1.f, b[j]) - (j == 7 ? slack : 0.f));
+        x = __builtin_fmaxf(x, __builtin_fabsf(g[j]) - tol * __builtin_fmaxf(ms, b[j]) - (j == 7 ? slack : 0.f));
     return x <= 0.f;
 }
 
-// |sum a - sum b| in fp32 (for the stopping test)
-__device__ __forceinline__ float mass_slack8(const float a[8], const float b[8]) {
-    return __builtin_fabsf((((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]))) -
-                           (((b[0] + b[1]) + (b[2] + b[3])) + ((b[4] + b[5]) + (b[6] + b[7]))));
+__device__ __forceinline__ float sum8v(const float v[8]) {
+    return ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
 }
 
 // Output of one 8 x 8 OT problem: T = diag(a) S, dual alpha_i = eta (ln a_i - lse_i), beta_j =
@@ -1620,7 +1619,7 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
         if constexpr (OT) {
             const float sa = psum((ma[0] + ma[1]) + (ma[2] + ma[3]));
             const float sb = ((mb[0] + mb[1]) + (mb[2] + mb[3])) + ((mb[4] + mb[5]) + (mb[6] + mb[7]));
-            conv = ot_within_tol8(gi, mb, tol, __builtin_fabsf(sa - sb));
+            conv = ot_within_tol8(gi, mb, tol, sa, sb);
         }
         const bool done = valid && (!fin || conv || max_iter == 0);
         const bool fresh = valid && !done;
@@ -1685,7 +1684,7 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
                     for (int i = 1; i < 8; ++i) c = __builtin_fmaf(ma8[i], T[8 * i + j], c);
                     g[j] = c - mb8[j];
                 }
-                within = ot_within_tol8(g, mb8, tol, mass_slack8(ma8, mb8));
+                within = ot_within_tol8(g, mb8, tol, sum8v(ma8), sum8v(mb8));
 #pragma unroll
                 for (int i = 0; i < 8; ++i) {
                     a[i] += l[i];
@@ -2096,16 +2095,17 @@ __device__ __forceinline__ bool ot_init(const float* M, const float* av, const f
     return ok;
 }
 
-// The OT stopping test: |c_j - b_j| <= tol max(1, b_j) for every column (absolute for
-// marginals up to one, relative above: the fp32 resolution of a column sum grows with it).
-// The last column, whose potential is fixed, also absorbs |sum a - sum b|, which marginals
-// given in fp32 cannot make exactly zero.
+// The OT stopping test: |c_j - b_j| <= tol max(1, sum a / 4, b_j) for every column: absolute
+// for unit-sized marginals (the Birkhoff test), relative above, where the fp32 resolution of
+// the column sums grows with the masses. The last column, whose potential is fixed, also
+// absorbs |sum a - sum b|, which marginals given in fp32 cannot make exactly zero.
 __device__ __forceinline__ bool ot_within_tol4(const float g[4], const float a[4], const float b[4], float tol) {
-    const float slack = __builtin_fabsf(((a[0] + a[1]) + (a[2] + a[3])) - ((b[0] + b[1]) + (b[2] + b[3])));
+    const float sa = (a[0] + a[1]) + (a[2] + a[3]);
+    const float slack = __builtin_fabsf(sa - ((b[0] + b[1]) + (b[2] + b[3]))), ms = __builtin_fmaxf(1.f, 0.25f * sa);
     float x = -1.f;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-        x = __builtin_fmaxf(x, __builtin_fabsf(g[j]) - tol * __builtin_fmaxf(1.f, b[j]) - (j == 3 ? slack : 0.f));
+        x = __builtin_fmaxf(x, __builtin_fabsf(g[j]) - tol * __builtin_fmaxf(ms, b[j]) - (j == 3 ? slack : 0.f));
     return x <= 0.f;
 }
 

@@ -8,6 +8,7 @@ import torch
 
 import paper_2606_07574_amd as b4
 from oracle import birkhoffn as on
+import workloads
 from tests._gpu import say, to_dev
 
 pytestmark = pytest.mark.gpu
@@ -168,3 +169,31 @@ def test_large_batch_sampled():
     assert marg.max() <= 2 * TOL_MARG
     idx = np.unique(np.concatenate([np.random.default_rng(15).choice(B, 3000, replace=False), np.argsort(marg)[-100:]]))
     check(M[idx], a[idx], b[idx], 0.5, T[idx], dual[idx], G[idx], dM[idx], "sampled")
+
+
+def test_fullsize_bench_workload():
+    # the benchmark's 8x8 OT workload and launch (dual written, no step counts); a second launch
+    # with step counts must give the same bits
+    B = 1 << 22
+    say(f"test: OT8 full-size workload B={B}, benchmark launch")
+    M, a, b, G = workloads.ot_device(B, 48, "cuda", 8)
+    T, dual, _ = b4.ot8_fwd(M, a, b, 0.5, 1e-6, 64, want_dual=True)
+    dM = b4.ot8_bwd(T, a, G, 0.5)
+    T2, dual2, it = b4.ot8_fwd(M, a, b, 0.5, 1e-6, 64, want_dual=True, want_iters=True)
+    torch.cuda.synchronize()
+    assert torch.equal(T, T2) and torch.equal(dual, dual2)
+    itn = it.cpu().numpy()
+    T64 = T.double()
+    marg = torch.maximum((T64.sum(-1) - a.double()).abs().amax(-1),
+                         (T64.sum(-2) - b.double()).abs().amax(-1)).cpu().numpy()
+    del T64, T2, dual2
+    say(f"  iters mean={itn.mean():.2f} max={itn.max()} not converged={(itn < 0).sum()}; "
+        f"max marginal over all {B}: {marg.max():.3e}")
+    assert (itn >= 0).all()
+    assert marg.max() <= TOL_MARG
+    rng = np.random.default_rng(18)
+    idx = np.unique(np.concatenate([rng.choice(B, 2000, replace=False), np.argsort(marg)[-100:],
+                                    np.argsort(itn)[-100:], np.arange(64), np.arange(B - 64, B)]))
+    it_ = torch.from_numpy(idx).cuda()
+    check(M[it_].cpu().numpy(), a[it_].cpu().numpy(), b[it_].cpu().numpy(), 0.5, T[it_].cpu().numpy(),
+          dual[it_].cpu().numpy(), G[it_].cpu().numpy(), dM[it_].cpu().numpy(), "full-size sample")

@@ -218,16 +218,16 @@ def n8_mix_device(B: int, seed: int, dev):
     return H.to(torch.bfloat16).contiguous(), G.to(torch.bfloat16).contiguous()
 
 
-def ot_device(B: int, seed: int, dev):
-    """4x4 entropic-OT problems: cost M = 2 N(0,1), marginals a, b ~ U(0.2, 2) with b
+def ot_device(B: int, seed: int, dev, n: int = 4):
+    """n x n entropic-OT problems: cost M = 2 N(0,1), marginals a, b ~ U(0.2, 2) with b
     rescaled (in fp64) to the sum of a, upstream gradient dT ~ N(0,1); fp32. Returns
     (M, a, b, dT) on ``dev``."""
     import torch
     g = torch.Generator(device=dev)
     g.manual_seed(seed)
-    M = 2.0 * torch.randn(B, 4, 4, device=dev, generator=g)
-    a = 0.2 + 1.8 * torch.rand(B, 4, device=dev, generator=g)
-    b = 0.2 + 1.8 * torch.rand(B, 4, device=dev, generator=g)
+    M = 2.0 * torch.randn(B, n, n, device=dev, generator=g)
+    a = 0.2 + 1.8 * torch.rand(B, n, device=dev, generator=g)
+    b = 0.2 + 1.8 * torch.rand(B, n, device=dev, generator=g)
     b = (b.double() * (a.double().sum(1) / b.double().sum(1))[:, None]).float()
-    G = torch.randn(B, 4, 4, device=dev, generator=g)
+    G = torch.randn(B, n, n, device=dev, generator=g)
     return M.contiguous(), a.contiguous(), b.contiguous(), G.contiguous()
