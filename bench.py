@@ -91,6 +91,8 @@ def main() -> int:
     ap.add_argument("--no-ot", action="store_true", help="skip the general-OT measurement")
     ap.add_argument("--ot8-only", action="store_true", help="time only the 8x8 general-OT path (for profiler runs)")
     ap.add_argument("--ot-only", action="store_true", help="time only the general-OT path (for profiler runs)")
+    ap.add_argument("--no-small", action="store_true", help="skip the small-batch launch timing")
+    ap.add_argument("--small-only", action="store_true", help="time only the small-batch cases")
     ap.add_argument("--no-extras", action="store_true",
                     help="time only the path (for profiler runs)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -128,6 +130,9 @@ def main() -> int:
         return 0
     if args.ot_only:
         print(json.dumps({"ot": bench_ot(args, dev, torch.cuda.current_stream(dev))}), flush=True)
+        return 0
+    if args.small_only:
+        print(json.dumps({"small_batch": bench_small_batch(dev)}), flush=True)
         return 0
     if args.ot8_only:
         print(json.dumps({"ot8": bench_ot(args, dev, torch.cuda.current_stream(dev), n=8)}), flush=True)
@@ -336,9 +341,73 @@ def main() -> int:
     if not args.no_ot:
         out["ot"] = bench_ot(args, dev, stream)
         out["ot8"] = bench_ot(args, dev, stream, n=8)
+    if not args.no_small:
+        out["small_batch"] = bench_small_batch(dev)
 
     print(json.dumps(out), flush=True)
     return 0
+
+
+def bench_small_batch(dev, sizes=(512, 4096, 32768), pairs=32, reps=20) -> list:
+    """Small batches are launch-bound: per fwd + bwd pair (N(0,1) logits, fp32, default
+    variant), the wall time of back-to-back eager calls, the same pairs replayed from a HIP
+    graph that holds `pairs` of them, and the two kernels' event-timed durations."""
+    import torch
+
+    import paper_2606_07574_amd as b4
+    import workloads
+    res = []
+    for B in sizes:
+        H32, dP32 = workloads.gauss(B, 1.0, seed=B)
+        H = torch.from_numpy(H32).to(dev)
+        dP = torch.from_numpy(dP32).to(dev)
+        P = torch.empty_like(H)
+        dH = torch.empty_like(H)
+
+        def pair():
+            b4.fwd(H, out=P, want_dual=False)
+            b4.bwd(P, dP, out=dH)
+        for _ in range(20):
+            pair()
+        torch.cuda.synchronize()
+        n = pairs * reps
+        t0 = time.perf_counter()
+        for _ in range(n):
+            pair()
+        torch.cuda.synchronize()
+        eager_us = (time.perf_counter() - t0) / n * 1e6
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(pairs):
+                pair()
+        for _ in range(2):
+            g.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            g.replay()
+        torch.cuda.synchronize()
+        graph_us = (time.perf_counter() - t0) / n * 1e6
+        stream = torch.cuda.current_stream(dev)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        f_ms = b_ms = 0.0
+        for _ in range(reps):
+            ev[0].record(stream)
+            b4.fwd(H, out=P, want_dual=False)
+            ev[1].record(stream)
+            b4.bwd(P, dP, out=dH)
+            ev[2].record(stream)
+            torch.cuda.synchronize()
+            f_ms += ev[0].elapsed_time(ev[1])
+            b_ms += ev[1].elapsed_time(ev[2])
+        row = {"B": B, "eager_us_per_pair": round(eager_us, 2), "graph_us_per_pair": round(graph_us, 2),
+               "pairs_per_graph": pairs, "fwd_event_us": round(f_ms / reps * 1e3, 2),
+               "bwd_event_us": round(b_ms / reps * 1e3, 2),
+               "graph_proj_per_s": round(B / (graph_us * 1e-6), 1)}
+        log(f"small batch: {row}")
+        res.append(row)
+        del g, H, dP, P, dH
+    return res
 
 
 def bench_saved_hessian(args, lib, sets, n_sets, B, hcode, bf16, stream, inb, default_ms):
