@@ -309,6 +309,10 @@ def main() -> int:
             sk_marg = None
         out["buckets"] = bucket_report(w, ch, itn, marg.cpu().numpy(), sk_marg)
         del P, P64
+        if w.grad:
+            out["autograd_step"] = bench_autograd_step(args, lib, sets, n_sets, B, hcode, bf16, stream,
+                                                       in_bytes(bf16))
+            log(f"autograd step (no dual): {out['autograd_step']}")
         if w.grad and not args.no_hess:
             out["saved_hessian"] = bench_saved_hessian(args, lib, sets, n_sets, B, hcode, bf16, stream,
                                                        in_bytes(bf16), ms_per_step)
@@ -408,6 +412,51 @@ def bench_small_batch(dev, sizes=(512, 4096, 32768), pairs=32, reps=20) -> list:
         res.append(row)
         del g, H, dP, P, dH
     return res
+
+
+def bench_autograd_step(args, lib, sets, n_sets, B, hcode, bf16, stream, inb) -> dict:
+    """The step that autograd runs (project(): the forward without the dual, which the backward
+    does not read, then the backward) on the benchmark's buffers, timed like the headline."""
+    import torch
+
+    import paper_2606_07574_amd as b4
+    sptr = stream.cuda_stream
+    gcode = hcode if bf16 else b4.F32
+    K = args.steps
+    e0 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    e1 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    e2 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+
+    def step(k, ev):
+        st = sets[k % n_sets]
+        if ev:
+            e0[k].record(stream)
+        rc = lib.birkhoff4_fwd_ex(st["H"].data_ptr(), hcode, st["P"].data_ptr(), None, None, B, args.tol,
+                                  args.max_iter, sptr)
+        if rc:
+            raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+        if ev:
+            e1[k].record(stream)
+        rc = lib.birkhoff4_bwd_ex(st["P"].data_ptr(), st["G"].data_ptr(), gcode, st["dH"].data_ptr(), B, sptr)
+        if rc:
+            raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+        if ev:
+            e2[k].record(stream)
+    for k in range(args.warmup):
+        step(k, False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        step(k, True)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / K
+    f_ms = float(np.mean([e0[k].elapsed_time(e1[k]) for k in range(K)]))
+    b_ms = float(np.mean([e1[k].elapsed_time(e2[k]) for k in range(K)]))
+    fb, bb = inb + 64, 64 + inb + 64
+    return {"ms_per_step": round(wall * 1e3, 4), "value": round(B / wall, 1), "unit": "proj/s",
+            "fwd_ms": round(f_ms, 4), "bwd_ms": round(b_ms, 4), "alg_bytes_per_projection": fb + bb,
+            "fwd_GBs": round(B * fb / (f_ms * 1e-3) / 1e9, 1), "bwd_GBs": round(B * bb / (b_ms * 1e-3) / 1e9, 1),
+            "path_hbm_frac": round(B * (fb + bb) / wall / 1e9 / HBM_PEAK_GBS, 4)}
 
 
 def bench_saved_hessian(args, lib, sets, n_sets, B, hcode, bf16, stream, inb, default_ms):
