@@ -92,6 +92,8 @@ def main() -> int:
     ap.add_argument("--ot8-only", action="store_true", help="time only the 8x8 general-OT path (for profiler runs)")
     ap.add_argument("--ot-only", action="store_true", help="time only the general-OT path (for profiler runs)")
     ap.add_argument("--no-small", action="store_true", help="skip the small-batch launch timing")
+    ap.add_argument("--no-mix", action="store_true", help="skip the residual-mixing measurement")
+    ap.add_argument("--mix-only", action="store_true", help="time only the residual-mixing pair (for profiler runs)")
     ap.add_argument("--small-only", action="store_true", help="time only the small-batch cases")
     ap.add_argument("--no-extras", action="store_true",
                     help="time only the path (for profiler runs)")
@@ -130,6 +132,9 @@ def main() -> int:
         return 0
     if args.ot_only:
         print(json.dumps({"ot": bench_ot(args, dev, torch.cuda.current_stream(dev))}), flush=True)
+        return 0
+    if args.mix_only:
+        print(json.dumps({"mix_streams": bench_mix_streams(args, dev, torch.cuda.current_stream(dev))}), flush=True)
         return 0
     if args.small_only:
         print(json.dumps({"small_batch": bench_small_batch(dev)}), flush=True)
@@ -347,9 +352,96 @@ def main() -> int:
         out["ot8"] = bench_ot(args, dev, stream, n=8)
     if not args.no_small:
         out["small_batch"] = bench_small_batch(dev)
+    if not args.no_mix:
+        out["mix_streams"] = bench_mix_streams(args, dev, stream)
 
     print(json.dumps(out), flush=True)
     return 0
+
+
+def bench_mix_streams(args, dev, stream, B=1 << 15, C=4096) -> dict:
+    """Residual mixing of the mHC layer (Y = P X per token, P = proj(exp(H))) and its backward
+    on B tokens of 4 bf16 streams with C channels: per-call event times, algorithmic GB/s
+    and the oracle's rate on a sample of tokens."""
+    import torch
+
+    import paper_2606_07574_amd as b4
+    import workloads
+    H, X, G = workloads.mix_streams_device(B, C, 60, dev)
+    Y = torch.empty_like(X)
+    dX = torch.empty_like(X)
+    P = torch.empty(B, 4, 4, device=dev)
+    dH = torch.empty(B, 4, 4, device=dev)
+    lib = b4.lib()
+    sptr = stream.cuda_stream
+    K = max(5, args.steps // 2)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+
+    def step(e):
+        if e:
+            e[0].record(stream)
+        rc = lib.birkhoff4_mix_fwd(H.data_ptr(), b4.BF16, X.data_ptr(), b4.BF16, Y.data_ptr(), P.data_ptr(), None,
+                                   None, B, C, args.tol, args.max_iter, sptr)
+        if rc:
+            raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+        if e:
+            e[1].record(stream)
+        rc = lib.birkhoff4_mix_bwd(P.data_ptr(), X.data_ptr(), G.data_ptr(), b4.BF16, dX.data_ptr(), dH.data_ptr(),
+                                   B, C, sptr)
+        if rc:
+            raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+        if e:
+            e[2].record(stream)
+    for _ in range(2):
+        step(None)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        step(ev[k])
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / K
+    f_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    b_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    fb = 32 + 64 + 16 * C          # H (bf16), P, X, Y
+    bb = 64 + 24 * C + 64          # P, X, dY, dX, dH
+    res = {"workload": f"mix_streams_b2e{B.bit_length() - 1}_c{C}", "B": B, "C": C,
+           "desc": f"B={B} tokens, 4 bf16 streams of C={C} channels, X, dY ~ N(0,1); logits H from the "
+                   "headline mixture in bf16; fwd = projection + Y = P X, bwd = dX = P^T dY, dP = dY X^T, dH",
+           "steps": K, "value": round(B / wall, 1), "unit": "tokens/s", "ms_per_step": round(wall * 1e3, 4),
+           "fwd_ms": round(f_ms, 4), "bwd_ms": round(b_ms, 4),
+           "alg_bytes_per_token": {"fwd": fb, "bwd": bb},
+           "kernels": {"mix_fwd (projection + mixing)": {"achieved_GBs": round(B * fb / (f_ms * 1e-3) / 1e9, 1)},
+                       "mix_bwd": {"achieved_GBs": round(B * bb / (b_ms * 1e-3) / 1e9, 1)}},
+           "path_hbm_frac": round(B * (fb + bb) / wall / 1e9 / HBM_PEAK_GBS, 4)}
+    # context: torch's own device copy of X into Y (the forward's stream bytes, no arithmetic)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    Y.copy_(X)
+    c0.record(stream)
+    for _ in range(K):
+        Y.copy_(X)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    res["copy_reference_GBs"] = round(2 * X.numel() * 2 * K / (c0.elapsed_time(c1) * 1e-3) / 1e9, 1)
+    dom = "mix_bwd" if b_ms >= f_ms else "mix_fwd (projection + mixing)"
+    ach = res["kernels"][dom]["achieved_GBs"]
+    res["roofline"] = {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                       "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+    log(f"mix streams: {res}")
+    if not args.no_cpu_baseline:
+        from oracle.mix import mix_bwd as o_bwd, mix_fwd as o_fwd
+        import oracle
+        n = 256
+        Hs, Xs, Gs = H[:n].float().cpu().numpy(), X[:n].float().cpu().numpy(), G[:n].float().cpu().numpy()
+        threads = oracle.default_threads()
+        t0 = time.perf_counter()
+        _, Pr = o_fwd(Hs, Xs, threads=threads)
+        o_bwd(Pr, Xs, Gs, threads=threads)
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": round(n / dt, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+                               "sample": f"first {n} tokens of {res['workload']}; fp64 oracle (projection tol "
+                                         f"{oracle.DEFAULT_TOL:g}, numpy products) fwd + bwd, {dt:.2f} s"}
+    del H, X, G, Y, dX, P, dH
+    return res
 
 
 def bench_small_batch(dev, sizes=(512, 4096, 32768), pairs=32, reps=20) -> list:

@@ -49,7 +49,8 @@ enum {
     BIRKHOFF4_ERR_DEVICE = -9,    /* HIP device query failed */
     BIRKHOFF4_ERR_LAUNCH = -10,   /* kernel launch failed (hipGetLastError) */
     BIRKHOFF4_ERR_VARIANT = -11,  /* unknown forward variant */
-    BIRKHOFF4_ERR_ETA = -12       /* eta not positive and finite */
+    BIRKHOFF4_ERR_ETA = -12,      /* eta not positive and finite */
+    BIRKHOFF4_ERR_CHANNELS = -13  /* stream width C negative or not a whole number of 16-byte chunks */
 };
 
 /* Forward kernel variants (birkhoff4_fwd_ex2). Both compute the same projection to the
@@ -220,6 +221,33 @@ int birkhoff8_ot_fwd(const float* M, const float* a, const float* b, float eta, 
                      int32_t* iters, int64_t B, float tol, int max_iter, hipStream_t stream);
 int birkhoff8_ot_bwd(const float* T, const float* a, const float* dT, float eta, float* dM, int64_t B,
                      hipStream_t stream);
+
+/* Residual mixing of the mHC layer (Sec. 2.1): each token's n = 4 streams are mixed by its
+ * projected matrix, Y = P X with P = proj(exp(H)), the term H^res x_l of the layer's update.
+ *
+ * H      [B][4][4] logits, h_dtype F32 or BF16 (as in birkhoff4_fwd_ex).
+ * X      [B][4][C] streams of each token, row-major (stream i of token b starts at element
+ *        (4 b + i) C), x_dtype F32 or BF16; NULL allowed when C = 0.
+ * Y      [B][4][C] output in x_dtype: Y_i = sum_j P_ij X_j per token, accumulated in fp32;
+ *        bf16 results are rounded to nearest even.
+ * P      [B][4][4] fp32 output: the projection, exactly what birkhoff4_fwd_ex would write
+ *        for H (the default forward variant); the backward needs it.
+ * dual, iters  NULL or outputs as in birkhoff4_fwd_ex.
+ * C      channels per stream, >= 0, a multiple of 8 for BF16 streams or 4 for F32
+ *        (BIRKHOFF4_ERR_CHANNELS otherwise): every row is whole 16-byte chunks.
+ * tol, max_iter as in birkhoff4_fwd. Y must not overlap any input or P, dual or iters; P,
+ * dual and iters must not overlap X. Every check is made before anything is queued. */
+int birkhoff4_mix_fwd(const void* H, int h_dtype, const void* X, int x_dtype, void* Y, float* P, float* dual,
+                      int32_t* iters, int64_t B, int64_t C, float tol, int max_iter, hipStream_t stream);
+
+/* Backward of birkhoff4_mix_fwd: from P (its output), the streams X and dY = dL/dY
+ * ([B][4][C], both in x_dtype), writes dX = dL/dX = P^T dY per token ([B][4][C] in x_dtype,
+ * fp32 accumulation, bf16 rounded to nearest even) and dH = dL/dH ([B][4][4] fp32): the
+ * projection's backward (eq. derivative, as in birkhoff4_bwd) applied to
+ * dP_ij = sum_c dY_i[c] X_j[c]. One pass over X and dY. Outputs must not overlap each other
+ * or any input. Return codes as for birkhoff4_mix_fwd. */
+int birkhoff4_mix_bwd(const float* P, const void* X, const void* dY, int x_dtype, void* dX, float* dH, int64_t B,
+                      int64_t C, hipStream_t stream);
 
 /* Human-readable text for a return code (static storage). */
 const char* birkhoff4_strerror(int code);

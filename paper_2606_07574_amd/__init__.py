@@ -14,6 +14,8 @@ a GPU, the calls raise.
     P, dual = fwd8(H); dH = bwd8(P, dP); P = project8(H)   # the same for 8 x 8 matrices
     T, dual = ot_fwd(M, a, b, eta); dM = ot_bwd(T, a, dT, eta)  # general entropic OT, 4 x 4
     T, dual = ot8_fwd(M, a, b, eta); dM = ot8_bwd(T, a, dT, eta)  # the same for 8 x 8
+    Y, P, _, _ = mix_fwd(H, X); dX, dH = mix_bwd(P, X, dY)  # residual mixing Y = P X (Sec. 2.1)
+    Y = mix(H, X)                     # autograd-aware, gradients for H and X
 """
 from __future__ import annotations
 
@@ -64,6 +66,8 @@ def _load():
         "birkhoff8_bwd": [vp, vp, i32, vp, i64, st],
         "birkhoff8_ot_fwd": [vp, vp, vp, f32, vp, vp, vp, i64, f32, i32, st],
         "birkhoff8_ot_bwd": [vp, vp, vp, f32, vp, i64, st],
+        "birkhoff4_mix_fwd": [vp, i32, vp, i32, vp, vp, vp, vp, i64, i64, f32, i32, st],
+        "birkhoff4_mix_bwd": [vp, vp, vp, i32, vp, vp, i64, i64, st],
         "birkhoff4_version": [],
     }
     for name, args in sigs.items():
@@ -407,6 +411,78 @@ class OT8Fn(torch.autograd.Function):
 def ot8(M: torch.Tensor, a: torch.Tensor, b: torch.Tensor, eta: float = 1.0, tol: float = DEFAULT_TOL,
         max_iter: int = DEFAULT_MAX_ITER) -> torch.Tensor:
     return OT8Fn.apply(M, a, b, eta, tol, max_iter)
+
+
+def _streams(X: torch.Tensor, lead, name: str) -> int:
+    """Checks X as [..., 4, C] streams matching the leading dims; returns C."""
+    if not X.is_cuda:
+        raise Birkhoff4Error(f"{name} must be a GPU tensor (no CPU path)")
+    if X.dim() < 2 or tuple(X.shape[:-2]) != tuple(lead) or X.shape[-2] != 4:
+        raise ValueError(f"{name} must have shape {(*lead, 4, 'C')}, got {tuple(X.shape)}")
+    if not X.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return X.shape[-1]
+
+
+def mix_fwd(H: torch.Tensor, X: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER,
+            want_dual: bool = False, want_iters: bool = False):
+    """Residual mixing of the mHC layer: P = proj(exp(H)) per token and Y = P X.
+
+    H: [..., 4, 4] float32 or bfloat16 logits; X: [..., 4, C] float32 or bfloat16 streams
+    (C a multiple of 8 for bfloat16, of 4 for float32). Returns (Y like X, P float32,
+    dual or None, iters or None)."""
+    B = _batch(H, "H")
+    lead = H.shape[:-2]
+    C = _streams(X, lead, "X")
+    _same_device(H, X)
+    Y = torch.empty_like(X)
+    P = torch.empty(H.shape, dtype=torch.float32, device=H.device)
+    dual = torch.empty(*lead, 8, dtype=torch.float32, device=H.device) if want_dual else None
+    iters = torch.empty(lead, dtype=torch.int32, device=H.device) if want_iters else None
+    with torch.cuda.device(H.device):
+        _check(_load().birkhoff4_mix_fwd(_ptr(H), _dtype_code(H), _ptr(X), _dtype_code(X), _ptr(Y), _ptr(P),
+                                         _ptr(dual), _ptr(iters), B, C, float(tol), int(max_iter), _stream(H)))
+    return Y, P, dual, iters
+
+
+def mix_bwd(P: torch.Tensor, X: torch.Tensor, dY: torch.Tensor):
+    """Backward of mix_fwd: (dX = P^T dY like X, dH float32) from P, X and dY (dtype of X)."""
+    B = _batch(P, "P")
+    if P.dtype != torch.float32:
+        raise TypeError("P must be float32")
+    lead = P.shape[:-2]
+    C = _streams(X, lead, "X")
+    if _streams(dY, lead, "dY") != C or dY.dtype != X.dtype:
+        raise ValueError("dY must have the shape and dtype of X")
+    _same_device(P, X, dY)
+    dX = torch.empty_like(X)
+    dH = torch.empty(P.shape, dtype=torch.float32, device=P.device)
+    with torch.cuda.device(P.device):
+        _check(_load().birkhoff4_mix_bwd(_ptr(P), _ptr(X), _ptr(dY), _dtype_code(X), _ptr(dX), _ptr(dH), B, C,
+                                         _stream(P)))
+    return dX, dH
+
+
+class MixFn(torch.autograd.Function):
+    """Y = proj(exp(H)) X per token; the backward is one pass over X and dY (mix_bwd)."""
+
+    @staticmethod
+    def forward(ctx, H, X, tol=DEFAULT_TOL, max_iter=DEFAULT_MAX_ITER):
+        X = X.contiguous()
+        Y, P, _, _ = mix_fwd(H.contiguous(), X, tol, max_iter)
+        ctx.save_for_backward(P, X)
+        ctx.h_dtype = H.dtype
+        return Y
+
+    @staticmethod
+    def backward(ctx, dY):
+        P, X = ctx.saved_tensors
+        dX, dH = mix_bwd(P, X, dY.contiguous().to(X.dtype))
+        return dH.to(ctx.h_dtype), dX, None, None
+
+
+def mix(H: torch.Tensor, X: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER) -> torch.Tensor:
+    return MixFn.apply(H, X, tol, max_iter)
 
 
 def version() -> int:

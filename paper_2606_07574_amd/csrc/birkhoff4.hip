@@ -1007,6 +1007,275 @@ __global__ __launch_bounds__(kBwdBlock) void implicit_bwd_kernel(const float* __
 }
 
 // ---------------------------------------------------------------------------
+// Residual mixing of the mHC layer (Sec. 2.1): the streams of a token are mixed by its
+// projected matrix, x <- H^res x
+// ---------------------------------------------------------------------------
+// A token carries n = 4 streams of C channels, [B][4][C] row-major. The forward writes
+// Y_i = sum_j P_ij X_j; the backward writes dX_j = sum_i P_ij dY_i and forms
+// dP_ij = sum_c dY_i[c] X_j[c], from which dH follows as in the projection's backward. A
+// wave owns one token at a time: P is uniform over the wave (scalar loads) and the lanes
+// stream 16-byte chunks of the four rows, so that each load or store instruction covers
+// 1 KB of one row. Every stream byte is touched once: non-temporal loads and stores.
+constexpr int kMixBlock = 256;
+constexpr int kMixWaves = kMixBlock / 64;
+constexpr int kMixPerCu = 8;  // blocks per CU the grid is sized for
+
+template <int DX>
+struct MixChunk {  // channels in one 16-byte chunk of a row
+    static constexpr int E = (DX == BIRKHOFF4_BF16) ? 8 : 4;
+};
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+template <int DX>
+__device__ __forceinline__ void unpack_chunk(const v4u w, float v[MixChunk<DX>::E]) {
+    const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        if constexpr (DX == BIRKHOFF4_BF16) {
+            v[2 * k + 0] = __uint_as_float(u[k] << 16);
+            v[2 * k + 1] = __uint_as_float(u[k] & 0xffff0000u);
+        } else {
+            v[k] = __uint_as_float(u[k]);
+        }
+    }
+}
+
+// bf16 outputs are rounded to nearest even (the hardware conversion).
+template <int DX>
+__device__ __forceinline__ v4u pack_chunk(const float v[MixChunk<DX>::E]) {
+    uint32_t u[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        if constexpr (DX == BIRKHOFF4_BF16)
+            u[k] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{v[2 * k], v[2 * k + 1]}), bf16x2));
+        else
+            u[k] = __float_as_uint(v[k]);
+    }
+    return v4u{u[0], u[1], u[2], u[3]};
+}
+
+// out_i = sum_j m_ij in_j over the E channels of one chunk of each of the four rows.
+template <int DX>
+__device__ __forceinline__ void mix_chunk(const float m[16], const v4u in[4], v4u out[4]) {
+    constexpr int E = MixChunk<DX>::E;
+    float x[4][E];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) unpack_chunk<DX>(in[j], x[j]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        float y[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            y[e] = __builtin_fmaf(m[4 * i + 3], x[3][e],
+                   __builtin_fmaf(m[4 * i + 2], x[2][e], __builtin_fmaf(m[4 * i + 1], x[1][e], m[4 * i] * x[0][e])));
+        out[i] = pack_chunk<DX>(y);
+    }
+}
+
+// P of token t, uniform over the wave.
+__device__ __forceinline__ void load_token_matrix(const float* __restrict__ P, int64_t t, float p[16]) {
+    const float* pt = P + 16 * t;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) p[q] = pt[q];
+}
+
+// A wave walks the items (t, c0) of its tokens, c0 = 0, 64, 128, ... < nc: lane l handles
+// chunk c0 + l of each of the four rows. The next item's loads are issued before the
+// current item is mixed and stored (loads and stores retire in order, so a wait for loads
+// issued after a store would also wait for that store), into the other of two buffers so
+// that no register copy waits for them. Lanes past the end of a row take its last chunk:
+// they load, mix and store the same bytes as that chunk's own lane, so every memory
+// instruction is issued by the whole wave and the waits count exactly.
+template <int DX>
+__global__ __launch_bounds__(kMixBlock) void mix_fwd_kernel(const float* __restrict__ P,
+                                                             const v4u* __restrict__ X, v4u* __restrict__ Y,
+                                                             int64_t B, int64_t nc) {
+    const int lane = threadIdx.x & 63;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kMixWaves;
+    int64_t t = static_cast<int64_t>(blockIdx.x) * kMixWaves +
+                __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+    if (t >= B) return;  // uniform; nc >= 1 here
+    int64_t c0 = 0;
+    auto offset = [&](int64_t tt, int64_t cc0) {
+        const int64_t cc = cc0 + lane;
+        return 4 * nc * tt + (cc < nc ? cc : nc - 1);
+    };
+    auto load_item = [&](int64_t off, v4u v[4]) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = __builtin_nontemporal_load(X + off + j * nc);
+    };
+    float p[16];
+    load_token_matrix(P, t, p);
+    // mix the item in `cur` while the next one (or, after the last, this one again) loads
+    // into `nxt`
+    auto step = [&](const v4u cur[4], v4u nxt[4]) {
+        int64_t tn = t, cn = c0 + 64;
+        if (cn >= nc) {
+            cn = 0;
+            tn = t + stride;
+        }
+        const bool more = tn < B;
+        load_item(more ? offset(tn, cn) : offset(t, c0), nxt);
+        __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the waits for `cur`
+        v4u out[4];
+        mix_chunk<DX>(p, cur, out);
+        const int64_t off = offset(t, c0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) __builtin_nontemporal_store(out[i], Y + off + i * nc);
+        if (more && tn != t) load_token_matrix(P, tn, p);
+        t = tn;
+        c0 = cn;
+    };
+    // The first step is peeled and the rest run as a counted loop of two steps: each step's
+    // loads are then used unconditionally by the next one (so they stay where they are
+    // issued), and every path into a step leaves the same loads and stores in flight (so the
+    // wait for `cur` does not cover the previous step's stores).
+    const int64_t items = ((B - t + stride - 1) / stride) * ((nc + 63) >> 6);
+    v4u a[4], b[4];
+    load_item(offset(t, 0), a);
+    step(a, b);
+    int64_t k = 1;
+    for (; k + 2 <= items; k += 2) {
+        step(b, a);
+        step(a, b);
+    }
+    if (k < items) step(b, a);
+}
+
+// Sum over the 64 lanes of the wave of each of v[0..15]; every lane receives all sixteen
+// sums. Halving exchange: at lane mask m a lane keeps the half of its values selected by
+// its bit m and adds its partner's copy of that half, so after masks 32, 16, 8, 4 lane L
+// holds value (L >> 2) & 15 summed over the lanes that share its two low bits; two more
+// exchanges complete the sums (17 shuffles instead of 96).
+__device__ __forceinline__ void wave_sum16(float v[16], int lane, float s[16]) {
+#pragma unroll
+    for (int step = 0; step < 4; ++step) {
+        const int m = 32 >> step, n = 8 >> step;
+        const bool hi = (lane & m) != 0;
+#pragma unroll
+        for (int k = 0; k < n; ++k) {
+            const float send = hi ? v[k] : v[k + n];
+            const float keep = hi ? v[k + n] : v[k];
+            v[k] = keep + __shfl_xor(send, m);
+        }
+    }
+    float r = v[0];
+    r += __shfl_xor(r, 1);
+    r += __shfl_xor(r, 2);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) s[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(r), 4 * q));
+}
+
+// The same walk; a token's dP is summed over the wave when its last item is done, while
+// the next item's loads are in flight. Lanes past the end of a row zero their X words, so
+// that the chunk they repeat adds nothing to dP.
+template <int DX>
+__global__ __launch_bounds__(kMixBlock) void mix_bwd_kernel(const float* __restrict__ P,
+                                                             const v4u* __restrict__ X,
+                                                             const v4u* __restrict__ dY, v4u* __restrict__ dX,
+                                                             float* __restrict__ dH, int64_t B, int64_t nc) {
+    constexpr int E = MixChunk<DX>::E;
+    const int lane = threadIdx.x & 63;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kMixWaves;
+    int64_t t = static_cast<int64_t>(blockIdx.x) * kMixWaves +
+                __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+    if (t >= B) return;
+    float p[16], pt[16], acc[16];  // acc: this lane's part of dP_ij = sum_c dY_i[c] X_j[c]
+    auto token_matrix = [&](int64_t tt) {
+        load_token_matrix(P, tt, p);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) pt[4 * j + i] = p[4 * i + j];
+    };
+    // dH of token t from the lanes' partial dP (uniform branch: every lane takes part)
+    auto finish_token = [&]() {
+        float G[16], out[16];
+        wave_sum16(acc, lane, G);
+        implicit_vjp(p, G, out);
+        if (lane < 4) {
+            const v4f row = lane == 0 ? v4f{out[0], out[1], out[2], out[3]}
+                          : lane == 1 ? v4f{out[4], out[5], out[6], out[7]}
+                          : lane == 2 ? v4f{out[8], out[9], out[10], out[11]}
+                                      : v4f{out[12], out[13], out[14], out[15]};
+            reinterpret_cast<v4f*>(dH)[4 * t + lane] = row;
+        }
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+    };
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+    token_matrix(t);
+    if (nc == 0) {  // no channels: dP = 0 (uniform)
+        for (;;) {
+            finish_token();
+            t += stride;
+            if (t >= B) return;
+            token_matrix(t);
+        }
+    }
+    int64_t c0 = 0;
+    auto offset = [&](int64_t tt, int64_t cc0) {
+        const int64_t cc = cc0 + lane;
+        return 4 * nc * tt + (cc < nc ? cc : nc - 1);
+    };
+    auto load_item = [&](int64_t off, v4u x[4], v4u g[4]) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            x[j] = __builtin_nontemporal_load(X + off + j * nc);
+            g[j] = __builtin_nontemporal_load(dY + off + j * nc);
+        }
+    };
+    auto step = [&](const v4u xc[4], const v4u gc[4], v4u xn[4], v4u gn[4]) {
+        int64_t tn = t, cn = c0 + 64;
+        if (cn >= nc) {
+            cn = 0;
+            tn = t + stride;
+        }
+        const bool more = tn < B;
+        load_item(more ? offset(tn, cn) : offset(t, c0), xn, gn);
+        __builtin_amdgcn_sched_barrier(0);
+        v4u o[4];
+        mix_chunk<DX>(pt, gc, o);
+        const int64_t off = offset(t, c0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) __builtin_nontemporal_store(o[j], dX + off + j * nc);
+        const bool own = c0 + lane < nc;
+        float xv[4][E], gv[4][E];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            unpack_chunk<DX>(own ? xc[j] : v4u{0u, 0u, 0u, 0u}, xv[j]);
+            unpack_chunk<DX>(gc[j], gv[j]);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int e = 0; e < E; ++e) acc[4 * i + j] = __builtin_fmaf(gv[i][e], xv[j][e], acc[4 * i + j]);
+        if (tn != t) {
+            finish_token();
+            if (more) token_matrix(tn);
+        }
+        t = tn;
+        c0 = cn;
+    };
+    // peeled first step and counted loop of two, as in the forward
+    const int64_t items = ((B - t + stride - 1) / stride) * ((nc + 63) >> 6);
+    v4u xa[4], ga[4], xb[4], gb[4];
+    load_item(offset(t, 0), xa, ga);
+    step(xa, ga, xb, gb);
+    int64_t k = 1;
+    for (; k + 2 <= items; k += 2) {
+        step(xb, gb, xa, ga);
+        step(xa, ga, xb, gb);
+    }
+    if (k < items) step(xb, gb, xa, ga);
+}
+
+// ---------------------------------------------------------------------------
 // Sinkhorn-Knopp baseline (eq. sinkhorn_knopp), one problem per lane
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void sk_kernel_matrix(const float h[16], float A[16]) {
@@ -2637,6 +2906,24 @@ int64_t grid_for(int64_t B, int block, int cus, int per_cu) {
     return blocks < cap ? blocks : cap;
 }
 
+// Residual mixing: one token per wave at a time, grid-stride over the tokens.
+template <int DX>
+int launch_mix_fwd(const float* P, const void* X, void* Y, int64_t B, int64_t nc, hipStream_t stream, int cus) {
+    const int64_t grid = grid_for(B, kMixWaves, cus, kMixPerCu);
+    hipLaunchKernelGGL((mix_fwd_kernel<DX>), dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
+                       static_cast<const v4u*>(X), static_cast<v4u*>(Y), B, nc);
+    return launch_status();
+}
+
+template <int DX>
+int launch_mix_bwd(const float* P, const void* X, const void* dY, void* dX, float* dH, int64_t B, int64_t nc,
+                   hipStream_t stream, int cus) {
+    const int64_t grid = grid_for(B, kMixWaves, cus, kMixPerCu);
+    hipLaunchKernelGGL((mix_bwd_kernel<DX>), dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
+                       static_cast<const v4u*>(X), static_cast<const v4u*>(dY), static_cast<v4u*>(dX), dH, B, nc);
+    return launch_status();
+}
+
 }  // namespace
 
 extern "C" {
@@ -2944,6 +3231,58 @@ int birkhoff4_sk_bwd(const void* H, int h_dtype, const void* dP, int dp_dtype, f
     return launch_status();
 }
 
+int birkhoff4_mix_fwd(const void* H, int h_dtype, const void* X, int x_dtype, void* Y, float* P, float* dual,
+                      int32_t* iters, int64_t B, int64_t C, float tol, int max_iter, hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 64)) return BIRKHOFF4_ERR_SIZE;
+    if (!dtype_ok(h_dtype) || !dtype_ok(x_dtype)) return BIRKHOFF4_ERR_DTYPE;
+    const int64_t E = x_dtype == BIRKHOFF4_BF16 ? 8 : 4;
+    if (C < 0 || C % E != 0) return BIRKHOFF4_ERR_CHANNELS;
+    const int64_t nc = C / E;  // 16-byte chunks per row
+    if (B > 0 && nc > INT64_MAX / 64 / B) return BIRKHOFF4_ERR_SIZE;
+    if (!(tol >= 0.f)) return BIRKHOFF4_ERR_TOL;
+    if (max_iter < 0 || max_iter > kMaxIterCap) return BIRKHOFF4_ERR_MAX_ITER;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!H || !P || (nc > 0 && (!X || !Y))) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(H) || misaligned(X) || misaligned(Y) || misaligned(P) || misaligned(dual) || misaligned(iters))
+        return BIRKHOFF4_ERR_ALIGN;
+    const size_t nh = static_cast<size_t>(B) * 16 * dtype_bytes(h_dtype), nx = static_cast<size_t>(B) * 64 * nc;
+    const size_t np = static_cast<size_t>(B) * 64, nd = dual ? static_cast<size_t>(B) * 32 : 0,
+                 ni = iters ? static_cast<size_t>(B) * 4 : 0;
+    if (overlaps(Y, nx, H, nh) || overlaps(Y, nx, X, nx) || overlaps(Y, nx, P, np) || overlaps(Y, nx, dual, nd) ||
+        overlaps(Y, nx, iters, ni) || overlaps(P, np, X, nx) || overlaps(dual, nd, X, nx) ||
+        overlaps(iters, ni, X, nx))
+        return BIRKHOFF4_ERR_OVERLAP;
+    int cus = 0;
+    if (int e = device_cus(&cus)) return e;
+    // the projection checks and queues P first; the mixing kernel then reads it
+    if (int e = birkhoff4_fwd_ex2(H, h_dtype, P, dual, iters, B, tol, max_iter, BIRKHOFF4_AUTO, stream)) return e;
+    if (nc == 0) return BIRKHOFF4_OK;
+    if (x_dtype == BIRKHOFF4_BF16) return launch_mix_fwd<BIRKHOFF4_BF16>(P, X, Y, B, nc, stream, cus);
+    return launch_mix_fwd<BIRKHOFF4_F32>(P, X, Y, B, nc, stream, cus);
+}
+
+int birkhoff4_mix_bwd(const float* P, const void* X, const void* dY, int x_dtype, void* dX, float* dH, int64_t B,
+                      int64_t C, hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 64)) return BIRKHOFF4_ERR_SIZE;
+    if (!dtype_ok(x_dtype)) return BIRKHOFF4_ERR_DTYPE;
+    const int64_t E = x_dtype == BIRKHOFF4_BF16 ? 8 : 4;
+    if (C < 0 || C % E != 0) return BIRKHOFF4_ERR_CHANNELS;
+    const int64_t nc = C / E;
+    if (B > 0 && nc > INT64_MAX / 64 / B) return BIRKHOFF4_ERR_SIZE;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!P || !dH || (nc > 0 && (!X || !dY || !dX))) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(P) || misaligned(X) || misaligned(dY) || misaligned(dX) || misaligned(dH))
+        return BIRKHOFF4_ERR_ALIGN;
+    const size_t np = static_cast<size_t>(B) * 64, nx = static_cast<size_t>(B) * 64 * nc;
+    if (overlaps(dX, nx, P, np) || overlaps(dX, nx, X, nx) || overlaps(dX, nx, dY, nx) || overlaps(dX, nx, dH, np) ||
+        overlaps(dH, np, P, np) || overlaps(dH, np, X, nx) || overlaps(dH, np, dY, nx))
+        return BIRKHOFF4_ERR_OVERLAP;
+    int cus = 0;
+    if (int e = device_cus(&cus)) return e;
+    if (x_dtype == BIRKHOFF4_BF16) return launch_mix_bwd<BIRKHOFF4_BF16>(P, X, dY, dX, dH, B, nc, stream, cus);
+    return launch_mix_bwd<BIRKHOFF4_F32>(P, X, dY, dX, dH, B, nc, stream, cus);
+}
+
 const char* birkhoff4_strerror(int code) {
     switch (code) {
         case BIRKHOFF4_OK: return "ok";
@@ -2959,6 +3298,7 @@ const char* birkhoff4_strerror(int code) {
         case BIRKHOFF4_ERR_LAUNCH: return "kernel launch failed";
         case BIRKHOFF4_ERR_VARIANT: return "unknown forward variant";
         case BIRKHOFF4_ERR_ETA: return "eta must be positive and finite";
+        case BIRKHOFF4_ERR_CHANNELS: return "C must be >= 0 and a multiple of 8 (bf16 streams) or 4 (fp32)";
         default: return "unknown error";
     }
 }

@@ -20,6 +20,9 @@ OK, ERR_NULL, ERR_SIZE, ERR_TOL, ERR_MAX_ITER, ERR_DTYPE, ERR_ALIGN, ERR_OVERLAP
     0, -1, -2, -3, -4, -5, -6, -7, -8)
 ERR_VARIANT = -11
 ERR_ETA = -12
+ERR_CHANNELS = -13
+E = 0x50000000
+F = 0x60000000
 
 A = 0x10000000        # fake, 16-byte aligned device addresses far apart
 Bp = 0x20000000
@@ -208,3 +211,36 @@ def test_ot8_argument_errors():
     assert g(A, Bp, C, -1.0, D, 5, None) == ERR_ETA
     assert g(A, None, C, 1.0, D, 5, None) == ERR_NULL
     assert g(A, Bp, C, 1.0, A + 256, 5, None) == ERR_OVERLAP
+
+
+def test_mix_argument_errors():
+    lib = b4.lib()
+    f = lib.birkhoff4_mix_fwd  # (H, h_dtype, X, x_dtype, Y, P, dual, iters, B, C, tol, max_iter, stream)
+    BF, F32 = b4.BF16, b4.F32
+    assert f(A, F32, Bp, BF, C, D, None, None, 0, 64, 1e-6, 20, None) == OK
+    assert f(A, F32, Bp, BF, C, D, None, None, -1, 64, 1e-6, 20, None) == ERR_SIZE
+    assert f(A, F32, Bp, 7, C, D, None, None, 5, 64, 1e-6, 20, None) == ERR_DTYPE
+    assert f(A, 7, Bp, BF, C, D, None, None, 5, 64, 1e-6, 20, None) == ERR_DTYPE
+    assert f(A, F32, Bp, BF, C, D, None, None, 5, 12, 1e-6, 20, None) == ERR_CHANNELS  # bf16: C % 8
+    assert f(A, F32, Bp, F32, C, D, None, None, 5, 6, 1e-6, 20, None) == ERR_CHANNELS  # fp32: C % 4
+    assert f(A, F32, Bp, F32, C, D, None, None, 5, -4, 1e-6, 20, None) == ERR_CHANNELS
+    assert f(A, F32, Bp, BF, C, D, None, None, 1 << 40, 1 << 30, 1e-6, 20, None) == ERR_SIZE
+    assert f(A, F32, Bp, BF, C, D, None, None, 5, 64, -1.0, 20, None) == ERR_TOL
+    assert f(A, F32, Bp, BF, C, D, None, None, 5, 64, 1e-6, -1, None) == ERR_MAX_ITER
+    assert f(A, F32, None, BF, C, D, None, None, 5, 64, 1e-6, 20, None) == ERR_NULL
+    assert f(A, F32, Bp, BF, None, D, None, None, 5, 64, 1e-6, 20, None) == ERR_NULL
+    assert f(A, F32, Bp, BF, C, None, None, None, 5, 64, 1e-6, 20, None) == ERR_NULL
+    assert f(A, F32, Bp + 8, BF, C, D, None, None, 5, 64, 1e-6, 20, None) == ERR_ALIGN
+    assert f(A, F32, Bp, BF, Bp + 16, D, None, None, 5, 64, 1e-6, 20, None) == ERR_OVERLAP   # Y inside X
+    assert f(A, F32, Bp, BF, C, Bp + 64, None, None, 5, 64, 1e-6, 20, None) == ERR_OVERLAP   # P inside X
+    assert f(A, F32, Bp, BF, C, D, C + 32, None, 5, 64, 1e-6, 20, None) == ERR_OVERLAP      # dual inside Y
+    g = lib.birkhoff4_mix_bwd  # (P, X, dY, x_dtype, dX, dH, B, C, stream)
+    assert g(A, Bp, C, BF, D, E, 0, 64, None) == OK
+    assert g(A, Bp, C, BF, D, E, 5, 60, None) == ERR_CHANNELS
+    assert g(A, Bp, C, 9, D, E, 5, 64, None) == ERR_DTYPE
+    assert g(A, Bp, C, BF, D, None, 5, 64, None) == ERR_NULL
+    assert g(A, Bp, None, BF, D, E, 5, 64, None) == ERR_NULL
+    assert g(A, Bp, C, BF, D + 4, E, 5, 64, None) == ERR_ALIGN
+    assert g(A, Bp, C, BF, C + 256, E, 5, 64, None) == ERR_OVERLAP    # dX inside dY
+    assert g(A, Bp, C, BF, D, A + 64, 5, 64, None) == ERR_OVERLAP     # dH inside P
+    assert g(A, Bp, C, BF, D, Bp + 128, 5, 64, None) == ERR_OVERLAP   # dH inside X

@@ -135,3 +135,15 @@ def test_graph_many_launches():
         return outs
 
     graph_roundtrip(fn, sets, "16 pairs")
+
+
+def test_graph_mix():
+    say("test: graph capture of the residual-mixing pair")
+    sets = [list(workloads.mix_streams_device(3001, 264, 70 + k, "cuda")) for k in range(N_SETS)]
+
+    def fn(H, X, G):
+        Y, P, _, it = b4.mix_fwd(H, X, 1e-6, 64, want_iters=True)
+        dX, dH = b4.mix_bwd(P, X, G)
+        return Y, P, it, dX, dH
+
+    graph_roundtrip(fn, sets, "mix")

@@ -66,3 +66,18 @@ def test_device_generators_on_cpu():
     assert M.shape == (500, 4, 4) and a.shape == (500, 4) and b.shape == (500, 4) and dT.shape == (500, 4, 4)
     assert (a >= 0.2).all() and (a <= 2.0).all() and (b > 0).all()
     assert (a.double().sum(1) - b.double().sum(1)).abs().max() < 1e-5
+
+
+def test_mix_streams_generator_on_cpu():
+    import torch
+    H, X, G = workloads.mix_streams_device(400, 24, 60, "cpu")
+    assert H.shape == (400, 4, 4) and X.shape == (400, 4, 24) and G.shape == (400, 4, 24)
+    assert H.dtype == X.dtype == G.dtype == torch.bfloat16
+    H2, X2, _ = workloads.mix_streams_device(400, 24, 60, "cpu")
+    assert torch.equal(H, H2) and torch.equal(X, X2)
+    Hf = H.float()
+    near20 = (Hf - 20).abs() < 0.6
+    rest_small = torch.where(near20, torch.zeros_like(Hf), Hf).abs().amax(dim=(1, 2)) < 0.6
+    is_perm = (near20.sum(2) == 1).all(1) & (near20.sum(1) == 1).all(1) & rest_small
+    assert 0.35 < is_perm.float().mean().item() < 0.65
+    assert abs(X.float().std().item() - 1.0) < 0.05
