@@ -54,6 +54,19 @@ def valu_from_profiles(workload: str, kernel: str, kind: str = "valu"):
     return float(mm.group(1)) if mm else None
 
 
+def profile_figure(fname: str, key: str):
+    """A `key: value` figure of profiles/<fname>, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", fname)
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"source_sha256[^:]*:\s*([0-9a-f]{64})", text)
+    if not m or m.group(1) != hashlib.sha256(open(SRC, "rb").read()).hexdigest():
+        return None
+    mm = re.search(rf"{key}:\s*([0-9.eE+]+)", text)
+    return float(mm.group(1)) if mm else None
+
+
 def traffic_from_profiles(workload: str):
     """HBM bytes per launch measured by rocprofv3 counters, if they were taken on
     the current kernel source (profiles/traffic_<workload>.md)."""
@@ -96,7 +109,7 @@ def main() -> int:
     ap.add_argument("--mix-only", action="store_true", help="time only the residual-mixing pair (for profiler runs)")
     ap.add_argument("--small-only", action="store_true", help="time only the small-batch cases")
     ap.add_argument("--no-extras", action="store_true",
-                    help="time only the path (for profiler runs)")
+                    help="time only the headline path, none of the other measurements (for profiler runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy 5 times (scale for HBM byte counters)")
     args = ap.parse_args()
@@ -345,14 +358,15 @@ def main() -> int:
                                         "tol": args.tol, "seconds": round(rates["gpu_tol"][1], 2)}
         log(f"cpu baseline: {out['cpu_baseline']}")
 
-    if not args.no_n8:
+    # the other workloads, each timed after the headline's region (--no-extras: the path only)
+    if not args.no_n8 and not args.no_extras:
         out["n8"] = bench_n8(args, dev, stream)
-    if not args.no_ot:
+    if not args.no_ot and not args.no_extras:
         out["ot"] = bench_ot(args, dev, stream)
         out["ot8"] = bench_ot(args, dev, stream, n=8)
-    if not args.no_small:
+    if not args.no_small and not args.no_extras:
         out["small_batch"] = bench_small_batch(dev)
-    if not args.no_mix:
+    if not args.no_mix and not args.no_extras:
         out["mix_streams"] = bench_mix_streams(args, dev, stream)
 
     print(json.dumps(out), flush=True)
@@ -425,7 +439,10 @@ def bench_mix_streams(args, dev, stream, B=1 << 15, C=4096) -> dict:
     dom = "mix_bwd" if b_ms >= f_ms else "mix_fwd (projection + mixing)"
     ach = res["kernels"][dom]["achieved_GBs"]
     res["roofline"] = {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                       "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+                       "frac": round(ach / HBM_PEAK_GBS, 4),
+                       "traffic": profile_figure(f"kernel_trace_{res['workload']}.md",
+                                                 "mix_bwd_hbm_bytes_per_launch" if dom == "mix_bwd"
+                                                 else "mix_fwd_hbm_bytes_per_launch")}
     log(f"mix streams: {res}")
     if not args.no_cpu_baseline:
         from oracle.mix import mix_bwd as o_bwd, mix_fwd as o_fwd
