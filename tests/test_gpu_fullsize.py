@@ -78,3 +78,29 @@ def test_fullsize(name):
     dHs = dH[idx_t].cpu().numpy() if dH is not None else None
     dPs = ch.dP[idx] if ch.dP is not None else None
     check_parity(ch.H[idx], Ps, ds, dPs, dHs, f"{name} sample of {len(idx)}")
+
+
+def test_beyond_32bit_offsets():
+    # B = 2^27 fp32 matrices: every array is 8 GB (dual 4 GB) and byte offsets pass 2^32 at
+    # b = 2^26; both forward variants' index arithmetic is 64-bit. Every matrix is checked for
+    # convergence and marginals; parity on samples around 2^26 and at the end.
+    B = 1 << 27
+    say(f"test: B={B} fp32 (8 GB per array), throughput forward + backward")
+    g = torch.Generator(device="cuda").manual_seed(27)
+    H = 5.0 * torch.randn(B, 4, 4, device="cuda", generator=g)
+    G = torch.randn(B, 4, 4, device="cuda", generator=g)
+    P, dual, it = b4.fwd(H, 1e-6, MAX_ITER, want_dual=True, want_iters=True)
+    dH = b4.bwd(P, G)
+    torch.cuda.synchronize()
+    assert (it >= 0).all().item()
+    worst = 0.0
+    for s in range(0, B, 1 << 24):  # fp64 marginals in slices, to bound the temporary memory
+        worst = max(worst, marginal_linf_device(P[s:s + (1 << 24)]).max().item())
+    say(f"  max marginal over all {B}: {worst:.3e}")
+    assert worst <= TOL_MARGINAL
+    rng = np.random.default_rng(27)
+    idx = np.unique(np.concatenate([np.arange((1 << 26) - 64, (1 << 26) + 64), np.arange(B - 128, B),
+                                    rng.choice(B, 1000, replace=False)]))
+    ti = torch.from_numpy(idx).cuda()
+    check_parity(H[ti].cpu().numpy(), P[ti].cpu().numpy(), dual[ti].cpu().numpy(), G[ti].cpu().numpy(),
+                 dH[ti].cpu().numpy(), "B=2^27 sample")

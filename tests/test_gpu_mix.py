@@ -3,8 +3,9 @@ with the fp64 oracle, element by element.
 
 Bounds, per element: P within 1e-5 of the oracle's (the projection's own bound), so an
 output mixed from four inputs may differ by 1e-5 times the sum of their magnitudes, plus
-fp32 rounding, plus for bf16 outputs one rounding to bf16 (at most half a unit in the last
-place, 2^-9 relative; 2^-8 is allowed). dH is held to the projection backward's bound,
+fp32 rounding, plus for bf16 outputs one rounding to bf16. With an 8-bit significand, half a
+unit in the last place is up to 2^-8 of the value just above a power of two, and the value
+rounded is the fp32 result, not the exact one: 2^-7 of the value is allowed. dH is held to the projection backward's bound,
 |dH - dH_ref|_inf / max(1, |dH_ref|_inf) <= 1e-4 per token.
 """
 import numpy as np
@@ -36,7 +37,7 @@ def mixed_bound(P_err, inputs, out_ref, bf16):
     s = np.abs(inputs).sum(axis=1, keepdims=True)
     b = P_err * s + 1e-6 * s + 1e-30
     if bf16:
-        b = b + 2.0 ** -8 * np.abs(out_ref)
+        b = b + 2.0 ** -7 * np.abs(out_ref)
     return b
 
 
@@ -170,6 +171,30 @@ def test_fullsize_bench_workload():
     Hs = H[ti].float().cpu().numpy()
     Xs = X[ti].float().cpu().numpy()
     Gs = G[ti].float().cpu().numpy()
+    Yr, Pr = o_fwd(Hs, Xs)
+    dXr, dHr = o_bwd(Pr, Xs, Gs)
+    assert np.abs(P[ti].cpu().numpy() - Pr).max() <= TOL_P
+    ey = np.abs(Y[ti].float().cpu().numpy() - Yr) / mixed_bound(TOL_P, Xs, Yr, True)
+    ex = np.abs(dX[ti].float().cpu().numpy() - dXr) / mixed_bound(TOL_P, Gs, dXr, True)
+    e = np.abs(dH[ti].cpu().numpy() - dHr).max(axis=(1, 2)) / np.maximum(1.0, np.abs(dHr).max(axis=(1, 2)))
+    say(f"  sample of {len(idx)}: Y err/bound={ey.max():.3f} dX err/bound={ex.max():.3f} dH rel={e.max():.2e}")
+    assert ey.max() <= 1.0 and ex.max() <= 1.0 and e.max() <= TOL_DH
+
+
+def test_beyond_32bit_offsets():
+    # 2^16 tokens x 4 streams x C = 16384 bf16: 8 GB per stream tensor, byte offsets pass 2^32
+    # at token 2^15; samples on both sides of it and at the end
+    B, C = 1 << 16, 16384
+    say(f"test: mix B={B} C={C} bf16 (8 GB per stream tensor)")
+    H, X, G = workloads.mix_streams_device(B, C, 61, "cuda")
+    Y, P, _, it = b4.mix_fwd(H, X, want_iters=True)
+    dX, dH = b4.mix_bwd(P, X, G)
+    torch.cuda.synchronize()
+    assert (it >= 0).all().item()
+    idx = np.unique(np.concatenate([np.arange((1 << 15) - 40, (1 << 15) + 40), np.arange(B - 40, B),
+                                    np.random.default_rng(5).choice(B, 60, replace=False)]))
+    ti = torch.from_numpy(idx).cuda()
+    Hs, Xs, Gs = H[ti].float().cpu().numpy(), X[ti].float().cpu().numpy(), G[ti].float().cpu().numpy()
     Yr, Pr = o_fwd(Hs, Xs)
     dXr, dHr = o_bwd(Pr, Xs, Gs)
     assert np.abs(P[ti].cpu().numpy() - Pr).max() <= TOL_P
