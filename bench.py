@@ -147,7 +147,9 @@ def main() -> int:
         print(json.dumps({"ot": bench_ot(args, dev, torch.cuda.current_stream(dev))}), flush=True)
         return 0
     if args.mix_only:
-        print(json.dumps({"mix_streams": bench_mix_streams(args, dev, torch.cuda.current_stream(dev))}), flush=True)
+        st = torch.cuda.current_stream(dev)
+        print(json.dumps({"mix_streams": bench_mix_streams(args, dev, st),
+                          "mix8_streams": bench_mix_streams(args, dev, st, B=1 << 14, n=8)}), flush=True)
         return 0
     if args.small_only:
         print(json.dumps({"small_batch": bench_small_batch(dev)}), flush=True)
@@ -368,12 +370,13 @@ def main() -> int:
         out["small_batch"] = bench_small_batch(dev)
     if not args.no_mix and not args.no_extras:
         out["mix_streams"] = bench_mix_streams(args, dev, stream)
+        out["mix8_streams"] = bench_mix_streams(args, dev, stream, B=1 << 14, n=8)
 
     print(json.dumps(out), flush=True)
     return 0
 
 
-def bench_mix_streams(args, dev, stream, B=1 << 15, C=4096) -> dict:
+def bench_mix_streams(args, dev, stream, B=1 << 15, C=4096, n=4) -> dict:
     """Residual mixing of the mHC layer (Y = P X per token, P = proj(exp(H))) and its backward
     on B tokens of 4 bf16 streams with C channels: per-call event times, algorithmic GB/s
     and the oracle's rate on a sample of tokens."""
@@ -381,12 +384,14 @@ def bench_mix_streams(args, dev, stream, B=1 << 15, C=4096) -> dict:
 
     import paper_2606_07574_amd as b4
     import workloads
-    H, X, G = workloads.mix_streams_device(B, C, 60, dev)
+    H, X, G = workloads.mix_streams_device(B, C, 60 + n, dev, n)
     Y = torch.empty_like(X)
     dX = torch.empty_like(X)
-    P = torch.empty(B, 4, 4, device=dev)
-    dH = torch.empty(B, 4, 4, device=dev)
+    P = torch.empty(B, n, n, device=dev)
+    dH = torch.empty(B, n, n, device=dev)
     lib = b4.lib()
+    mfwd, mbwd = (lib.birkhoff4_mix_fwd, lib.birkhoff4_mix_bwd) if n == 4 else (lib.birkhoff8_mix_fwd,
+                                                                                 lib.birkhoff8_mix_bwd)
     sptr = stream.cuda_stream
     K = max(5, args.steps // 2)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
@@ -394,14 +399,13 @@ def bench_mix_streams(args, dev, stream, B=1 << 15, C=4096) -> dict:
     def step(e):
         if e:
             e[0].record(stream)
-        rc = lib.birkhoff4_mix_fwd(H.data_ptr(), b4.BF16, X.data_ptr(), b4.BF16, Y.data_ptr(), P.data_ptr(), None,
-                                   None, B, C, args.tol, args.max_iter, sptr)
+        rc = mfwd(H.data_ptr(), b4.BF16, X.data_ptr(), b4.BF16, Y.data_ptr(), P.data_ptr(), None, None, B, C,
+                  args.tol, args.max_iter, sptr)
         if rc:
             raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
         if e:
             e[1].record(stream)
-        rc = lib.birkhoff4_mix_bwd(P.data_ptr(), X.data_ptr(), G.data_ptr(), b4.BF16, dX.data_ptr(), dH.data_ptr(),
-                                   B, C, sptr)
+        rc = mbwd(P.data_ptr(), X.data_ptr(), G.data_ptr(), b4.BF16, dX.data_ptr(), dH.data_ptr(), B, C, sptr)
         if rc:
             raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
         if e:
@@ -416,10 +420,12 @@ def bench_mix_streams(args, dev, stream, B=1 << 15, C=4096) -> dict:
     wall = (time.perf_counter() - t0) / K
     f_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
     b_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
-    fb = 32 + 64 + 16 * C          # H (bf16), P, X, Y
-    bb = 64 + 24 * C + 64          # P, X, dY, dX, dH
-    res = {"workload": f"mix_streams_b2e{B.bit_length() - 1}_c{C}", "B": B, "C": C,
-           "desc": f"B={B} tokens, 4 bf16 streams of C={C} channels, X, dY ~ N(0,1); logits H from the "
+    nn = n * n
+    fb = 2 * nn + 4 * nn + 4 * n * C        # H (bf16), P, X, Y (bf16)
+    bb = 4 * nn + 6 * n * C + 4 * nn        # P, X, dY, dX, dH
+    name = f"mix_streams_b2e{B.bit_length() - 1}_c{C}" + ("" if n == 4 else f"_n{n}")
+    res = {"workload": name, "B": B, "C": C, "n": n,
+           "desc": f"B={B} tokens, {n} bf16 streams of C={C} channels, X, dY ~ N(0,1); logits H from the "
                    "headline mixture in bf16; fwd = projection + Y = P X, bwd = dX = P^T dY, dP = dY X^T, dH",
            "steps": K, "value": round(B / wall, 1), "unit": "tokens/s", "ms_per_step": round(wall * 1e3, 4),
            "fwd_ms": round(f_ms, 4), "bwd_ms": round(b_ms, 4),

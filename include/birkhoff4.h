@@ -249,6 +249,16 @@ int birkhoff4_mix_fwd(const void* H, int h_dtype, const void* X, int x_dtype, vo
 int birkhoff4_mix_bwd(const float* P, const void* X, const void* dY, int x_dtype, void* dX, float* dH, int64_t B,
                       int64_t C, hipStream_t stream);
 
+/* Residual mixing with n = 8 streams per token: birkhoff4_mix_fwd / birkhoff4_mix_bwd with the
+ * 8 x 8 projection (birkhoff8_fwd / birkhoff8_bwd). H and P are [B][8][8], X, Y, dY, dX are
+ * [B][8][C] (stream i of token b starts at element (8 b + i) C), dual [B][16] and iters as for
+ * birkhoff8_fwd, dH [B][8][8] fp32. Arguments, dtypes, the rule for C, return codes and overlap
+ * rules as for the 4 x 4 calls. */
+int birkhoff8_mix_fwd(const void* H, int h_dtype, const void* X, int x_dtype, void* Y, float* P, float* dual,
+                      int32_t* iters, int64_t B, int64_t C, float tol, int max_iter, hipStream_t stream);
+int birkhoff8_mix_bwd(const float* P, const void* X, const void* dY, int x_dtype, void* dX, float* dH, int64_t B,
+                      int64_t C, hipStream_t stream);
+
 /* Human-readable text for a return code (static storage). */
 const char* birkhoff4_strerror(int code);
 

@@ -12,7 +12,7 @@ matrix product Y = P X with P = proj(exp(H)) (eq. birkhoff_projection, computed 
 dX = P^T dY and dP = dY X^T, and dH is the projection's gradient (eq. derivative,
 the 4x4 oracle's bwd) applied to that dP.
 
-Functions:
+Functions (n streams per token: the 4 x 4 oracle for n = 4, the size-generic one otherwise):
   mix_fwd(H, X, tol) -> Y, P       Y[b] = P[b] @ X[b]
   mix_bwd(P, X, dY) -> dX, dH      dX[b] = P[b]^T @ dY[b], dH = bwd(P, dY @ X^T)
 """
@@ -20,25 +20,31 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import bwd, fwd
+from . import birkhoffn, bwd, fwd
+
+
+def _projection(n: int):
+    """The 4 x 4 oracle for n = 4, the size-generic one otherwise."""
+    return (fwd, bwd) if n == 4 else (birkhoffn.fwd, birkhoffn.bwd)
 
 
 def mix_fwd(H: np.ndarray, X: np.ndarray, tol: float | None = None, threads: int | None = None):
-    """H [B, 4, 4], X [B, 4, C] (any float dtype; computed in fp64). Returns (Y, P)."""
+    """H [B, n, n], X [B, n, C] (any float dtype; computed in fp64). Returns (Y, P)."""
+    H = np.asarray(H, dtype=np.float64)
     kw = {} if tol is None else {"tol": tol}
     if threads is not None:
         kw["threads"] = threads
-    P, _, _ = fwd(np.asarray(H, dtype=np.float64), **kw)
+    P, _, _ = _projection(H.shape[-1])[0](H, **kw)
     Y = np.matmul(P, np.asarray(X, dtype=np.float64))
     return Y, P
 
 
 def mix_bwd(P: np.ndarray, X: np.ndarray, dY: np.ndarray, threads: int | None = None):
-    """From the forward's P [B, 4, 4], X and dY [B, 4, C]: (dX [B, 4, C], dH [B, 4, 4])."""
+    """From the forward's P [B, n, n], X and dY [B, n, C]: (dX [B, n, C], dH [B, n, n])."""
     P = np.asarray(P, dtype=np.float64)
     X = np.asarray(X, dtype=np.float64)
     dY = np.asarray(dY, dtype=np.float64)
     dX = np.matmul(np.swapaxes(P, -1, -2), dY)
     dP = np.matmul(dY, np.swapaxes(X, -1, -2))
     kw = {} if threads is None else {"threads": threads}
-    return dX, bwd(P, dP, **kw)
+    return dX, _projection(P.shape[-1])[1](P, dP, **kw)

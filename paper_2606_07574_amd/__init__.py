@@ -15,7 +15,8 @@ a GPU, the calls raise.
     T, dual = ot_fwd(M, a, b, eta); dM = ot_bwd(T, a, dT, eta)  # general entropic OT, 4 x 4
     T, dual = ot8_fwd(M, a, b, eta); dM = ot8_bwd(T, a, dT, eta)  # the same for 8 x 8
     Y, P, _, _ = mix_fwd(H, X); dX, dH = mix_bwd(P, X, dY)  # residual mixing Y = P X (Sec. 2.1)
-    Y = mix(H, X)                     # autograd-aware, gradients for H and X
+    Y = mix(H, X)                     # autograd-aware, gradients for H and X (4 or 8 streams)
+    Y, P, _, _ = mix8_fwd(H8, X8); dX, dH = mix8_bwd(P, X8, dY)  # 8 streams per token
 """
 from __future__ import annotations
 
@@ -68,6 +69,8 @@ def _load():
         "birkhoff8_ot_bwd": [vp, vp, vp, f32, vp, i64, st],
         "birkhoff4_mix_fwd": [vp, i32, vp, i32, vp, vp, vp, vp, i64, i64, f32, i32, st],
         "birkhoff4_mix_bwd": [vp, vp, vp, i32, vp, vp, i64, i64, st],
+        "birkhoff8_mix_fwd": [vp, i32, vp, i32, vp, vp, vp, vp, i64, i64, f32, i32, st],
+        "birkhoff8_mix_bwd": [vp, vp, vp, i32, vp, vp, i64, i64, st],
         "birkhoff4_version": [],
     }
     for name, args in sigs.items():
@@ -413,15 +416,48 @@ def ot8(M: torch.Tensor, a: torch.Tensor, b: torch.Tensor, eta: float = 1.0, tol
     return OT8Fn.apply(M, a, b, eta, tol, max_iter)
 
 
-def _streams(X: torch.Tensor, lead, name: str) -> int:
-    """Checks X as [..., 4, C] streams matching the leading dims; returns C."""
+def _streams(X: torch.Tensor, lead, name: str, n: int = 4) -> int:
+    """Checks X as [..., n, C] streams matching the leading dims; returns C."""
     if not X.is_cuda:
         raise Birkhoff4Error(f"{name} must be a GPU tensor (no CPU path)")
-    if X.dim() < 2 or tuple(X.shape[:-2]) != tuple(lead) or X.shape[-2] != 4:
-        raise ValueError(f"{name} must have shape {(*lead, 4, 'C')}, got {tuple(X.shape)}")
+    if X.dim() < 2 or tuple(X.shape[:-2]) != tuple(lead) or X.shape[-2] != n:
+        raise ValueError(f"{name} must have shape {(*lead, n, 'C')}, got {tuple(X.shape)}")
     if not X.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     return X.shape[-1]
+
+
+def _mix_fwd(n, H, X, tol, max_iter, want_dual, want_iters):
+    B = _batch(H, "H", n)
+    lead = H.shape[:-2]
+    C = _streams(X, lead, "X", n)
+    _same_device(H, X)
+    Y = torch.empty_like(X)
+    P = torch.empty(H.shape, dtype=torch.float32, device=H.device)
+    dual = torch.empty(*lead, 2 * n, dtype=torch.float32, device=H.device) if want_dual else None
+    iters = torch.empty(lead, dtype=torch.int32, device=H.device) if want_iters else None
+    fn = _load().birkhoff4_mix_fwd if n == 4 else _load().birkhoff8_mix_fwd
+    with torch.cuda.device(H.device):
+        _check(fn(_ptr(H), _dtype_code(H), _ptr(X), _dtype_code(X), _ptr(Y), _ptr(P), _ptr(dual), _ptr(iters), B, C,
+                  float(tol), int(max_iter), _stream(H)))
+    return Y, P, dual, iters
+
+
+def _mix_bwd(n, P, X, dY):
+    B = _batch(P, "P", n)
+    if P.dtype != torch.float32:
+        raise TypeError("P must be float32")
+    lead = P.shape[:-2]
+    C = _streams(X, lead, "X", n)
+    if _streams(dY, lead, "dY", n) != C or dY.dtype != X.dtype:
+        raise ValueError("dY must have the shape and dtype of X")
+    _same_device(P, X, dY)
+    dX = torch.empty_like(X)
+    dH = torch.empty(P.shape, dtype=torch.float32, device=P.device)
+    fn = _load().birkhoff4_mix_bwd if n == 4 else _load().birkhoff8_mix_bwd
+    with torch.cuda.device(P.device):
+        _check(fn(_ptr(P), _ptr(X), _ptr(dY), _dtype_code(X), _ptr(dX), _ptr(dH), B, C, _stream(P)))
+    return dX, dH
 
 
 def mix_fwd(H: torch.Tensor, X: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER,
@@ -431,57 +467,50 @@ def mix_fwd(H: torch.Tensor, X: torch.Tensor, tol: float = DEFAULT_TOL, max_iter
     H: [..., 4, 4] float32 or bfloat16 logits; X: [..., 4, C] float32 or bfloat16 streams
     (C a multiple of 8 for bfloat16, of 4 for float32). Returns (Y like X, P float32,
     dual or None, iters or None)."""
-    B = _batch(H, "H")
-    lead = H.shape[:-2]
-    C = _streams(X, lead, "X")
-    _same_device(H, X)
-    Y = torch.empty_like(X)
-    P = torch.empty(H.shape, dtype=torch.float32, device=H.device)
-    dual = torch.empty(*lead, 8, dtype=torch.float32, device=H.device) if want_dual else None
-    iters = torch.empty(lead, dtype=torch.int32, device=H.device) if want_iters else None
-    with torch.cuda.device(H.device):
-        _check(_load().birkhoff4_mix_fwd(_ptr(H), _dtype_code(H), _ptr(X), _dtype_code(X), _ptr(Y), _ptr(P),
-                                         _ptr(dual), _ptr(iters), B, C, float(tol), int(max_iter), _stream(H)))
-    return Y, P, dual, iters
+    return _mix_fwd(4, H, X, tol, max_iter, want_dual, want_iters)
 
 
 def mix_bwd(P: torch.Tensor, X: torch.Tensor, dY: torch.Tensor):
     """Backward of mix_fwd: (dX = P^T dY like X, dH float32) from P, X and dY (dtype of X)."""
-    B = _batch(P, "P")
-    if P.dtype != torch.float32:
-        raise TypeError("P must be float32")
-    lead = P.shape[:-2]
-    C = _streams(X, lead, "X")
-    if _streams(dY, lead, "dY") != C or dY.dtype != X.dtype:
-        raise ValueError("dY must have the shape and dtype of X")
-    _same_device(P, X, dY)
-    dX = torch.empty_like(X)
-    dH = torch.empty(P.shape, dtype=torch.float32, device=P.device)
-    with torch.cuda.device(P.device):
-        _check(_load().birkhoff4_mix_bwd(_ptr(P), _ptr(X), _ptr(dY), _dtype_code(X), _ptr(dX), _ptr(dH), B, C,
-                                         _stream(P)))
-    return dX, dH
+    return _mix_bwd(4, P, X, dY)
+
+
+def mix8_fwd(H: torch.Tensor, X: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER,
+             want_dual: bool = False, want_iters: bool = False):
+    """mix_fwd for 8 streams per token: H [..., 8, 8], X [..., 8, C]."""
+    return _mix_fwd(8, H, X, tol, max_iter, want_dual, want_iters)
+
+
+def mix8_bwd(P: torch.Tensor, X: torch.Tensor, dY: torch.Tensor):
+    """Backward of mix8_fwd."""
+    return _mix_bwd(8, P, X, dY)
 
 
 class MixFn(torch.autograd.Function):
-    """Y = proj(exp(H)) X per token; the backward is one pass over X and dY (mix_bwd)."""
+    """Y = proj(exp(H)) X per token (4 or 8 streams, from H's shape); the backward is one
+    pass over X and dY."""
 
     @staticmethod
     def forward(ctx, H, X, tol=DEFAULT_TOL, max_iter=DEFAULT_MAX_ITER):
         X = X.contiguous()
-        Y, P, _, _ = mix_fwd(H.contiguous(), X, tol, max_iter)
+        n = H.shape[-1]
+        Y, P, _, _ = _mix_fwd(n, H.contiguous(), X, tol, max_iter, False, False)
         ctx.save_for_backward(P, X)
         ctx.h_dtype = H.dtype
+        ctx.n = n
         return Y
 
     @staticmethod
     def backward(ctx, dY):
         P, X = ctx.saved_tensors
-        dX, dH = mix_bwd(P, X, dY.contiguous().to(X.dtype))
+        dX, dH = _mix_bwd(ctx.n, P, X, dY.contiguous().to(X.dtype))
         return dH.to(ctx.h_dtype), dX, None, None
 
 
 def mix(H: torch.Tensor, X: torch.Tensor, tol: float = DEFAULT_TOL, max_iter: int = DEFAULT_MAX_ITER) -> torch.Tensor:
+    """Y = proj(exp(H)) X per token with gradients for H and X; H [..., n, n] with n = 4 or 8."""
+    if H.dim() < 2 or H.shape[-1] not in (4, 8):
+        raise ValueError(f"H must have shape [..., 4, 4] or [..., 8, 8], got {tuple(H.shape)}")
     return MixFn.apply(H, X, tol, max_iter)
 
 

@@ -1056,29 +1056,55 @@ __device__ __forceinline__ v4u pack_chunk(const float v[MixChunk<DX>::E]) {
     return v4u{u[0], u[1], u[2], u[3]};
 }
 
-// out_i = sum_j m_ij in_j over the E channels of one chunk of each of the four rows.
+// Channels of 32-bit word w of a chunk: two for bf16, one for fp32.
 template <int DX>
-__device__ __forceinline__ void mix_chunk(const float m[16], const v4u in[4], v4u out[4]) {
-    constexpr int E = MixChunk<DX>::E;
-    float x[4][E];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) unpack_chunk<DX>(in[j], x[j]);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        float y[E];
-#pragma unroll
-        for (int e = 0; e < E; ++e)
-            y[e] = __builtin_fmaf(m[4 * i + 3], x[3][e],
-                   __builtin_fmaf(m[4 * i + 2], x[2][e], __builtin_fmaf(m[4 * i + 1], x[1][e], m[4 * i] * x[0][e])));
-        out[i] = pack_chunk<DX>(y);
+__device__ __forceinline__ void unpack_word(const v4u c, int w, float v[MixChunk<DX>::E / 4]) {
+    const uint32_t u = w == 0 ? c.x : w == 1 ? c.y : w == 2 ? c.z : c.w;
+    if constexpr (DX == BIRKHOFF4_BF16) {
+        v[0] = __uint_as_float(u << 16);
+        v[1] = __uint_as_float(u & 0xffff0000u);
+    } else {
+        v[0] = __uint_as_float(u);
     }
 }
 
-// P of token t, uniform over the wave.
-__device__ __forceinline__ void load_token_matrix(const float* __restrict__ P, int64_t t, float p[16]) {
-    const float* pt = P + 16 * t;
+// out_i = sum_j m_ij in_j over the E channels of one chunk of each of the N rows (TRANS:
+// m_ji, the transpose, read in place), one 32-bit word of the chunk at a time so that only
+// that word's channels are unpacked at once.
+template <int DX, int N, bool TRANS = false>
+__device__ __forceinline__ void mix_chunk(const float m[N * N], const v4u in[N], v4u out[N]) {
+    constexpr int EW = MixChunk<DX>::E / 4;
+    uint32_t o[N][4];
 #pragma unroll
-    for (int q = 0; q < 16; ++q) p[q] = pt[q];
+    for (int w = 0; w < 4; ++w) {
+        float x[N][EW];
+#pragma unroll
+        for (int j = 0; j < N; ++j) unpack_word<DX>(in[j], w, x[j]);
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            float y[EW];
+#pragma unroll
+            for (int e = 0; e < EW; ++e) {
+                y[e] = m[TRANS ? i : N * i] * x[0][e];
+#pragma unroll
+                for (int j = 1; j < N; ++j) y[e] = __builtin_fmaf(m[TRANS ? N * j + i : N * i + j], x[j][e], y[e]);
+            }
+            if constexpr (DX == BIRKHOFF4_BF16)
+                o[i][w] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{y[0], y[1]}), bf16x2));
+            else
+                o[i][w] = __float_as_uint(y[0]);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < N; ++i) out[i] = v4u{o[i][0], o[i][1], o[i][2], o[i][3]};
+}
+
+// P of token t (N x N), uniform over the wave.
+template <int N>
+__device__ __forceinline__ void load_token_matrix(const float* __restrict__ P, int64_t t, float p[N * N]) {
+    const float* pt = P + N * N * t;
+#pragma unroll
+    for (int q = 0; q < N * N; ++q) p[q] = pt[q];
 }
 
 // A wave walks the items (t, c0) of its tokens, c0 = 0, 64, 128, ... < nc: lane l handles
@@ -1088,7 +1114,7 @@ __device__ __forceinline__ void load_token_matrix(const float* __restrict__ P, i
 // that no register copy waits for them. Lanes past the end of a row take its last chunk:
 // they load, mix and store the same bytes as that chunk's own lane, so every memory
 // instruction is issued by the whole wave and the waits count exactly.
-template <int DX>
+template <int DX, int N>
 __global__ __launch_bounds__(kMixBlock) void mix_fwd_kernel(const float* __restrict__ P,
                                                              const v4u* __restrict__ X, v4u* __restrict__ Y,
                                                              int64_t B, int64_t nc) {
@@ -1100,17 +1126,17 @@ __global__ __launch_bounds__(kMixBlock) void mix_fwd_kernel(const float* __restr
     int64_t c0 = 0;
     auto offset = [&](int64_t tt, int64_t cc0) {
         const int64_t cc = cc0 + lane;
-        return 4 * nc * tt + (cc < nc ? cc : nc - 1);
+        return N * nc * tt + (cc < nc ? cc : nc - 1);
     };
-    auto load_item = [&](int64_t off, v4u v[4]) {
+    auto load_item = [&](int64_t off, v4u v[N]) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = __builtin_nontemporal_load(X + off + j * nc);
+        for (int j = 0; j < N; ++j) v[j] = __builtin_nontemporal_load(X + off + j * nc);
     };
-    float p[16];
-    load_token_matrix(P, t, p);
+    float p[N * N];
+    load_token_matrix<N>(P, t, p);
     // mix the item in `cur` while the next one (or, after the last, this one again) loads
     // into `nxt`
-    auto step = [&](const v4u cur[4], v4u nxt[4]) {
+    auto step = [&](const v4u cur[N], v4u nxt[N]) {
         int64_t tn = t, cn = c0 + 64;
         if (cn >= nc) {
             cn = 0;
@@ -1119,12 +1145,12 @@ __global__ __launch_bounds__(kMixBlock) void mix_fwd_kernel(const float* __restr
         const bool more = tn < B;
         load_item(more ? offset(tn, cn) : offset(t, c0), nxt);
         __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the waits for `cur`
-        v4u out[4];
-        mix_chunk<DX>(p, cur, out);
+        v4u out[N];
+        mix_chunk<DX, N>(p, cur, out);
         const int64_t off = offset(t, c0);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) __builtin_nontemporal_store(out[i], Y + off + i * nc);
-        if (more && tn != t) load_token_matrix(P, tn, p);
+        for (int i = 0; i < N; ++i) __builtin_nontemporal_store(out[i], Y + off + i * nc);
+        if (more && tn != t) load_token_matrix<N>(P, tn, p);
         t = tn;
         c0 = cn;
     };
@@ -1133,7 +1159,7 @@ __global__ __launch_bounds__(kMixBlock) void mix_fwd_kernel(const float* __restr
     // issued), and every path into a step leaves the same loads and stores in flight (so the
     // wait for `cur` does not cover the previous step's stores).
     const int64_t items = ((B - t + stride - 1) / stride) * ((nc + 63) >> 6);
-    v4u a[4], b[4];
+    v4u a[N], b[N];
     load_item(offset(t, 0), a);
     step(a, b);
     int64_t k = 1;
@@ -1149,6 +1175,23 @@ __global__ __launch_bounds__(kMixBlock) void mix_fwd_kernel(const float* __restr
 // its bit m and adds its partner's copy of that half, so after masks 32, 16, 8, 4 lane L
 // holds value (L >> 2) & 15 summed over the lanes that share its two low bits; two more
 // exchanges complete the sums (17 shuffles instead of 96).
+// The same exchange for 64 values: after masks 32 .. 1 lane L holds the wave's sum of
+// value L (63 shuffles).
+__device__ __forceinline__ float wave_sum64_own(float v[64], int lane) {
+#pragma unroll
+    for (int step = 0; step < 6; ++step) {
+        const int m = 32 >> step, n = 32 >> step;
+        const bool hi = (lane & m) != 0;
+#pragma unroll
+        for (int k = 0; k < n; ++k) {
+            const float send = hi ? v[k] : v[k + n];
+            const float keep = hi ? v[k + n] : v[k];
+            v[k] = keep + __shfl_xor(send, m);
+        }
+    }
+    return v[0];
+}
+
 __device__ __forceinline__ void wave_sum16(float v[16], int lane, float s[16]) {
 #pragma unroll
     for (int step = 0; step < 4; ++step) {
@@ -1171,7 +1214,7 @@ __device__ __forceinline__ void wave_sum16(float v[16], int lane, float s[16]) {
 // The same walk; a token's dP is summed over the wave when its last item is done, while
 // the next item's loads are in flight. Lanes past the end of a row zero their X words, so
 // that the chunk they repeat adds nothing to dP.
-template <int DX>
+template <int DX, int N>
 __global__ __launch_bounds__(kMixBlock) void mix_bwd_kernel(const float* __restrict__ P,
                                                              const v4u* __restrict__ X,
                                                              const v4u* __restrict__ dY, v4u* __restrict__ dX,
@@ -1182,31 +1225,31 @@ __global__ __launch_bounds__(kMixBlock) void mix_bwd_kernel(const float* __restr
     int64_t t = static_cast<int64_t>(blockIdx.x) * kMixWaves +
                 __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
     if (t >= B) return;
-    float p[16], pt[16], acc[16];  // acc: this lane's part of dP_ij = sum_c dY_i[c] X_j[c]
-    auto token_matrix = [&](int64_t tt) {
-        load_token_matrix(P, tt, p);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) pt[4 * j + i] = p[4 * i + j];
-    };
+    constexpr int NN = N * N;
+    float p[NN], acc[NN];  // acc: this lane's part of dP_ij = sum_c dY_i[c] X_j[c]
+    auto token_matrix = [&](int64_t tt) { load_token_matrix<N>(P, tt, p); };
     // dH of token t from the lanes' partial dP (uniform branch: every lane takes part)
+    // (n = 8: dP itself, lane L writing entry L, for the 8 x 8 backward to take over)
     auto finish_token = [&]() {
-        float G[16], out[16];
-        wave_sum16(acc, lane, G);
-        implicit_vjp(p, G, out);
-        if (lane < 4) {
-            const v4f row = lane == 0 ? v4f{out[0], out[1], out[2], out[3]}
-                          : lane == 1 ? v4f{out[4], out[5], out[6], out[7]}
-                          : lane == 2 ? v4f{out[8], out[9], out[10], out[11]}
-                                      : v4f{out[12], out[13], out[14], out[15]};
-            reinterpret_cast<v4f*>(dH)[4 * t + lane] = row;
+        if constexpr (N == 4) {
+            float G[16], out[16];
+            wave_sum16(acc, lane, G);
+            implicit_vjp(p, G, out);
+            if (lane < 4) {
+                const v4f row = lane == 0 ? v4f{out[0], out[1], out[2], out[3]}
+                              : lane == 1 ? v4f{out[4], out[5], out[6], out[7]}
+                              : lane == 2 ? v4f{out[8], out[9], out[10], out[11]}
+                                          : v4f{out[12], out[13], out[14], out[15]};
+                reinterpret_cast<v4f*>(dH)[4 * t + lane] = row;
+            }
+        } else {
+            dH[64 * t + lane] = wave_sum64_own(acc, lane);
         }
 #pragma unroll
-        for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+        for (int q = 0; q < NN; ++q) acc[q] = 0.f;
     };
 #pragma unroll
-    for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+    for (int q = 0; q < NN; ++q) acc[q] = 0.f;
     token_matrix(t);
     if (nc == 0) {  // no channels: dP = 0 (uniform)
         for (;;) {
@@ -1219,60 +1262,91 @@ __global__ __launch_bounds__(kMixBlock) void mix_bwd_kernel(const float* __restr
     int64_t c0 = 0;
     auto offset = [&](int64_t tt, int64_t cc0) {
         const int64_t cc = cc0 + lane;
-        return 4 * nc * tt + (cc < nc ? cc : nc - 1);
+        return N * nc * tt + (cc < nc ? cc : nc - 1);
     };
-    auto load_item = [&](int64_t off, v4u x[4], v4u g[4]) {
+    auto load_item = [&](int64_t off, v4u x[N], v4u g[N]) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < N; ++j) {
             x[j] = __builtin_nontemporal_load(X + off + j * nc);
             g[j] = __builtin_nontemporal_load(dY + off + j * nc);
         }
     };
-    auto step = [&](const v4u xc[4], const v4u gc[4], v4u xn[4], v4u gn[4]) {
-        int64_t tn = t, cn = c0 + 64;
-        if (cn >= nc) {
-            cn = 0;
-            tn = t + stride;
-        }
-        const bool more = tn < B;
-        load_item(more ? offset(tn, cn) : offset(t, c0), xn, gn);
-        __builtin_amdgcn_sched_barrier(0);
-        v4u o[4];
-        mix_chunk<DX>(pt, gc, o);
+    // dX of the item in (xc, gc) and its part of dP
+    auto process = [&](const v4u xc[N], const v4u gc[N]) {
+        v4u o[N];
+        mix_chunk<DX, N, true>(p, gc, o);
         const int64_t off = offset(t, c0);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) __builtin_nontemporal_store(o[j], dX + off + j * nc);
+        for (int j = 0; j < N; ++j) __builtin_nontemporal_store(o[j], dX + off + j * nc);
         const bool own = c0 + lane < nc;
-        float xv[4][E], gv[4][E];
+        constexpr int EW = E / 4;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            unpack_chunk<DX>(own ? xc[j] : v4u{0u, 0u, 0u, 0u}, xv[j]);
-            unpack_chunk<DX>(gc[j], gv[j]);
+        for (int w = 0; w < 4; ++w) {  // one 32-bit word of the chunk at a time
+            float xv[N][EW], gv[N][EW];
+#pragma unroll
+            for (int j = 0; j < N; ++j) {
+                unpack_word<DX>(own ? xc[j] : v4u{0u, 0u, 0u, 0u}, w, xv[j]);
+                unpack_word<DX>(gc[j], w, gv[j]);
+            }
+#pragma unroll
+            for (int i = 0; i < N; ++i)
+#pragma unroll
+                for (int j = 0; j < N; ++j)
+#pragma unroll
+                    for (int e = 0; e < EW; ++e)
+                        acc[N * i + j] = __builtin_fmaf(gv[i][e], xv[j][e], acc[N * i + j]);
         }
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-#pragma unroll
-                for (int e = 0; e < E; ++e) acc[4 * i + j] = __builtin_fmaf(gv[i][e], xv[j][e], acc[4 * i + j]);
-        if (tn != t) {
-            finish_token();
-            if (more) token_matrix(tn);
-        }
-        t = tn;
-        c0 = cn;
     };
-    // peeled first step and counted loop of two, as in the forward
     const int64_t items = ((B - t + stride - 1) / stride) * ((nc + 63) >> 6);
-    v4u xa[4], ga[4], xb[4], gb[4];
-    load_item(offset(t, 0), xa, ga);
-    step(xa, ga, xb, gb);
-    int64_t k = 1;
-    for (; k + 2 <= items; k += 2) {
-        step(xb, gb, xa, ga);
+    if constexpr (N == 4) {
+        // process the item in (xc, gc) while the next one loads into (xn, gn)
+        auto step = [&](const v4u xc[N], const v4u gc[N], v4u xn[N], v4u gn[N]) {
+            int64_t tn = t, cn = c0 + 64;
+            if (cn >= nc) {
+                cn = 0;
+                tn = t + stride;
+            }
+            const bool more = tn < B;
+            load_item(more ? offset(tn, cn) : offset(t, c0), xn, gn);
+            __builtin_amdgcn_sched_barrier(0);
+            process(xc, gc);
+            if (tn != t) {
+                finish_token();
+                if (more) token_matrix(tn);
+            }
+            t = tn;
+            c0 = cn;
+        };
+        // peeled first step and counted loop of two, as in the forward
+        v4u xa[N], ga[N], xb[N], gb[N];
+        load_item(offset(t, 0), xa, ga);
         step(xa, ga, xb, gb);
+        int64_t k = 1;
+        for (; k + 2 <= items; k += 2) {
+            step(xb, gb, xa, ga);
+            step(xa, ga, xb, gb);
+        }
+        if (k < items) step(xb, gb, xa, ga);
+    } else {
+        // n = 8: the 64 partial sums leave no room for a second buffer at two waves per SIMD
+        // (with it: one wave per SIMD, measured the same; forced to two waves: spills, slower)
+        for (int64_t k = 0; k < items; ++k) {
+            v4u x[N], g[N];
+            load_item(offset(t, c0), x, g);
+            process(x, g);
+            int64_t tn = t, cn = c0 + 64;
+            if (cn >= nc) {
+                cn = 0;
+                tn = t + stride;
+            }
+            if (tn != t) {
+                finish_token();
+                if (tn < B) token_matrix(tn);
+            }
+            t = tn;
+            c0 = cn;
+        }
     }
-    if (k < items) step(xb, gb, xa, ga);
 }
 
 // ---------------------------------------------------------------------------
@@ -2907,19 +2981,19 @@ int64_t grid_for(int64_t B, int block, int cus, int per_cu) {
 }
 
 // Residual mixing: one token per wave at a time, grid-stride over the tokens.
-template <int DX>
+template <int DX, int N = 4>
 int launch_mix_fwd(const float* P, const void* X, void* Y, int64_t B, int64_t nc, hipStream_t stream, int cus) {
     const int64_t grid = grid_for(B, kMixWaves, cus, kMixPerCu);
-    hipLaunchKernelGGL((mix_fwd_kernel<DX>), dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
+    hipLaunchKernelGGL((mix_fwd_kernel<DX, N>), dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
                        static_cast<const v4u*>(X), static_cast<v4u*>(Y), B, nc);
     return launch_status();
 }
 
-template <int DX>
+template <int DX, int N = 4>
 int launch_mix_bwd(const float* P, const void* X, const void* dY, void* dX, float* dH, int64_t B, int64_t nc,
                    hipStream_t stream, int cus) {
     const int64_t grid = grid_for(B, kMixWaves, cus, kMixPerCu);
-    hipLaunchKernelGGL((mix_bwd_kernel<DX>), dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
+    hipLaunchKernelGGL((mix_bwd_kernel<DX, N>), dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
                        static_cast<const v4u*>(X), static_cast<const v4u*>(dY), static_cast<v4u*>(dX), dH, B, nc);
     return launch_status();
 }
@@ -3250,7 +3324,9 @@ int birkhoff4_mix_fwd(const void* H, int h_dtype, const void* X, int x_dtype, vo
                  ni = iters ? static_cast<size_t>(B) * 4 : 0;
     if (overlaps(Y, nx, H, nh) || overlaps(Y, nx, X, nx) || overlaps(Y, nx, P, np) || overlaps(Y, nx, dual, nd) ||
         overlaps(Y, nx, iters, ni) || overlaps(P, np, X, nx) || overlaps(dual, nd, X, nx) ||
-        overlaps(iters, ni, X, nx))
+        overlaps(iters, ni, X, nx) || overlaps(H, nh, P, np) || overlaps(H, nh, dual, nd) ||
+        overlaps(H, nh, iters, ni) || overlaps(P, np, dual, nd) || overlaps(P, np, iters, ni) ||
+        overlaps(dual, nd, iters, ni))
         return BIRKHOFF4_ERR_OVERLAP;
     int cus = 0;
     if (int e = device_cus(&cus)) return e;
@@ -3281,6 +3357,68 @@ int birkhoff4_mix_bwd(const float* P, const void* X, const void* dY, int x_dtype
     if (int e = device_cus(&cus)) return e;
     if (x_dtype == BIRKHOFF4_BF16) return launch_mix_bwd<BIRKHOFF4_BF16>(P, X, dY, dX, dH, B, nc, stream, cus);
     return launch_mix_bwd<BIRKHOFF4_F32>(P, X, dY, dX, dH, B, nc, stream, cus);
+}
+
+int birkhoff8_mix_fwd(const void* H, int h_dtype, const void* X, int x_dtype, void* Y, float* P, float* dual,
+                      int32_t* iters, int64_t B, int64_t C, float tol, int max_iter, hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 256)) return BIRKHOFF4_ERR_SIZE;
+    if (!dtype_ok(h_dtype) || !dtype_ok(x_dtype)) return BIRKHOFF4_ERR_DTYPE;
+    const int64_t E = x_dtype == BIRKHOFF4_BF16 ? 8 : 4;
+    if (C < 0 || C % E != 0) return BIRKHOFF4_ERR_CHANNELS;
+    const int64_t nc = C / E;  // 16-byte chunks per row
+    if (B > 0 && nc > INT64_MAX / 128 / B) return BIRKHOFF4_ERR_SIZE;
+    if (!(tol >= 0.f)) return BIRKHOFF4_ERR_TOL;
+    if (max_iter < 0 || max_iter > kMaxIterCap) return BIRKHOFF4_ERR_MAX_ITER;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!H || !P || (nc > 0 && (!X || !Y))) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(H) || misaligned(X) || misaligned(Y) || misaligned(P) || misaligned(dual) || misaligned(iters))
+        return BIRKHOFF4_ERR_ALIGN;
+    const size_t nh = static_cast<size_t>(B) * 64 * dtype_bytes(h_dtype), nx = static_cast<size_t>(B) * 128 * nc;
+    const size_t np = static_cast<size_t>(B) * 256, nd = dual ? static_cast<size_t>(B) * 64 : 0,
+                 ni = iters ? static_cast<size_t>(B) * 4 : 0;
+    if (overlaps(Y, nx, H, nh) || overlaps(Y, nx, X, nx) || overlaps(Y, nx, P, np) || overlaps(Y, nx, dual, nd) ||
+        overlaps(Y, nx, iters, ni) || overlaps(P, np, X, nx) || overlaps(dual, nd, X, nx) ||
+        overlaps(iters, ni, X, nx) || overlaps(H, nh, P, np) || overlaps(H, nh, dual, nd) ||
+        overlaps(H, nh, iters, ni) || overlaps(P, np, dual, nd) || overlaps(P, np, iters, ni) ||
+        overlaps(dual, nd, iters, ni))
+        return BIRKHOFF4_ERR_OVERLAP;
+    int cus = 0;
+    if (int e = device_cus(&cus)) return e;
+    if (int e = birkhoff8_fwd(H, h_dtype, P, dual, iters, B, tol, max_iter, stream)) return e;
+    if (nc == 0) return BIRKHOFF4_OK;
+    if (x_dtype == BIRKHOFF4_BF16) return launch_mix_fwd<BIRKHOFF4_BF16, 8>(P, X, Y, B, nc, stream, cus);
+    return launch_mix_fwd<BIRKHOFF4_F32, 8>(P, X, Y, B, nc, stream, cus);
+}
+
+int birkhoff8_mix_bwd(const float* P, const void* X, const void* dY, int x_dtype, void* dX, float* dH, int64_t B,
+                      int64_t C, hipStream_t stream) {
+    if (B < 0 || B > (INT64_MAX / 256)) return BIRKHOFF4_ERR_SIZE;
+    if (!dtype_ok(x_dtype)) return BIRKHOFF4_ERR_DTYPE;
+    const int64_t E = x_dtype == BIRKHOFF4_BF16 ? 8 : 4;
+    if (C < 0 || C % E != 0) return BIRKHOFF4_ERR_CHANNELS;
+    const int64_t nc = C / E;
+    if (B > 0 && nc > INT64_MAX / 128 / B) return BIRKHOFF4_ERR_SIZE;
+    if (B == 0) return BIRKHOFF4_OK;
+    if (!P || !dH || (nc > 0 && (!X || !dY || !dX))) return BIRKHOFF4_ERR_NULL;
+    if (misaligned(P) || misaligned(X) || misaligned(dY) || misaligned(dX) || misaligned(dH))
+        return BIRKHOFF4_ERR_ALIGN;
+    const size_t np = static_cast<size_t>(B) * 256, nx = static_cast<size_t>(B) * 128 * nc;
+    if (overlaps(dX, nx, P, np) || overlaps(dX, nx, X, nx) || overlaps(dX, nx, dY, nx) || overlaps(dX, nx, dH, np) ||
+        overlaps(dH, np, P, np) || overlaps(dH, np, X, nx) || overlaps(dH, np, dY, nx))
+        return BIRKHOFF4_ERR_OVERLAP;
+    int cus = 0;
+    if (int e = device_cus(&cus)) return e;
+    // dX, and dP into dH's memory; then the 8 x 8 backward turns dP into dH in place (each of
+    // its waves reads a chunk's dP whole before it writes that chunk's dH)
+    const int e = x_dtype == BIRKHOFF4_BF16 ? launch_mix_bwd<BIRKHOFF4_BF16, 8>(P, X, dY, dX, dH, B, nc, stream, cus)
+                                            : launch_mix_bwd<BIRKHOFF4_F32, 8>(P, X, dY, dX, dH, B, nc, stream, cus);
+    if (e) return e;
+    const int64_t chunks = (B + 63) / 64;
+    const int64_t want = (chunks + kB8Waves - 1) / kB8Waves;
+    const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
+    hipLaunchKernelGGL((implicit8_bwd_kernel<BIRKHOFF4_F32, false>), dim3(static_cast<unsigned>(grid)),
+                       dim3(kB8Block), 0, stream, P, dH, dH, B, nullptr, 1.f);
+    return launch_status();
 }
 
 const char* birkhoff4_strerror(int code) {

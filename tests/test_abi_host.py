@@ -234,6 +234,8 @@ def test_mix_argument_errors():
     assert f(A, F32, Bp, BF, Bp + 16, D, None, None, 5, 64, 1e-6, 20, None) == ERR_OVERLAP   # Y inside X
     assert f(A, F32, Bp, BF, C, Bp + 64, None, None, 5, 64, 1e-6, 20, None) == ERR_OVERLAP   # P inside X
     assert f(A, F32, Bp, BF, C, D, C + 32, None, 5, 64, 1e-6, 20, None) == ERR_OVERLAP      # dual inside Y
+    assert f(A, F32, Bp, BF, C, D, D + 32, None, 5, 64, 1e-6, 20, None) == ERR_OVERLAP      # dual inside P
+    assert f(A, F32, Bp, BF, C, A + 16, None, None, 5, 64, 1e-6, 20, None) == ERR_OVERLAP   # P inside H
     g = lib.birkhoff4_mix_bwd  # (P, X, dY, x_dtype, dX, dH, B, C, stream)
     assert g(A, Bp, C, BF, D, E, 0, 64, None) == OK
     assert g(A, Bp, C, BF, D, E, 5, 60, None) == ERR_CHANNELS
@@ -244,3 +246,19 @@ def test_mix_argument_errors():
     assert g(A, Bp, C, BF, C + 256, E, 5, 64, None) == ERR_OVERLAP    # dX inside dY
     assert g(A, Bp, C, BF, D, A + 64, 5, 64, None) == ERR_OVERLAP     # dH inside P
     assert g(A, Bp, C, BF, D, Bp + 128, 5, 64, None) == ERR_OVERLAP   # dH inside X
+
+
+def test_mix8_argument_errors():
+    lib = b4.lib()
+    f = lib.birkhoff8_mix_fwd
+    BF, F32 = b4.BF16, b4.F32
+    assert f(A, F32, Bp, BF, C, D, None, None, 0, 64, 1e-6, 20, None) == OK
+    assert f(A, F32, Bp, BF, C, D, None, None, 5, 12, 1e-6, 20, None) == ERR_CHANNELS
+    assert f(A, F32, None, BF, C, D, None, None, 5, 64, 1e-6, 20, None) == ERR_NULL
+    assert f(A, F32, Bp, BF, Bp + 128 * 8, D, None, None, 5, 64, 1e-6, 20, None) == ERR_OVERLAP  # Y inside X
+    assert f(A, F32, Bp, BF, C, D, D + 256, None, 5, 64, 1e-6, 20, None) == ERR_OVERLAP           # dual inside P
+    g = lib.birkhoff8_mix_bwd
+    assert g(A, Bp, C, BF, D, E, 0, 64, None) == OK
+    assert g(A, Bp, C, BF, D, E, 5, 4, None) == ERR_CHANNELS
+    assert g(A, Bp, C, BF, D, A + 256, 5, 64, None) == ERR_OVERLAP    # dH inside P
+    assert g(A, Bp, C, BF, D + 4, E, 5, 64, None) == ERR_ALIGN

@@ -137,13 +137,15 @@ def test_graph_many_launches():
     graph_roundtrip(fn, sets, "16 pairs")
 
 
-def test_graph_mix():
-    say("test: graph capture of the residual-mixing pair")
-    sets = [list(workloads.mix_streams_device(3001, 264, 70 + k, "cuda")) for k in range(N_SETS)]
+@pytest.mark.parametrize("n", [4, 8])
+def test_graph_mix(n):
+    say(f"test: graph capture of the residual-mixing pair, {n} streams")
+    sets = [list(workloads.mix_streams_device(3001, 264, 70 + k, "cuda", n)) for k in range(N_SETS)]
+    mfwd, mbwd = (b4.mix_fwd, b4.mix_bwd) if n == 4 else (b4.mix8_fwd, b4.mix8_bwd)
 
     def fn(H, X, G):
-        Y, P, _, it = b4.mix_fwd(H, X, 1e-6, 64, want_iters=True)
-        dX, dH = b4.mix_bwd(P, X, G)
+        Y, P, _, it = mfwd(H, X, 1e-6, 64, want_iters=True)
+        dX, dH = mbwd(P, X, G)
         return Y, P, it, dX, dH
 
     graph_roundtrip(fn, sets, "mix")

@@ -43,10 +43,12 @@ def mixed_bound(P_err, inputs, out_ref, bf16):
 
 def check_case(H, X, G, dtype, label, h_dtype=torch.float32):
     bf16 = dtype == torch.bfloat16
+    n = H.shape[-1]
+    mfwd, mbwd = (b4.mix_fwd, b4.mix_bwd) if n == 4 else (b4.mix8_fwd, b4.mix8_bwd)
     Hd, Xd, Gd = to_dev(H, h_dtype), to_dev(X, dtype), to_dev(G, dtype)
-    Y, P, _, it = b4.mix_fwd(Hd, Xd, want_iters=True)
-    dX, dH = b4.mix_bwd(P, Xd, Gd)
-    P_alone, _, _ = b4.fwd(Hd, want_dual=False)
+    Y, P, _, it = mfwd(Hd, Xd, want_iters=True)
+    dX, dH = mbwd(P, Xd, Gd)
+    P_alone, _, _ = (b4.fwd if n == 4 else b4.fwd8)(Hd, want_dual=False)
     torch.cuda.synchronize()
     assert torch.equal(P, P_alone), f"{label}: P differs from the projection's own"
     assert (it.cpu().numpy() >= 0).all()
@@ -203,3 +205,37 @@ def test_beyond_32bit_offsets():
     e = np.abs(dH[ti].cpu().numpy() - dHr).max(axis=(1, 2)) / np.maximum(1.0, np.abs(dHr).max(axis=(1, 2)))
     say(f"  sample of {len(idx)}: Y err/bound={ey.max():.3f} dX err/bound={ex.max():.3f} dH rel={e.max():.2e}")
     assert ey.max() <= 1.0 and ex.max() <= 1.0 and e.max() <= TOL_DH
+
+
+
+CASES8 = [(1, 8, torch.bfloat16, 1.0), (9, 40, torch.float32, 5.0), (300, 520, torch.bfloat16, 5.0),
+          (1000, 4096, torch.bfloat16, 20.0), (2049, 1028, torch.float32, 1.0), (64, 0, torch.bfloat16, 5.0)]
+
+
+@pytest.mark.parametrize("B,C,dtype,sigma", CASES8,
+                         ids=[f"B{b}-C{c}-{str(d)[6:]}-s{s:g}" for b, c, d, s in CASES8])
+def test_parity_8_streams(B, C, dtype, sigma):
+    say(f"test: 8-stream mix parity B={B} C={C} {dtype} sigma={sigma}")
+    H = sigma * np.random.default_rng(B + C + 1).standard_normal((B, 8, 8), dtype=np.float32)
+    rng = np.random.default_rng(np.random.SeedSequence([B, C, 88]))
+    X = rng.standard_normal((B, 8, C), dtype=np.float32)
+    G = rng.standard_normal((B, 8, C), dtype=np.float32)
+    if dtype == torch.bfloat16:
+        X = workloads.bf16_to_f32(workloads.bf16_bits(X))
+        G = workloads.bf16_to_f32(workloads.bf16_bits(G))
+    check_case(H, X, G, dtype, f"n=8 B={B} C={C}")
+
+
+def test_8_streams_autograd_and_workload():
+    say("test: 8-stream mix autograd on the mixture workload")
+    H, X, G = workloads.mix_streams_device(3000, 256, 62, "cuda", n=8)
+    Hr = H.float().requires_grad_()
+    Xr = X.clone().requires_grad_()
+    Y = b4.mix(Hr, Xr)
+    (Y.float() * G.float()).sum().backward()
+    Y2, P, _, _ = b4.mix8_fwd(H.float(), X)
+    dX, dH = b4.mix8_bwd(P, X, G)
+    torch.cuda.synchronize()
+    assert torch.equal(Y, Y2) and torch.equal(Hr.grad, dH) and torch.equal(Xr.grad, dX)
+    check_case(H.float().cpu().numpy(), X.float().cpu().numpy(), G.float().cpu().numpy(), torch.bfloat16,
+               "n=8 mixture")

@@ -116,3 +116,53 @@ def test_finite_differences(sigma):
     scale = np.maximum(1.0, np.abs(fdH).max(axis=(1, 2)))
     assert (np.abs(dH - fdH).max(axis=(1, 2)) / scale).max() < 1e-7
     assert np.abs(dX - fdX).max() < 1e-8
+
+
+# n = 8 streams (the size-generic projection oracle)
+def _logits8(B, sigma, seed):
+    return sigma * np.random.default_rng(seed).standard_normal((B, 8, 8))
+
+
+def test_n8_structure():
+    H = _logits8(40, 5.0, 20)
+    rng = np.random.default_rng(21)
+    v = rng.standard_normal((40, 1, 6))
+    Y, _ = mix_fwd(H, np.repeat(v, 8, axis=1))
+    assert np.abs(Y - v).max() < 1e-11                       # unit row sums
+    X = rng.standard_normal((40, 8, 6))
+    Y, P = mix_fwd(H, X)
+    assert np.abs(Y.sum(axis=1) - X.sum(axis=1)).max() < 1e-11  # unit column sums
+    Hs = rng.standard_normal((10, 8, 1)) + rng.standard_normal((10, 1, 8))
+    Ys, _ = mix_fwd(Hs, X[:10])
+    assert np.abs(Ys - X[:10].mean(axis=1, keepdims=True)).max() < 1e-12
+    G = rng.standard_normal((40, 8, 6))
+    dX, _ = mix_bwd(P, X, G)
+    assert np.abs((G * Y).sum(axis=(1, 2)) - (dX * X).sum(axis=(1, 2))).max() < 1e-12
+
+
+def test_n8_finite_differences():
+    B, C = 3, 2
+    H = _logits8(B, 2.0, 22)
+    rng = np.random.default_rng(23)
+    X = rng.standard_normal((B, 8, C))
+    G = rng.standard_normal((B, 8, C))
+    _, P = mix_fwd(H, X, tol=1e-14)
+    dX, dH = mix_bwd(P, X, G)
+    h = 1e-5
+
+    def loss(Hh, Xx):
+        Y, _ = mix_fwd(Hh, Xx, tol=1e-14)
+        return (G * Y).sum(axis=(1, 2))
+    fdH = np.zeros_like(H)
+    for k in range(64):
+        E = np.zeros((8, 8))
+        E[divmod(k, 8)] = h
+        fdH[:, k // 8, k % 8] = (loss(H + E, X) - loss(H - E, X)) / (2 * h)
+    fdX = np.zeros_like(X)
+    for k in range(8 * C):
+        E = np.zeros((8, C))
+        E[divmod(k, C)] = h
+        fdX[:, k // C, k % C] = (loss(H, X + E) - loss(H, X - E)) / (2 * h)
+    scale = np.maximum(1.0, np.abs(fdH).max(axis=(1, 2)))
+    assert (np.abs(dH - fdH).max(axis=(1, 2)) / scale).max() < 1e-7
+    assert np.abs(dX - fdX).max() < 1e-8

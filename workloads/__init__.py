@@ -233,20 +233,21 @@ def ot_device(B: int, seed: int, dev, n: int = 4):
     return M.contiguous(), a.contiguous(), b.contiguous(), G.contiguous()
 
 
-def mix_streams_device(B: int, C: int, seed: int, dev):
-    """Residual mixing of the mHC layer: per token, 4x4 logits H from the headline mixture
-    (half sigma * N(0,1) with sigma drawn from {1, 5, 20}, half 20 Pi + 0.1 N(0,1), kinds
-    shuffled) and 4 streams of C channels X ~ N(0,1), with upstream gradient dY ~ N(0,1) of
-    the same shape; all stored as bf16. Returns (H [B,4,4], X [B,4,C], dY [B,4,C]) on ``dev``."""
+def mix_streams_device(B: int, C: int, seed: int, dev, n: int = 4):
+    """Residual mixing of the mHC layer: per token, n x n logits H from the headline mixture
+    (half sigma * N(0,1) with sigma drawn from {1, 5, 20}, half 20 Pi + 0.1 N(0,1) for a
+    random permutation Pi, kinds shuffled) and n streams of C channels X ~ N(0,1), with
+    upstream gradient dY ~ N(0,1) of the same shape; all stored as bf16. Returns
+    (H [B,n,n], X [B,n,C], dY [B,n,C]) on ``dev``."""
     import torch
     g = torch.Generator(device=dev)
     g.manual_seed(seed)
-    Z = torch.randn(B, 4, 4, device=dev, generator=g)
+    Z = torch.randn(B, n, n, device=dev, generator=g)
     kind = torch.randint(0, 2, (B,), device=dev, generator=g)
     sig = torch.tensor([1.0, 5.0, 20.0], device=dev)[torch.randint(0, 3, (B,), device=dev, generator=g)]
-    perm = torch.argsort(torch.rand(B, 4, device=dev, generator=g), dim=1)
-    Pi = torch.zeros(B, 4, 4, device=dev).scatter_(2, perm[:, :, None], 1.0)
+    perm = torch.argsort(torch.rand(B, n, device=dev, generator=g), dim=1)
+    Pi = torch.zeros(B, n, n, device=dev).scatter_(2, perm[:, :, None], 1.0)
     H = torch.where(kind[:, None, None] == 0, sig[:, None, None] * Z, 20.0 * Pi + 0.1 * Z)
-    X = torch.randn(B, 4, C, device=dev, generator=g).to(torch.bfloat16)
-    G = torch.randn(B, 4, C, device=dev, generator=g).to(torch.bfloat16)
+    X = torch.randn(B, n, C, device=dev, generator=g).to(torch.bfloat16)
+    G = torch.randn(B, n, C, device=dev, generator=g).to(torch.bfloat16)
     return H.to(torch.bfloat16).contiguous(), X.contiguous(), G.contiguous()
