@@ -1176,20 +1176,28 @@ __global__ __launch_bounds__(kMixBlock) void mix_fwd_kernel(const float* __restr
 // holds value (L >> 2) & 15 summed over the lanes that share its two low bits; two more
 // exchanges complete the sums (17 shuffles instead of 96).
 // The same exchange for 64 values: after masks 32 .. 1 lane L holds the wave's sum of
-// value L (63 shuffles).
-__device__ __forceinline__ float wave_sum64_own(float v[64], int lane) {
+// value L (63 shuffles). Each step writes a new array of half the size, so that every value
+// stays in a register.
+template <int M>
+__device__ __forceinline__ void halve_step(const float (&v)[2 * M], float (&h)[M], int lane) {
+    const bool hi = (lane & M) != 0;
 #pragma unroll
-    for (int step = 0; step < 6; ++step) {
-        const int m = 32 >> step, n = 32 >> step;
-        const bool hi = (lane & m) != 0;
-#pragma unroll
-        for (int k = 0; k < n; ++k) {
-            const float send = hi ? v[k] : v[k + n];
-            const float keep = hi ? v[k + n] : v[k];
-            v[k] = keep + __shfl_xor(send, m);
-        }
+    for (int k = 0; k < M; ++k) {
+        const float send = hi ? v[k] : v[k + M];
+        const float keep = hi ? v[k + M] : v[k];
+        h[k] = keep + __shfl_xor(send, M);
     }
-    return v[0];
+}
+
+__device__ __forceinline__ float wave_sum64_own(const float (&v)[64], int lane) {
+    float a[32], b[16], c[8], d[4], e[2], f[1];
+    halve_step<32>(v, a, lane);
+    halve_step<16>(a, b, lane);
+    halve_step<8>(b, c, lane);
+    halve_step<4>(c, d, lane);
+    halve_step<2>(d, e, lane);
+    halve_step<1>(e, f, lane);
+    return f[0];
 }
 
 __device__ __forceinline__ void wave_sum16(float v[16], int lane, float s[16]) {
