@@ -1337,7 +1337,6 @@ __global__ __launch_bounds__(kMixBlock) void mix_bwd_kernel(const float* __restr
         if (k < items) step(xb, gb, xa, ga);
     } else {
         // n = 8: the 64 partial sums leave no room for a second buffer at two waves per SIMD
-        // (with it: one wave per SIMD, measured the same; forced to two waves: spills, slower)
         for (int64_t k = 0; k < items; ++k) {
             v4u x[N], g[N];
             load_item(offset(t, c0), x, g);
