@@ -55,6 +55,8 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <tuple>
+#include <type_traits>
 
 #include "birkhoff4.h"
 
@@ -2223,10 +2225,16 @@ constexpr int kB8Stride = 17;  // v4f per problem in the LDS tile
 // With OT it is the backward of 8 x 8 entropic OT (eq. derivative): P is the solution T, av
 // the row marginal, dP = dL/dT (fp32) and dH = dL/dM; weights and flows carry 1/a_i, and
 // dM_ij = -T_ij (psi_ij - sum_k T_ik psi_ik / a_i) / eta.
-template <int DT, bool OT>
+// IN_PLACE: dP and dH are the same memory (the 8-stream mixing backward forms dP in dH's
+// buffer); they are then not declared non-aliasing. Each wave reads a chunk's dP whole into
+// LDS before it writes that chunk's dH, so the in-place update is safe.
+template <bool IN_PLACE, typename T>
+using MaybeRestrict = std::conditional_t<IN_PLACE, T*, T* __restrict__>;
+
+template <int DT, bool OT, bool IN_PLACE = false>
 __global__ __launch_bounds__(kB8Block, 2) void implicit8_bwd_kernel(const float* __restrict__ P,
-                                                                     const void* __restrict__ dP,
-                                                                     float* __restrict__ dH, int64_t B,
+                                                                     MaybeRestrict<IN_PLACE, const void> dP,
+                                                                     MaybeRestrict<IN_PLACE, float> dH, int64_t B,
                                                                      const float* __restrict__ av, float eta) {
     __shared__ v4f tile_all[kB8Waves][64 * kB8Stride];
     const int lane = threadIdx.x & 63;
@@ -2835,9 +2843,11 @@ __global__ __launch_bounds__(kOtBlock) void ot4_bwd_kernel(const float* __restri
 constexpr int kMaxDevices = 64;
 int g_cus[kMaxDevices];  // cached compute-unit counts (0 = not queried yet)
 
-int device_cus(int* cus) {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return BIRKHOFF4_ERR_DEVICE;
+// Compute units of the device that `stream` belongs to (the null stream: the current device).
+int device_cus(hipStream_t stream, int* cus, int* dev_out = nullptr) {
+    hipDevice_t dev = 0;
+    if (hipStreamGetDevice(stream, &dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return BIRKHOFF4_ERR_DEVICE;
     if (g_cus[dev] == 0) {
         int n = 0;
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
@@ -2845,6 +2855,7 @@ int device_cus(int* cus) {
         g_cus[dev] = n;
     }
     *cus = g_cus[dev];
+    if (dev_out) *dev_out = dev;
     return BIRKHOFF4_OK;
 }
 
@@ -2859,37 +2870,60 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 size_t dtype_bytes(int dt) { return dt == BIRKHOFF4_BF16 ? 2 : 4; }
 bool dtype_ok(int dt) { return dt == BIRKHOFF4_F32 || dt == BIRKHOFF4_BF16; }
 
+// Status of the launches made by this thread since the last call: taken from each launch's
+// own return value, so an error left pending by someone else's earlier launch is neither
+// reported as ours nor cleared.
+thread_local int t_launch = BIRKHOFF4_OK;
+
+template <typename... KArgs, typename... Args>
+void launch_kernel(void (*kern)(KArgs...), dim3 grid, dim3 block, unsigned lds, hipStream_t stream, Args... args) {
+    static_assert(sizeof...(KArgs) == sizeof...(Args), "kernel argument count");
+    std::tuple<KArgs...> vals(args...);
+    void* ptrs[sizeof...(KArgs)];
+    std::apply([&](auto&... v) {
+        int k = 0;
+        ((ptrs[k++] = static_cast<void*>(&v)), ...);
+    }, vals);
+    if (hipLaunchKernel(reinterpret_cast<const void*>(kern), grid, block, ptrs, lds, stream) != hipSuccess &&
+        t_launch == BIRKHOFF4_OK)
+        t_launch = BIRKHOFF4_ERR_LAUNCH;
+}
+
 int launch_status() {
-    return hipGetLastError() == hipSuccess ? BIRKHOFF4_OK : BIRKHOFF4_ERR_LAUNCH;
+    const int r = t_launch;
+    t_launch = BIRKHOFF4_OK;
+    return r;
 }
 
 // Blocks of the forward kernel resident at once on one CU (VGPR-limited),
 // from the occupancy calculator; queried once per instantiation.
 template <int DT, bool WD, bool WI, bool WH>
-int fwd_blocks_per_cu() {
-    static int cached = 0;
-    if (cached == 0) {
-        int nb = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, newton_fwd_kernel<DT, WD, WI, WH>, kFwdBlock, 0) !=
+int fwd_blocks_per_cu(int dev) {
+    static int cached[kMaxDevices];
+    if (cached[dev] == 0) {
+        int nb = 0, cur = 0;
+        // the occupancy calculator answers for the current device
+        if (hipGetDevice(&cur) != hipSuccess || cur != dev ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, newton_fwd_kernel<DT, WD, WI, WH>, kFwdBlock, 0) !=
                 hipSuccess || nb <= 0)
             nb = 1;
-        cached = nb;
+        cached[dev] = nb;
     }
-    return cached;
+    return cached[dev];
 }
 
 // Launch one resident workgroup per CU (as many as the occupancy calculator allows),
 // each owning a contiguous range of whole 64-problem batches that its waves share.
 template <int DT, bool WD, bool WI, bool WH = false>
 int launch_fwd(const void* H, float* P, float* dual, int32_t* iters, int64_t B, float tol,
-               int max_iter, hipStream_t stream, int cus, float* hess = nullptr) {
+               int max_iter, hipStream_t stream, int cus, int dev, float* hess = nullptr) {
     const int64_t batches = (B + 63) / 64;
-    int64_t blocks = static_cast<int64_t>(cus) * fwd_blocks_per_cu<DT, WD, WI, WH>();
+    int64_t blocks = static_cast<int64_t>(cus) * fwd_blocks_per_cu<DT, WD, WI, WH>(dev);
     if (blocks > batches) blocks = batches;
     const int64_t chunk = ((batches + blocks - 1) / blocks) * 64;
     if (chunk > INT32_MAX / 2) return BIRKHOFF4_ERR_SIZE;  // problems are 32-bit offsets in a range
     blocks = (B + chunk - 1) / chunk;
-    hipLaunchKernelGGL((newton_fwd_kernel<DT, WD, WI, WH>), dim3(static_cast<unsigned>(blocks)),
+    launch_kernel((newton_fwd_kernel<DT, WD, WI, WH>), dim3(static_cast<unsigned>(blocks)),
                        dim3(kFwdBlock), 0, stream, H, P, dual, iters, hess, B, chunk, tol, max_iter);
     return launch_status();
 }
@@ -2900,7 +2934,7 @@ int launch_fwd_quad(const void* H, float* P, float* dual, int32_t* iters, int64_
                     int max_iter, hipStream_t stream) {
     const int64_t blocks = (B + 63) / 64;
     if (blocks > INT32_MAX) return BIRKHOFF4_ERR_SIZE;
-    hipLaunchKernelGGL((newton_fwd_quad_kernel<DT, WD, WI>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+    launch_kernel((newton_fwd_quad_kernel<DT, WD, WI>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
                        stream, H, P, dual, iters, B, tol, max_iter);
     return launch_status();
 }
@@ -2916,20 +2950,20 @@ int dispatch_fwd_quad(const void* H, float* P, float* dual, int32_t* iters, int6
 
 template <int DT>
 int dispatch_fwd(const void* H, float* P, float* dual, int32_t* iters, int64_t B, float tol,
-                 int max_iter, hipStream_t stream, int cus) {
-    if (dual && iters) return launch_fwd<DT, true, true>(H, P, dual, iters, B, tol, max_iter, stream, cus);
-    if (dual) return launch_fwd<DT, true, false>(H, P, dual, iters, B, tol, max_iter, stream, cus);
-    if (iters) return launch_fwd<DT, false, true>(H, P, dual, iters, B, tol, max_iter, stream, cus);
-    return launch_fwd<DT, false, false>(H, P, dual, iters, B, tol, max_iter, stream, cus);
+                 int max_iter, hipStream_t stream, int cus, int dev) {
+    if (dual && iters) return launch_fwd<DT, true, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, dev);
+    if (dual) return launch_fwd<DT, true, false>(H, P, dual, iters, B, tol, max_iter, stream, cus, dev);
+    if (iters) return launch_fwd<DT, false, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, dev);
+    return launch_fwd<DT, false, false>(H, P, dual, iters, B, tol, max_iter, stream, cus, dev);
 }
 
 template <int DT>
 int dispatch_fwd_hess(const void* H, float* P, float* dual, int32_t* iters, float* hess, int64_t B, float tol,
-                      int max_iter, hipStream_t stream, int cus) {
-    if (dual && iters) return launch_fwd<DT, true, true, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, hess);
-    if (dual) return launch_fwd<DT, true, false, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, hess);
-    if (iters) return launch_fwd<DT, false, true, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, hess);
-    return launch_fwd<DT, false, false, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, hess);
+                      int max_iter, hipStream_t stream, int cus, int dev) {
+    if (dual && iters) return launch_fwd<DT, true, true, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, dev, hess);
+    if (dual) return launch_fwd<DT, true, false, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, dev, hess);
+    if (iters) return launch_fwd<DT, false, true, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, dev, hess);
+    return launch_fwd<DT, false, false, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, dev, hess);
 }
 
 // n = 8: one range of problems per wave, blocks scheduled by the hardware.
@@ -2943,7 +2977,7 @@ int launch_fwd8(const void* H, float* P, float* dual, int32_t* iters, int64_t B,
     if (per_wave < waves_min) per_wave = waves_min;
     const int64_t waves = (B + per_wave - 1) / per_wave;
     const int64_t grid = (waves + kB8Waves - 1) / kB8Waves;
-    hipLaunchKernelGGL((newton8_fwd_kernel<DT, WD, WI, OT>), dim3(static_cast<unsigned>(grid)), dim3(kB8Block), 0,
+    launch_kernel((newton8_fwd_kernel<DT, WD, WI, OT>), dim3(static_cast<unsigned>(grid)), dim3(kB8Block), 0,
                        stream, H, P, dual, iters, B, tol, max_iter, per_wave, a, b, eta);
     return launch_status();
 }
@@ -2976,7 +3010,7 @@ int launch_ot_fwd(const float* M, const float* a, const float* b, float eta, flo
     if (per_wave < waves_min) per_wave = waves_min;
     const int64_t waves = (B + per_wave - 1) / per_wave;
     const int64_t grid = (waves + kOtWaves - 1) / kOtWaves;
-    hipLaunchKernelGGL((ot4_fwd_kernel<WD, WI>), dim3(static_cast<unsigned>(grid)), dim3(kOtBlock), 0, stream, M, a,
+    launch_kernel((ot4_fwd_kernel<WD, WI>), dim3(static_cast<unsigned>(grid)), dim3(kOtBlock), 0, stream, M, a,
                        b, eta, T, dual, iters, B, tol, max_iter, per_wave);
     return launch_status();
 }
@@ -2991,7 +3025,7 @@ int64_t grid_for(int64_t B, int block, int cus, int per_cu) {
 template <int DX, int N = 4>
 int launch_mix_fwd(const float* P, const void* X, void* Y, int64_t B, int64_t nc, hipStream_t stream, int cus) {
     const int64_t grid = grid_for(B, kMixWaves, cus, kMixPerCu);
-    hipLaunchKernelGGL((mix_fwd_kernel<DX, N>), dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
+    launch_kernel((mix_fwd_kernel<DX, N>), dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
                        static_cast<const v4u*>(X), static_cast<v4u*>(Y), B, nc);
     return launch_status();
 }
@@ -3000,7 +3034,7 @@ template <int DX, int N = 4>
 int launch_mix_bwd(const float* P, const void* X, const void* dY, void* dX, float* dH, int64_t B, int64_t nc,
                    hipStream_t stream, int cus) {
     const int64_t grid = grid_for(B, kMixWaves, cus, kMixPerCu);
-    hipLaunchKernelGGL((mix_bwd_kernel<DX, N>), dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
+    launch_kernel((mix_bwd_kernel<DX, N>), dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
                        static_cast<const v4u*>(X), static_cast<const v4u*>(dY), static_cast<v4u*>(dX), dH, B, nc);
     return launch_status();
 }
@@ -3030,11 +3064,11 @@ int birkhoff4_fwd_ex2(const void* H, int h_dtype, float* P, float* dual, int32_t
             return dispatch_fwd_quad<BIRKHOFF4_BF16>(H, P, dual, iters, B, tol, max_iter, stream);
         return dispatch_fwd_quad<BIRKHOFF4_F32>(H, P, dual, iters, B, tol, max_iter, stream);
     }
-    int cus = 0;
-    if (int e = device_cus(&cus)) return e;
+    int cus = 0, dev = 0;
+    if (int e = device_cus(stream, &cus, &dev)) return e;
     if (h_dtype == BIRKHOFF4_BF16)
-        return dispatch_fwd<BIRKHOFF4_BF16>(H, P, dual, iters, B, tol, max_iter, stream, cus);
-    return dispatch_fwd<BIRKHOFF4_F32>(H, P, dual, iters, B, tol, max_iter, stream, cus);
+        return dispatch_fwd<BIRKHOFF4_BF16>(H, P, dual, iters, B, tol, max_iter, stream, cus, dev);
+    return dispatch_fwd<BIRKHOFF4_F32>(H, P, dual, iters, B, tol, max_iter, stream, cus, dev);
 }
 
 int birkhoff4_fwd_hess(const void* H, int h_dtype, float* P, float* dual, float* hess, int32_t* iters,
@@ -3055,11 +3089,11 @@ int birkhoff4_fwd_hess(const void* H, int h_dtype, float* P, float* dual, float*
         overlaps(P, np, hess, nw) || overlaps(dual, nd, iters, ni) || overlaps(dual, nd, hess, nw) ||
         overlaps(hess, nw, iters, ni))
         return BIRKHOFF4_ERR_OVERLAP;
-    int cus = 0;
-    if (int e = device_cus(&cus)) return e;
+    int cus = 0, dev = 0;
+    if (int e = device_cus(stream, &cus, &dev)) return e;
     if (h_dtype == BIRKHOFF4_BF16)
-        return dispatch_fwd_hess<BIRKHOFF4_BF16>(H, P, dual, iters, hess, B, tol, max_iter, stream, cus);
-    return dispatch_fwd_hess<BIRKHOFF4_F32>(H, P, dual, iters, hess, B, tol, max_iter, stream, cus);
+        return dispatch_fwd_hess<BIRKHOFF4_BF16>(H, P, dual, iters, hess, B, tol, max_iter, stream, cus, dev);
+    return dispatch_fwd_hess<BIRKHOFF4_F32>(H, P, dual, iters, hess, B, tol, max_iter, stream, cus, dev);
 }
 
 int birkhoff4_fwd_ex(const void* H, int h_dtype, float* P, float* dual, int32_t* iters, int64_t B,
@@ -3110,7 +3144,7 @@ int birkhoff4_ot_bwd(const float* T, const float* a, const float* dT, float eta,
     const int64_t chunks = (B + 63) / 64;
     const int64_t want = (chunks + kOtWaves - 1) / kOtWaves;
     const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
-    hipLaunchKernelGGL(ot4_bwd_kernel, dim3(static_cast<unsigned>(grid)), dim3(kOtBlock), 0, stream, T, a, dT, eta,
+    launch_kernel(ot4_bwd_kernel, dim3(static_cast<unsigned>(grid)), dim3(kOtBlock), 0, stream, T, a, dT, eta,
                        dM, B);
     return launch_status();
 }
@@ -3150,7 +3184,7 @@ int birkhoff8_ot_bwd(const float* T, const float* a, const float* dT, float eta,
     const int64_t chunks = (B + 63) / 64;
     const int64_t want = (chunks + kB8Waves - 1) / kB8Waves;
     const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
-    hipLaunchKernelGGL((implicit8_bwd_kernel<BIRKHOFF4_F32, true>), dim3(static_cast<unsigned>(grid)),
+    launch_kernel((implicit8_bwd_kernel<BIRKHOFF4_F32, true>), dim3(static_cast<unsigned>(grid)),
                        dim3(kB8Block), 0, stream, T, dT, dM, B, a, eta);
     return launch_status();
 }
@@ -3186,10 +3220,10 @@ int birkhoff8_bwd(const float* P, const void* dP, int dp_dtype, float* dH, int64
     const int64_t want = (chunks + kB8Waves - 1) / kB8Waves;
     const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
     if (dp_dtype == BIRKHOFF4_BF16)
-        hipLaunchKernelGGL((implicit8_bwd_kernel<BIRKHOFF4_BF16, false>), dim3(static_cast<unsigned>(grid)),
+        launch_kernel((implicit8_bwd_kernel<BIRKHOFF4_BF16, false>), dim3(static_cast<unsigned>(grid)),
                            dim3(kB8Block), 0, stream, P, dP, dH, B, nullptr, 1.f);
     else
-        hipLaunchKernelGGL((implicit8_bwd_kernel<BIRKHOFF4_F32, false>), dim3(static_cast<unsigned>(grid)),
+        launch_kernel((implicit8_bwd_kernel<BIRKHOFF4_F32, false>), dim3(static_cast<unsigned>(grid)),
                            dim3(kB8Block), 0, stream, P, dP, dH, B, nullptr, 1.f);
     return launch_status();
 }
@@ -3208,10 +3242,10 @@ int birkhoff4_bwd_ex(const float* P, const void* dP, int dp_dtype, float* dH, in
     const int64_t want = (chunks + kBwdWaves - 1) / kBwdWaves;
     const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
     if (dp_dtype == BIRKHOFF4_BF16)
-        hipLaunchKernelGGL(implicit_bwd_kernel<BIRKHOFF4_BF16>, dim3(static_cast<unsigned>(grid)), dim3(kBwdBlock),
+        launch_kernel(implicit_bwd_kernel<BIRKHOFF4_BF16>, dim3(static_cast<unsigned>(grid)), dim3(kBwdBlock),
                            0, stream, P, dP, dH, B, nullptr);
     else
-        hipLaunchKernelGGL(implicit_bwd_kernel<BIRKHOFF4_F32>, dim3(static_cast<unsigned>(grid)), dim3(kBwdBlock),
+        launch_kernel(implicit_bwd_kernel<BIRKHOFF4_F32>, dim3(static_cast<unsigned>(grid)), dim3(kBwdBlock),
                            0, stream, P, dP, dH, B, nullptr);
     return launch_status();
 }
@@ -3230,10 +3264,10 @@ int birkhoff4_bwd_hess(const float* P, const float* hess, const void* dP, int dp
     const int64_t want = (chunks + kBwdWaves - 1) / kBwdWaves;
     const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
     if (dp_dtype == BIRKHOFF4_BF16)
-        hipLaunchKernelGGL((implicit_bwd_kernel<BIRKHOFF4_BF16, true>), dim3(static_cast<unsigned>(grid)),
+        launch_kernel((implicit_bwd_kernel<BIRKHOFF4_BF16, true>), dim3(static_cast<unsigned>(grid)),
                            dim3(kBwdBlock), 0, stream, P, dP, dH, B, hess);
     else
-        hipLaunchKernelGGL((implicit_bwd_kernel<BIRKHOFF4_F32, true>), dim3(static_cast<unsigned>(grid)),
+        launch_kernel((implicit_bwd_kernel<BIRKHOFF4_F32, true>), dim3(static_cast<unsigned>(grid)),
                            dim3(kBwdBlock), 0, stream, P, dP, dH, B, hess);
     return launch_status();
 }
@@ -3253,14 +3287,14 @@ int birkhoff4_sk_fwd(const void* H, int h_dtype, float* P, int64_t B, int n_step
     if (misaligned(H) || misaligned(P)) return BIRKHOFF4_ERR_ALIGN;
     if (overlaps(H, static_cast<size_t>(B) * 16 * dtype_bytes(h_dtype), P, static_cast<size_t>(B) * 64))
         return BIRKHOFF4_ERR_OVERLAP;
-    int cus = 0;
-    if (int e = device_cus(&cus)) return e;
+    int cus = 0, dev = 0;
+    if (int e = device_cus(stream, &cus, &dev)) return e;
     const int64_t grid = grid_for(B, 256, cus, 64);
     if (h_dtype == BIRKHOFF4_BF16)
-        hipLaunchKernelGGL(sk_fwd_kernel<BIRKHOFF4_BF16>, dim3(static_cast<unsigned>(grid)), dim3(256), 0,
+        launch_kernel(sk_fwd_kernel<BIRKHOFF4_BF16>, dim3(static_cast<unsigned>(grid)), dim3(256), 0,
                            stream, H, P, B, n_steps);
     else
-        hipLaunchKernelGGL(sk_fwd_kernel<BIRKHOFF4_F32>, dim3(static_cast<unsigned>(grid)), dim3(256), 0,
+        launch_kernel(sk_fwd_kernel<BIRKHOFF4_F32>, dim3(static_cast<unsigned>(grid)), dim3(256), 0,
                            stream, H, P, B, n_steps);
     return launch_status();
 }
@@ -3277,21 +3311,21 @@ int birkhoff4_sk_bwd(const void* H, int h_dtype, const void* dP, int dp_dtype, f
     if (overlaps(dH, n, H, static_cast<size_t>(B) * 16 * dtype_bytes(h_dtype)) ||
         overlaps(dH, n, dP, static_cast<size_t>(B) * 16 * dtype_bytes(dp_dtype)))
         return BIRKHOFF4_ERR_OVERLAP;
-    int cus = 0;
-    if (int e = device_cus(&cus)) return e;
+    int cus = 0, dev = 0;
+    if (int e = device_cus(stream, &cus, &dev)) return e;
     if (n_steps == kSkRegSteps) {
         const int64_t grid = grid_for(B, 256, cus, 64);
         const dim3 g(static_cast<unsigned>(grid)), blk(256);
         if (h_dtype == BIRKHOFF4_BF16) {
             if (dp_dtype == BIRKHOFF4_BF16)
-                hipLaunchKernelGGL((sk_bwd_reg_kernel<BIRKHOFF4_BF16, BIRKHOFF4_BF16, kSkRegSteps>), g, blk, 0, stream, H, dP, dH, B);
+                launch_kernel((sk_bwd_reg_kernel<BIRKHOFF4_BF16, BIRKHOFF4_BF16, kSkRegSteps>), g, blk, 0, stream, H, dP, dH, B);
             else
-                hipLaunchKernelGGL((sk_bwd_reg_kernel<BIRKHOFF4_BF16, BIRKHOFF4_F32, kSkRegSteps>), g, blk, 0, stream, H, dP, dH, B);
+                launch_kernel((sk_bwd_reg_kernel<BIRKHOFF4_BF16, BIRKHOFF4_F32, kSkRegSteps>), g, blk, 0, stream, H, dP, dH, B);
         } else {
             if (dp_dtype == BIRKHOFF4_BF16)
-                hipLaunchKernelGGL((sk_bwd_reg_kernel<BIRKHOFF4_F32, BIRKHOFF4_BF16, kSkRegSteps>), g, blk, 0, stream, H, dP, dH, B);
+                launch_kernel((sk_bwd_reg_kernel<BIRKHOFF4_F32, BIRKHOFF4_BF16, kSkRegSteps>), g, blk, 0, stream, H, dP, dH, B);
             else
-                hipLaunchKernelGGL((sk_bwd_reg_kernel<BIRKHOFF4_F32, BIRKHOFF4_F32, kSkRegSteps>), g, blk, 0, stream, H, dP, dH, B);
+                launch_kernel((sk_bwd_reg_kernel<BIRKHOFF4_F32, BIRKHOFF4_F32, kSkRegSteps>), g, blk, 0, stream, H, dP, dH, B);
         }
         return launch_status();
     }
@@ -3300,14 +3334,14 @@ int birkhoff4_sk_bwd(const void* H, int h_dtype, const void* dP, int dp_dtype, f
     const dim3 g(static_cast<unsigned>(grid)), blk(64);
     if (h_dtype == BIRKHOFF4_BF16) {
         if (dp_dtype == BIRKHOFF4_BF16)
-            hipLaunchKernelGGL((sk_bwd_kernel<BIRKHOFF4_BF16, BIRKHOFF4_BF16>), g, blk, lds, stream, H, dP, dH, B, n_steps);
+            launch_kernel((sk_bwd_kernel<BIRKHOFF4_BF16, BIRKHOFF4_BF16>), g, blk, lds, stream, H, dP, dH, B, n_steps);
         else
-            hipLaunchKernelGGL((sk_bwd_kernel<BIRKHOFF4_BF16, BIRKHOFF4_F32>), g, blk, lds, stream, H, dP, dH, B, n_steps);
+            launch_kernel((sk_bwd_kernel<BIRKHOFF4_BF16, BIRKHOFF4_F32>), g, blk, lds, stream, H, dP, dH, B, n_steps);
     } else {
         if (dp_dtype == BIRKHOFF4_BF16)
-            hipLaunchKernelGGL((sk_bwd_kernel<BIRKHOFF4_F32, BIRKHOFF4_BF16>), g, blk, lds, stream, H, dP, dH, B, n_steps);
+            launch_kernel((sk_bwd_kernel<BIRKHOFF4_F32, BIRKHOFF4_BF16>), g, blk, lds, stream, H, dP, dH, B, n_steps);
         else
-            hipLaunchKernelGGL((sk_bwd_kernel<BIRKHOFF4_F32, BIRKHOFF4_F32>), g, blk, lds, stream, H, dP, dH, B, n_steps);
+            launch_kernel((sk_bwd_kernel<BIRKHOFF4_F32, BIRKHOFF4_F32>), g, blk, lds, stream, H, dP, dH, B, n_steps);
     }
     return launch_status();
 }
@@ -3335,8 +3369,8 @@ int birkhoff4_mix_fwd(const void* H, int h_dtype, const void* X, int x_dtype, vo
         overlaps(H, nh, iters, ni) || overlaps(P, np, dual, nd) || overlaps(P, np, iters, ni) ||
         overlaps(dual, nd, iters, ni))
         return BIRKHOFF4_ERR_OVERLAP;
-    int cus = 0;
-    if (int e = device_cus(&cus)) return e;
+    int cus = 0, dev = 0;
+    if (int e = device_cus(stream, &cus, &dev)) return e;
     // the projection checks and queues P first; the mixing kernel then reads it
     if (int e = birkhoff4_fwd_ex2(H, h_dtype, P, dual, iters, B, tol, max_iter, BIRKHOFF4_AUTO, stream)) return e;
     if (nc == 0) return BIRKHOFF4_OK;
@@ -3360,8 +3394,8 @@ int birkhoff4_mix_bwd(const float* P, const void* X, const void* dY, int x_dtype
     if (overlaps(dX, nx, P, np) || overlaps(dX, nx, X, nx) || overlaps(dX, nx, dY, nx) || overlaps(dX, nx, dH, np) ||
         overlaps(dH, np, P, np) || overlaps(dH, np, X, nx) || overlaps(dH, np, dY, nx))
         return BIRKHOFF4_ERR_OVERLAP;
-    int cus = 0;
-    if (int e = device_cus(&cus)) return e;
+    int cus = 0, dev = 0;
+    if (int e = device_cus(stream, &cus, &dev)) return e;
     if (x_dtype == BIRKHOFF4_BF16) return launch_mix_bwd<BIRKHOFF4_BF16>(P, X, dY, dX, dH, B, nc, stream, cus);
     return launch_mix_bwd<BIRKHOFF4_F32>(P, X, dY, dX, dH, B, nc, stream, cus);
 }
@@ -3389,8 +3423,8 @@ int birkhoff8_mix_fwd(const void* H, int h_dtype, const void* X, int x_dtype, vo
         overlaps(H, nh, iters, ni) || overlaps(P, np, dual, nd) || overlaps(P, np, iters, ni) ||
         overlaps(dual, nd, iters, ni))
         return BIRKHOFF4_ERR_OVERLAP;
-    int cus = 0;
-    if (int e = device_cus(&cus)) return e;
+    int cus = 0, dev = 0;
+    if (int e = device_cus(stream, &cus, &dev)) return e;
     if (int e = birkhoff8_fwd(H, h_dtype, P, dual, iters, B, tol, max_iter, stream)) return e;
     if (nc == 0) return BIRKHOFF4_OK;
     if (x_dtype == BIRKHOFF4_BF16) return launch_mix_fwd<BIRKHOFF4_BF16, 8>(P, X, Y, B, nc, stream, cus);
@@ -3413,8 +3447,8 @@ int birkhoff8_mix_bwd(const float* P, const void* X, const void* dY, int x_dtype
     if (overlaps(dX, nx, P, np) || overlaps(dX, nx, X, nx) || overlaps(dX, nx, dY, nx) || overlaps(dX, nx, dH, np) ||
         overlaps(dH, np, P, np) || overlaps(dH, np, X, nx) || overlaps(dH, np, dY, nx))
         return BIRKHOFF4_ERR_OVERLAP;
-    int cus = 0;
-    if (int e = device_cus(&cus)) return e;
+    int cus = 0, dev = 0;
+    if (int e = device_cus(stream, &cus, &dev)) return e;
     // dX, and dP into dH's memory; then the 8 x 8 backward turns dP into dH in place (each of
     // its waves reads a chunk's dP whole before it writes that chunk's dH)
     const int e = x_dtype == BIRKHOFF4_BF16 ? launch_mix_bwd<BIRKHOFF4_BF16, 8>(P, X, dY, dX, dH, B, nc, stream, cus)
@@ -3423,8 +3457,8 @@ int birkhoff8_mix_bwd(const float* P, const void* X, const void* dY, int x_dtype
     const int64_t chunks = (B + 63) / 64;
     const int64_t want = (chunks + kB8Waves - 1) / kB8Waves;
     const int64_t grid = want < kMaxGrid ? want : kMaxGrid;
-    hipLaunchKernelGGL((implicit8_bwd_kernel<BIRKHOFF4_F32, false>), dim3(static_cast<unsigned>(grid)),
-                       dim3(kB8Block), 0, stream, P, dH, dH, B, nullptr, 1.f);
+    launch_kernel((implicit8_bwd_kernel<BIRKHOFF4_F32, false, true>), dim3(static_cast<unsigned>(grid)),
+                  dim3(kB8Block), 0, stream, P, dH, dH, B, nullptr, 1.f);
     return launch_status();
 }
 

@@ -3,9 +3,10 @@ with the fp64 oracle, element by element.
 
 Bounds, per element: P within 1e-5 of the oracle's (the projection's own bound), so an
 output mixed from four inputs may differ by 1e-5 times the sum of their magnitudes, plus
-fp32 rounding, plus for bf16 outputs one rounding to bf16. With an 8-bit significand, half a
-unit in the last place is up to 2^-8 of the value just above a power of two, and the value
-rounded is the fp32 result, not the exact one: 2^-7 of the value is allowed. dH is held to the projection backward's bound,
+fp32 rounding, plus for bf16 outputs one rounding to nearest even of the fp32 result. With an
+8-bit significand, half a unit in the last place is at most 2^-8 of the value rounded, and that
+value (the fp32 result) is within the additive slack of the exact one: 2^-8 (|ref| + slack) is
+allowed, half of what a truncating conversion could reach. dH is held to the projection backward's bound,
 |dH - dH_ref|_inf / max(1, |dH_ref|_inf) <= 1e-4 per token.
 """
 import numpy as np
@@ -37,7 +38,7 @@ def mixed_bound(P_err, inputs, out_ref, bf16):
     s = np.abs(inputs).sum(axis=1, keepdims=True)
     b = P_err * s + 1e-6 * s + 1e-30
     if bf16:
-        b = b + 2.0 ** -7 * np.abs(out_ref)
+        b = b + 2.0 ** -8 * (np.abs(out_ref) + b)
     return b
 
 

@@ -237,3 +237,27 @@ def test_binding_rejects_mismatched_outputs():
         b4.bwd(P, H, out=torch.empty(50, 4, 4, device="cuda"))
     with pytest.raises(ValueError):
         b4.fwd8(torch.zeros(10, 8, 8, device="cuda"), out=torch.empty(10, 4, 4, device="cuda"))
+
+
+@pytest.mark.parametrize("B", [1000, 100003])
+def test_north_star_signatures(B):
+    # birkhoff4_fwd(H, P, dual, B, tol, max_iter, stream) and birkhoff4_bwd(P, dual, dP, dH, B,
+    # stream) called directly through the C ABI on device buffers (fp32, the default dispatch:
+    # the four-lanes-per-problem forward below 2^15 problems, the throughput forward above)
+    say(f"test: birkhoff4_fwd / birkhoff4_bwd through the C ABI, B={B}")
+    H, dP = workloads.gauss(B, 5.0, seed=B + 17)
+    Hd, dPd = to_dev(H), to_dev(dP)
+    P = torch.empty(B, 4, 4, device="cuda:0")
+    dual = torch.empty(B, 8, device="cuda:0")
+    dH = torch.empty(B, 4, 4, device="cuda:0")
+    lib = b4.lib()
+    stream = torch.cuda.current_stream().cuda_stream
+    assert lib.birkhoff4_fwd(Hd.data_ptr(), P.data_ptr(), dual.data_ptr(), B, 1e-6, MAX_ITER, stream) == 0
+    assert lib.birkhoff4_bwd(P.data_ptr(), dual.data_ptr(), dPd.data_ptr(), dH.data_ptr(), B, stream) == 0
+    torch.cuda.synchronize()
+    check_parity(H, P.cpu().numpy(), dual.cpu().numpy(), dP, dH.cpu().numpy(), f"C ABI B={B}")
+    # the backward accepts dual = NULL (it reads only P and dP) and gives the same dH
+    dH2 = torch.empty_like(dH)
+    assert lib.birkhoff4_bwd(P.data_ptr(), None, dPd.data_ptr(), dH2.data_ptr(), B, stream) == 0
+    torch.cuda.synchronize()
+    assert torch.equal(dH, dH2)
