@@ -86,87 +86,66 @@ def traffic_from_profiles(workload: str):
     return out or None
 
 
-def main() -> int:
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="mix_bf16_b2e24")
-    ap.add_argument("--tol", type=float, default=1e-6)
-    ap.add_argument("--max-iter", type=int, default=64)
-    ap.add_argument("--cpu-sample", type=int, default=1 << 24,
-                    help="matrices in the oracle's CPU-baseline sample")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-sk", action="store_true")
-    ap.add_argument("--no-hess", action="store_true", help="skip the saved-Hessian variant's timing")
-    ap.add_argument("--no-n8", action="store_true", help="skip the 8x8 measurement")
-    ap.add_argument("--n8-only", action="store_true", help="time only the 8x8 path (for profiler runs)")
-    ap.add_argument("--no-ot", action="store_true", help="skip the general-OT measurement")
-    ap.add_argument("--ot8-only", action="store_true", help="time only the 8x8 general-OT path (for profiler runs)")
-    ap.add_argument("--ot-only", action="store_true", help="time only the general-OT path (for profiler runs)")
-    ap.add_argument("--no-small", action="store_true", help="skip the small-batch launch timing")
-    ap.add_argument("--no-mix", action="store_true", help="skip the residual-mixing measurement")
-    ap.add_argument("--mix-only", action="store_true", help="time only the residual-mixing pair (for profiler runs)")
-    ap.add_argument("--small-only", action="store_true", help="time only the small-batch cases")
-    ap.add_argument("--no-extras", action="store_true",
-                    help="time only the headline path, none of the other measurements (for profiler runs)")
-    ap.add_argument("--copy-calibration", action="store_true",
-                    help="only run a 1 GiB device copy 5 times (scale for HBM byte counters)")
-    args = ap.parse_args()
+# The paper's accuracy tables (Sec. 5, Tables 1-2): L1 marginal error ||T1 - 1||_1 + ||T^T 1 - 1||_1
+# over 10,000 matrices, mean / std / median / max; measured on an NVIDIA RTX 6000 Ada, precision not
+# stated, Newton at tol 1e-6 and at most 20 iterations, Sinkhorn-Knopp ("Vanilla") 20 iterations.
+PAPER_TABLES = {
+    "N(0,1)": {"newton": [0.654e-6, 0.385e-6, 0.527e-6, 2.503e-6], "sk20": [8.336e-6, 20.01e-6, 7.793e-6, 1381e-6]},
+    "Unif(-1,1)": {"newton": [0.593e-6, 0.352e-6, 0.477e-6, 2.325e-6], "sk20": [7.790e-6, 0.141e-6, 7.793e-6, 8.330e-6]},
+    "N(0,10^2)": {"newton": [1.594e-3, 4.428e-3, 0.0009e-3, 91.3e-3], "sk20": [72.54e-3, 61.12e-3, 65.13e-3, 832.6e-3]},
+    "Unif(-10,10)": {"newton": [0.159e-3, 1.479e-3, 0.0006e-3, 46.57e-3], "sk20": [40.02e-3, 37.16e-3, 32.93e-3, 234.0e-3]},
+}
+PAPER_CAP = 20  # the paper's iteration cap (Sec. 5)
 
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py: measures one GPU only; the projection shards by contiguous batch ranges with "
-              "no communication between GPUs, so only --gpus 1 is measured.",
-              file=sys.stderr)
-        return 2
 
+def step_stats(itn: np.ndarray) -> dict:
+    """Newton trial evaluations per matrix; frac_over_20: the share that the paper's cap of 20
+    iterations would leave unconverged (this library counts every trial evaluation)."""
+    conv = itn[itn >= 0]
+    n64 = (len(itn) // 64) * 64
+    wave_max = np.clip(itn[:n64], 0, None).reshape(-1, 64).max(axis=1).mean() if n64 else float("nan")
+    return {"mean": round(float(conv.mean()), 3) if len(conv) else None,
+            "p50": int(np.percentile(conv, 50)) if len(conv) else None,
+            "p99": int(np.percentile(conv, 99)) if len(conv) else None,
+            "max": int(conv.max()) if len(conv) else None,
+            "mean_of_wave_max": round(float(wave_max), 3),
+            "not_converged": int((itn == -1).sum()), "non_finite": int((itn == -2).sum()),
+            "frac_over_20": float(((itn > PAPER_CAP) | (itn == -1)).mean()),
+            "hist": np.bincount(np.clip(conv, 0, 40), minlength=41).tolist()}
+
+
+def l1_stats(P) -> tuple:
+    """Per-matrix max marginal error and the paper's L1 error, in fp64 on the device."""
+    P64 = P.double()
+    r, c = P64.sum(-1) - 1, P64.sum(-2) - 1
+    marg = torch_max(r.abs().amax(-1), c.abs().amax(-1))
+    l1 = r.abs().sum(-1) + c.abs().sum(-1)
+    return marg, l1
+
+
+def torch_max(a, b):
+    import torch
+    return torch.maximum(a, b)
+
+
+def measure(name, args, dev, stream, *, storage=None, steps=None, warmup=None, extras=True, sk=False,
+            buckets=False, autograd=False, hess=False):
+    """Time K steps of the whole path (forward, and backward when the workload has dP) on one
+    workload through the C ABI, inputs resident in HBM; per-kernel HIP-event times on the
+    launch stream. storage="f32" stores a bf16 workload's (bf16-rounded) values as fp32."""
     import torch
 
     import paper_2606_07574_amd as b4
     import workloads
-
-    if not torch.cuda.is_available():
-        print("bench.py: no GPU visible", file=sys.stderr)
-        return 2
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    if args.copy_calibration:
-        X = torch.ones(1 << 28, device=dev)
-        Y = torch.empty_like(X)
-        for _ in range(5):
-            Y.copy_(X)
-        torch.cuda.synchronize()
-        print(json.dumps({"copy_calibration": {"bytes_read": X.numel() * 4, "bytes_written": Y.numel() * 4,
-                                               "launches": 5}}), flush=True)
-        return 0
-    if args.n8_only:
-        print(json.dumps({"n8": bench_n8(args, dev, torch.cuda.current_stream(dev))}), flush=True)
-        return 0
-    if args.ot_only:
-        print(json.dumps({"ot": bench_ot(args, dev, torch.cuda.current_stream(dev))}), flush=True)
-        return 0
-    if args.mix_only:
-        st = torch.cuda.current_stream(dev)
-        print(json.dumps({"mix_streams": bench_mix_streams(args, dev, st),
-                          "mix8_streams": bench_mix_streams(args, dev, st, B=1 << 14, n=8)}), flush=True)
-        return 0
-    if args.small_only:
-        print(json.dumps({"small_batch": bench_small_batch(dev)}), flush=True)
-        return 0
-    if args.ot8_only:
-        print(json.dumps({"ot8": bench_ot(args, dev, torch.cuda.current_stream(dev), n=8)}), flush=True)
-        return 0
-    w = workloads.WORKLOADS[args.workload]
+    w = workloads.WORKLOADS[name]
     B = w.B
-    bf16 = w.storage == "bf16"
-
     t0 = time.time()
     ch = workloads.generate(w.name, threads=16)
     log(f"generated {w.name} B={B} in {time.time() - t0:.1f}s")
+    bf16 = w.storage == "bf16" and storage != "f32"
 
     def dev_input(x32, bits):
-        if bits is not None:
+        if bf16 and bits is not None:
             return torch.from_numpy(bits.view(np.int16)).to(dev).view(torch.bfloat16)
         return torch.from_numpy(x32).to(dev)
 
@@ -184,44 +163,46 @@ def main() -> int:
                          dH=torch.empty(B, 4, 4, device=dev) if w.grad else None))
     torch.cuda.synchronize()
     lib = b4.lib()
-    stream = torch.cuda.current_stream(dev)
     sptr = stream.cuda_stream
     hcode = b4.BF16 if bf16 else b4.F32
+    K = args.steps if steps is None else steps
+    W = args.warmup if warmup is None else warmup
+    ev_start = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    ev_mid = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    ev_end = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
 
-    def step(k):
+    def step(k, timed):
         st = sets[k % n_sets]
+        if timed:
+            ev_start[k].record(stream)
         rc = lib.birkhoff4_fwd_ex(st["H"].data_ptr(), hcode, st["P"].data_ptr(), st["dual"].data_ptr(),
                                   None, B, args.tol, args.max_iter, sptr)
         if rc:
             raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
-        ev_mid[k % len(ev_mid)].record(stream)
+        if timed:
+            ev_mid[k].record(stream)
         if w.grad:
-            rc = lib.birkhoff4_bwd_ex(st["P"].data_ptr(), st["G"].data_ptr(), hcode if bf16 else b4.F32,
+            rc = lib.birkhoff4_bwd_ex(st["P"].data_ptr(), st["G"].data_ptr(), hcode,
                                       st["dH"].data_ptr(), B, sptr)
             if rc:
                 raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+        if timed:
+            ev_end[k].record(stream)
 
-    K, W = args.steps, args.warmup
-    ev_start = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
-    ev_mid = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
-    ev_end = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
     for k in range(W):
-        step(k)
+        step(k, False)
     torch.cuda.synchronize()
-    log(f"warmup done ({W} steps); timing {K} steps")
+    log(f"{w.name}: warmup done ({W} steps); timing {K} steps")
     t_start = time.perf_counter()
     for k in range(K):
-        ev_start[k].record(stream)
-        step(k)
-        ev_end[k].record(stream)
+        step(k, True)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     fwd_ms = float(np.mean([ev_start[k].elapsed_time(ev_mid[k]) for k in range(K)]))
     bwd_ms = float(np.mean([ev_mid[k].elapsed_time(ev_end[k]) for k in range(K)])) if w.grad else 0.0
     ms_per_step = wall * 1e3 / K
-    value = B * K / wall
-    log(f"timed: {ms_per_step:.3f} ms/step  fwd {fwd_ms:.3f} ms  bwd {bwd_ms:.3f} ms")
-
+    log(f"{w.name}{' (fp32 storage)' if storage == 'f32' else ''} timed: {ms_per_step:.3f} ms/step  "
+        f"fwd {fwd_ms:.3f} ms  bwd {bwd_ms:.3f} ms")
     fwd_bytes = B * (in_bytes(bf16) + 64 + 32)
     bwd_bytes = B * (64 + in_bytes(bf16) + 64)
     kernels = {"newton_fwd": {"avg_ms": fwd_ms, "alg_bytes_per_launch": fwd_bytes,
@@ -231,73 +212,42 @@ def main() -> int:
         kernels["implicit_bwd"] = {"avg_ms": bwd_ms, "alg_bytes_per_launch": bwd_bytes,
                                    "achieved_GBs": bwd_bytes / (bwd_ms * 1e-3) / 1e9,
                                    "proj_per_s": B / (bwd_ms * 1e-3)}
-    dominant = max(kernels, key=lambda k: kernels[k]["avg_ms"])
-    traffic = traffic_from_profiles(w.name)
-    ach = kernels[dominant]["achieved_GBs"]
-    roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
-                "traffic": (traffic or {}).get(dominant)}
-    # the forward is bound by its write requests and its VALU work together: its VALU issue
-    # rate (lane-instructions counted by rocprofv3 on this source) is reported beside the bytes
-    valu = valu_from_profiles(w.name, dominant, "traffic")
-    if valu:
-        va = valu / (kernels[dominant]["avg_ms"] * 1e-3) / 1e12
-        roofline["valu"] = {"achieved": round(va, 2), "peak": VALU_PEAK_T, "unit": "T lane-instr/s",
-                            "frac": round(va / VALU_PEAK_T, 4), "counted_lane_instr_per_launch": valu}
     path_bytes = fwd_bytes + (bwd_bytes if w.grad else 0)
-    out = {
-        "metric": METRIC if w.name == "mix_bf16_b2e24" else f"4x4 Birkhoff projections/sec ({w.name})",
-        "value": round(value, 1), "unit": "proj/s", "n_gpus": 1, "steps": K, "warmup": W,
-        "ms_per_step": round(ms_per_step, 4), "fwd_proj_per_s": round(B / (fwd_ms * 1e-3), 1),
-        "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": w.name, "B": B, "storage": w.storage, "tol": args.tol,
-                   "max_iter": args.max_iter, "passes": "fwd+bwd" if w.grad else "fwd",
-                   "desc": w.desc, "buffer_sets": n_sets},
-        "roofline": roofline,
-        "path_hbm_frac": round(path_bytes * K / wall / 1e9 / HBM_PEAK_GBS, 4),
-        "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in v.items()}
-                    for k, v in kernels.items()},
-    }
-
-    if not args.no_extras:
-        # diagnostics outside the timed region: Newton step histogram, marginal errors
+    res = {"workload": w.name + ("_f32_storage" if storage == "f32" else ""), "B": B,
+           "storage": "bf16" if bf16 else "f32", "passes": "fwd+bwd" if w.grad else "fwd",
+           "desc": w.desc + (" -- stored as fp32 (the same bf16-rounded values)" if storage == "f32" else ""),
+           "steps": K, "buffer_sets": n_sets, "ms_per_step": round(ms_per_step, 4),
+           "value": round(B * K / wall, 1), "unit": "proj/s",
+           "alg_bytes_per_projection": path_bytes // B,
+           "path_hbm_frac": round(path_bytes * K / wall / 1e9 / HBM_PEAK_GBS, 4),
+           "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in v.items()}
+                       for k, v in kernels.items()}}
+    dom = max(kernels, key=lambda k: kernels[k]["avg_ms"])
+    ach = kernels[dom]["achieved_GBs"]
+    res["roofline"] = {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+                       "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4)}
+    res["_wall"], res["_fwd_ms"], res["_lib"], res["_hcode"] = wall, fwd_ms, lib, hcode
+    if extras:
+        # outside the timed region: Newton step histogram, marginal errors
         st = sets[0]
         P, dual, it = b4.fwd(st["H"], args.tol, args.max_iter, want_dual=True, want_iters=True)
         torch.cuda.synchronize()
         itn = it.cpu().numpy()
-        P64 = P.double()
-        marg = torch.maximum((P64.sum(-1) - 1).abs().amax(-1), (P64.sum(-2) - 1).abs().amax(-1))
-        l1 = (P64.sum(-1) - 1).abs().sum(-1) + (P64.sum(-2) - 1).abs().sum(-1)
-        conv = itn[itn >= 0]
-        # per-wave maximum: what a one-problem-per-lane kernel without refill would pay
-        n64 = (len(itn) // 64) * 64
-        wave_max = np.clip(itn[:n64], 0, None).reshape(-1, 64).max(axis=1).mean() if n64 else float("nan")
-        out["newton_steps"] = {
-            "mean": round(float(conv.mean()), 3) if len(conv) else None,
-            "p50": int(np.percentile(conv, 50)) if len(conv) else None,
-            "p99": int(np.percentile(conv, 99)) if len(conv) else None,
-            "max": int(conv.max()) if len(conv) else None,
-            "mean_of_wave_max": round(float(wave_max), 3),
-            "not_converged": int((itn == -1).sum()), "non_finite": int((itn == -2).sum()),
-            "hist": np.bincount(np.clip(conv, 0, 40), minlength=41).tolist(),
-        }
-        out["max_marginal_err"] = float(marg.max().item())
-        out["marginal_err_L1"] = {"mean": float(l1.mean().item()), "median": float(l1.median().item()),
+        marg, l1 = l1_stats(P)
+        res["newton_steps"] = step_stats(itn)
+        res["max_marginal_err"] = float(marg.max().item())
+        res["marginal_err_L1"] = {"mean": float(l1.mean().item()), "median": float(l1.median().item()),
                                   "max": float(l1.max().item())}
-        log(f"newton steps: {out['newton_steps']}")
-        log(f"max marginal err {out['max_marginal_err']:.3e}")
-
-        if not args.no_sk:
+        log(f"{w.name}: newton steps {res['newton_steps']}; max marginal err {res['max_marginal_err']:.3e}")
+        sk_marg = None
+        if sk:
             n_sk = 20
-            for k in range(2):
+            for _ in range(2):
                 b4.sk_fwd(st["H"], n_sk)
                 if w.grad:
                     b4.sk_bwd(st["H"], st["G"], n_sk)
             torch.cuda.synchronize()
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e2 = torch.cuda.Event(enable_timing=True)
+            e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
             ks = max(3, K // 4)
             f_ms = b_ms = 0.0
             for k in range(ks):
@@ -312,63 +262,275 @@ def main() -> int:
                 b_ms += e1.elapsed_time(e2) if w.grad else 0.0
             f_ms /= ks
             b_ms /= ks
-            S64 = Psk.double()
-            smarg = torch.maximum((S64.sum(-1) - 1).abs().amax(-1), (S64.sum(-2) - 1).abs().amax(-1))
-            sl1 = (S64.sum(-1) - 1).abs().sum(-1) + (S64.sum(-2) - 1).abs().sum(-1)
-            out["sk20_baseline"] = {
+            smarg, sl1 = l1_stats(Psk)
+            res["sk20_baseline"] = {
                 "value": round(B / ((f_ms + b_ms) * 1e-3), 1), "unit": "proj/s",
                 "fwd_ms": round(f_ms, 4), "bwd_ms": round(b_ms, 4),
                 "max_marginal_err": float(smarg.max().item()),
                 "marginal_err_L1": {"mean": float(sl1.mean().item()), "median": float(sl1.median().item()),
                                     "max": float(sl1.max().item())},
             }
-            log(f"sk20: {out['sk20_baseline']}")
+            log(f"{w.name}: sk20 {res['sk20_baseline']}")
             sk_marg = smarg.cpu().numpy()
-            del Psk, S64
-        else:
-            sk_marg = None
-        out["buckets"] = bucket_report(w, ch, itn, marg.cpu().numpy(), sk_marg)
-        del P, P64
-        if w.grad:
-            out["autograd_step"] = bench_autograd_step(args, lib, sets, n_sets, B, hcode, bf16, stream,
+            del Psk
+        if buckets:
+            res["buckets"] = bucket_report(w, ch, itn, marg.cpu().numpy(), sk_marg)
+        del P, dual, it, marg, l1
+        if autograd and w.grad:
+            res["autograd_step"] = bench_autograd_step(args, lib, sets, n_sets, B, hcode, bf16, stream,
                                                        in_bytes(bf16))
-            log(f"autograd step (no dual): {out['autograd_step']}")
-        if w.grad and not args.no_hess:
-            out["saved_hessian"] = bench_saved_hessian(args, lib, sets, n_sets, B, hcode, bf16, stream,
+            log(f"autograd step (no dual): {res['autograd_step']}")
+        if hess and w.grad:
+            res["saved_hessian"] = bench_saved_hessian(args, lib, sets, n_sets, B, hcode, bf16, stream,
                                                        in_bytes(bf16), ms_per_step)
-            log(f"saved hessian: {out['saved_hessian']}")
+            log(f"saved hessian: {res['saved_hessian']}")
+    res["_ch"] = ch
+    del sets, H0, G0
+    return res
 
+
+def public(res: dict) -> dict:
+    return {k: v for k, v in res.items() if not k.startswith("_")}
+
+
+def bench_b4096(args, dev) -> dict:
+    """n01_b4096 (B = 4096 N(0,1) fp32 matrices): launch-bound, reported in microseconds per
+    fwd + bwd call pair, eager and replayed from a HIP graph, plus each kernel's event time."""
+    import torch
+
+    import paper_2606_07574_amd as b4
+    import workloads
+    ch = workloads.make_chunk(workloads.WORKLOADS["n01_b4096"], 0)
+    row = bench_small_batch(dev, sizes=(4096,), inputs={4096: (ch.H, ch.dP)})[0]
+    H = torch.from_numpy(ch.H).to(dev)
+    P, dual, it = b4.fwd(H, args.tol, args.max_iter, want_dual=True, want_iters=True)
+    torch.cuda.synchronize()
+    marg, l1 = l1_stats(P)
+    return {"workload": "n01_b4096", "B": 4096, "desc": workloads.WORKLOADS["n01_b4096"].desc,
+            "unit": "us per fwd+bwd call pair", "eager_us_per_pair": row["eager_us_per_pair"],
+            "graph_us_per_pair": row["graph_us_per_pair"], "fwd_event_us": row["fwd_event_us"],
+            "bwd_event_us": row["bwd_event_us"], "graph_proj_per_s": row["graph_proj_per_s"],
+            "newton_steps": step_stats(it.cpu().numpy()), "max_marginal_err": float(marg.max().item())}
+
+
+def bench_accuracy(args, dev) -> dict:
+    """The paper's accuracy tables on this hardware: 10,000 matrices from each of its four input
+    families, L1 marginal error of the Newton forward and of the 20-step Sinkhorn-Knopp baseline
+    (mean / std / median / max), beside the paper's own figures (RTX 6000 Ada)."""
+    import torch
+
+    import paper_2606_07574_amd as b4
+    import workloads
+    fams = {"N(0,1)": workloads.gauss(10000, 1.0, seed=101, grad=False)[0],
+            "Unif(-1,1)": workloads.uniform(10000, 1.0, seed=102, grad=False)[0],
+            "N(0,10^2)": workloads.gauss(10000, 10.0, seed=103, grad=False)[0],
+            "Unif(-10,10)": workloads.uniform(10000, 10.0, seed=104, grad=False)[0]}
+    out = {"n": 10000, "measure": "L1 marginal error ||P1-1||_1 + ||P^T1-1||_1 (fp64 sums of the fp32 output)",
+           "order": ["mean", "std", "median", "max"], "tol": args.tol, "max_iter": args.max_iter,
+           "paper_hardware": "NVIDIA RTX 6000 Ada (paper, Sec. 5; precision not stated)", "families": {}}
+    for name, H32 in fams.items():
+        H = torch.from_numpy(H32).to(dev)
+        P, _, it = b4.fwd(H, args.tol, args.max_iter, want_dual=False, want_iters=True)
+        Psk = b4.sk_fwd(H, 20)
+        torch.cuda.synchronize()
+        row = {}
+        for label, X in (("newton", P), ("sk20", Psk)):
+            _, l1 = l1_stats(X)
+            row[label] = [float(l1.mean().item()), float(l1.std().item()), float(l1.median().item()),
+                          float(l1.max().item())]
+        itn = it.cpu().numpy()
+        row["newton_steps_mean"] = round(float(itn[itn >= 0].mean()), 3)
+        row["newton_frac_over_20"] = float(((itn > PAPER_CAP) | (itn == -1)).mean())
+        row["paper"] = PAPER_TABLES[name]
+        out["families"][name] = row
+        log(f"accuracy {name}: {row}")
+    return out
+
+
+def cpu_info() -> dict:
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        aff = len(os.sched_getaffinity(0))
+    except AttributeError:
+        aff = None
+    return {"host_cpus": os.cpu_count(), "affinity_cpus": aff, "cpu_model": model}
+
+
+def bench_cpu_baseline(args, ch, w) -> dict:
+    """The oracle as it stands (fp64, its own tolerance 1e-13) on the headline workload's first
+    matrices, fwd + bwd, on the machine's CPU share of threads; its 1-thread rate on a smaller sample
+    at 1e-13 and at the GPU's tolerance; and the host's core count and CPU model."""
+    import oracle
+    n = min(args.cpu_sample, w.B)
+    Hs = ch.H[:n].astype(np.float64)
+    Gs = ch.dP[:n].astype(np.float64) if w.grad else None
+    threads = oracle.default_threads()
+
+    def rate(H, G, tol, nth):
+        t0 = time.perf_counter()
+        Pr, _, _ = oracle.fwd(H, tol=tol, threads=nth)
+        if G is not None:
+            oracle.bwd(Pr, G, threads=nth)
+        dt = time.perf_counter() - t0
+        return H.shape[0] / dt, dt
+
+    v, dt = rate(Hs, Gs, oracle.DEFAULT_TOL, threads)
+    vg, dtg = rate(Hs, Gs, args.tol, threads)
+    n1 = min(n, 1 << 18)
+    v1, dt1 = rate(Hs[:n1], Gs[:n1] if Gs is not None else None, oracle.DEFAULT_TOL, 1)
+    v1g, dt1g = rate(Hs[:n1], Gs[:n1] if Gs is not None else None, args.tol, 1)
+    info = cpu_info()
+    res = {"value": round(v, 1), "unit": "proj/s", "cores": threads, "kind": "oracle",
+           "sample": f"first {n} matrices of {w.name}; fp64 oracle forward (tol {oracle.DEFAULT_TOL:g}) + "
+                     f"backward, {threads} threads (the GPU box's CPU share for one GPU), {dt:.1f} s",
+           **info,
+           "at_gpu_tol": {"value": round(vg, 1), "tol": args.tol, "threads": threads, "seconds": round(dtg, 2)},
+           "one_thread": {"value": round(v1, 1), "tol": oracle.DEFAULT_TOL, "sample": n1, "seconds": round(dt1, 2)},
+           "one_thread_at_gpu_tol": {"value": round(v1g, 1), "tol": args.tol, "sample": n1,
+                                     "seconds": round(dt1g, 2)}}
+    log(f"cpu baseline: {res}")
+    return res
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mix_bf16_b2e24")
+    ap.add_argument("--tol", type=float, default=1e-6)
+    ap.add_argument("--max-iter", type=int, default=64)
+    ap.add_argument("--cpu-sample", type=int, default=1 << 24,
+                    help="matrices in the oracle's CPU-baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sk", action="store_true")
+    ap.add_argument("--no-hess", action="store_true", help="skip the saved-Hessian variant's timing")
+    ap.add_argument("--no-configs", action="store_true", help="skip the other workload configurations")
+    ap.add_argument("--no-n8", action="store_true", help="skip the 8x8 measurement")
+    ap.add_argument("--n8-only", action="store_true", help="time only the 8x8 path (for profiler runs)")
+    ap.add_argument("--no-ot", action="store_true", help="skip the general-OT measurement")
+    ap.add_argument("--ot8-only", action="store_true", help="time only the 8x8 general-OT path (for profiler runs)")
+    ap.add_argument("--ot-only", action="store_true", help="time only the general-OT path (for profiler runs)")
+    ap.add_argument("--no-small", action="store_true", help="skip the small-batch launch timing")
+    ap.add_argument("--no-mix", action="store_true", help="skip the residual-mixing measurement")
+    ap.add_argument("--mix-only", action="store_true", help="time only the residual-mixing pair (for profiler runs)")
+    ap.add_argument("--small-only", action="store_true", help="time only the small-batch cases")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="time only the given workload's path, none of the other measurements (for profiler runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB device copy 5 times (scale for HBM byte counters)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: measures one GPU only; the projection shards by contiguous batch ranges with "
+              "no communication between GPUs, so only --gpus 1 is measured.",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    import workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 2
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    if args.copy_calibration:
+        X = torch.ones(1 << 28, device=dev)
+        Y = torch.empty_like(X)
+        for _ in range(5):
+            Y.copy_(X)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration": {"bytes_read": X.numel() * 4, "bytes_written": Y.numel() * 4,
+                                               "launches": 5}}), flush=True)
+        return 0
+    if args.n8_only:
+        print(json.dumps({"n8": bench_n8(args, dev, stream)}), flush=True)
+        return 0
+    if args.ot_only:
+        print(json.dumps({"ot": bench_ot(args, dev, stream)}), flush=True)
+        return 0
+    if args.mix_only:
+        print(json.dumps({"mix_streams": bench_mix_streams(args, dev, stream),
+                          "mix8_streams": bench_mix_streams(args, dev, stream, B=1 << 14, n=8)}), flush=True)
+        return 0
+    if args.small_only:
+        print(json.dumps({"small_batch": bench_small_batch(dev)}), flush=True)
+        return 0
+    if args.ot8_only:
+        print(json.dumps({"ot8": bench_ot(args, dev, stream, n=8)}), flush=True)
+        return 0
+
+    w = workloads.WORKLOADS[args.workload]
+    extras = not args.no_extras
+    head = measure(w.name, args, dev, stream, extras=extras, sk=extras and not args.no_sk, buckets=extras,
+                   autograd=extras, hess=extras and not args.no_hess)
+    B, K = w.B, args.steps
+    kernels = head["kernels"]
+    dominant = max(kernels, key=lambda k: kernels[k]["avg_ms"])
+    traffic = traffic_from_profiles(w.name)
+    ach = kernels[dominant]["achieved_GBs"]
+    roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                "traffic": (traffic or {}).get(dominant)}
+    # the forward is bound by its write requests and its VALU work together: its VALU issue
+    # rate (lane-instructions counted by rocprofv3 on this source) is reported beside the bytes
+    valu = valu_from_profiles(w.name, dominant, "traffic")
+    if valu:
+        va = valu / (kernels[dominant]["avg_ms"] * 1e-3) / 1e12
+        roofline["valu"] = {"achieved": round(va, 2), "peak": VALU_PEAK_T, "unit": "T lane-instr/s",
+                            "frac": round(va / VALU_PEAK_T, 4), "counted_lane_instr_per_launch": valu}
+    out = {
+        "metric": METRIC if w.name == "mix_bf16_b2e24" else f"4x4 Birkhoff projections/sec ({w.name})",
+        "value": head["value"], "unit": "proj/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"], "fwd_proj_per_s": round(B / (head["_fwd_ms"] * 1e-3), 1),
+        "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "storage": w.storage, "tol": args.tol,
+                   "max_iter": args.max_iter, "passes": head["passes"], "desc": w.desc,
+                   "buffer_sets": head["buffer_sets"]},
+        "roofline": roofline,
+        "path_hbm_frac": head["path_hbm_frac"],
+        "kernels": kernels,
+    }
+    for k in ("newton_steps", "max_marginal_err", "marginal_err_L1", "sk20_baseline", "buckets",
+              "autograd_step", "saved_hessian"):
+        if k in head:
+            out[k] = head[k]
     if not args.no_cpu_baseline:
-        # the oracle as it stands (fp64, its own tolerance 1e-13), then at the GPU's tolerance
-        import oracle
-        n = min(args.cpu_sample, B)
-        Hs = ch.H[:n].astype(np.float64)
-        Gs = ch.dP[:n].astype(np.float64) if w.grad else None
-        threads = oracle.default_threads()
-        rates = {}
-        for label, tol in (("default", oracle.DEFAULT_TOL), ("gpu_tol", args.tol)):
-            t0 = time.perf_counter()
-            Pr, _, _ = oracle.fwd(Hs, tol=tol, threads=threads)
-            if w.grad:
-                oracle.bwd(Pr, Gs, threads=threads)
-            rates[label] = (n / (time.perf_counter() - t0), time.perf_counter() - t0)
-        v, dt = rates["default"]
-        out["cpu_baseline"] = {"value": round(v, 1), "unit": "proj/s", "cores": threads, "kind": "oracle",
-                               "sample": f"first {n} matrices of {w.name}; fp64 oracle forward (tol "
-                                         f"{oracle.DEFAULT_TOL:g}) + backward, {threads} threads, {dt:.1f} s"}
-        out["cpu_oracle_at_gpu_tol"] = {"value": round(rates["gpu_tol"][0], 1), "unit": "proj/s",
-                                        "tol": args.tol, "seconds": round(rates["gpu_tol"][1], 2)}
-        log(f"cpu baseline: {out['cpu_baseline']}")
+        out["cpu_baseline"] = bench_cpu_baseline(args, head["_ch"], w)
+    del head
 
-    # the other workloads, each timed after the headline's region (--no-extras: the path only)
-    if not args.no_n8 and not args.no_extras:
+    if extras and not args.no_configs:
+        # the other workload configurations, each timed on its own after the headline's region
+        cfg = {"n01_b4096": bench_b4096(args, dev)}
+        for name, kw in (("n01_b2e20_fwd", {}), ("n10_b2e22", {"sk": True}),
+                         ("logunif_b2e25", {"sk": True, "buckets": True}),
+                         ("mix_bf16_b2e24", {"storage": "f32"})):
+            r = measure(name, args, dev, stream, extras=True, **kw)
+            cfg[r["workload"]] = public(r)
+            del r
+        out["configs"] = cfg
+        out["accuracy_tables"] = bench_accuracy(args, dev)
+    if not args.no_n8 and extras:
         out["n8"] = bench_n8(args, dev, stream)
-    if not args.no_ot and not args.no_extras:
+    if not args.no_ot and extras:
         out["ot"] = bench_ot(args, dev, stream)
         out["ot8"] = bench_ot(args, dev, stream, n=8)
-    if not args.no_small and not args.no_extras:
+    if not args.no_small and extras:
         out["small_batch"] = bench_small_batch(dev)
-    if not args.no_mix and not args.no_extras:
+    if not args.no_mix and extras:
         out["mix_streams"] = bench_mix_streams(args, dev, stream)
         out["mix8_streams"] = bench_mix_streams(args, dev, stream, B=1 << 14, n=8)
 
@@ -467,7 +629,7 @@ def bench_mix_streams(args, dev, stream, B=1 << 15, C=4096, n=4) -> dict:
     return res
 
 
-def bench_small_batch(dev, sizes=(512, 4096, 32768), pairs=32, reps=20) -> list:
+def bench_small_batch(dev, sizes=(512, 4096, 32768), pairs=32, reps=20, inputs=None) -> list:
     """Small batches are launch-bound: per fwd + bwd pair (N(0,1) logits, fp32, default
     variant), the wall time of back-to-back eager calls, the same pairs replayed from a HIP
     graph that holds `pairs` of them, and the two kernels' event-timed durations."""
@@ -477,7 +639,7 @@ def bench_small_batch(dev, sizes=(512, 4096, 32768), pairs=32, reps=20) -> list:
     import workloads
     res = []
     for B in sizes:
-        H32, dP32 = workloads.gauss(B, 1.0, seed=B)
+        H32, dP32 = inputs[B] if inputs and B in inputs else workloads.gauss(B, 1.0, seed=B)
         H = torch.from_numpy(H32).to(dev)
         dP = torch.from_numpy(dP32).to(dev)
         P = torch.empty_like(H)

@@ -251,3 +251,11 @@ def mix_streams_device(B: int, C: int, seed: int, dev, n: int = 4):
     X = torch.randn(B, n, C, device=dev, generator=g).to(torch.bfloat16)
     G = torch.randn(B, n, C, device=dev, generator=g).to(torch.bfloat16)
     return H.to(torch.bfloat16).contiguous(), X.contiguous(), G.contiguous()
+
+
+def uniform(B: int, half_width: float, seed: int, grad: bool = True) -> tuple[np.ndarray, np.ndarray | None]:
+    """Small ad-hoc batch: H ~ Unif(-half_width, half_width) and dP ~ N(0,1)."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 3000, int(round(half_width * 1000))]))
+    H = rng.uniform(-half_width, half_width, size=(B, 4, 4)).astype(np.float32)
+    dP = rng.standard_normal((B, 4, 4), dtype=np.float32) if grad else None
+    return H, dP
