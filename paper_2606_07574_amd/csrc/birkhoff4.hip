@@ -1109,23 +1109,45 @@ __device__ __forceinline__ void load_token_matrix(const float* __restrict__ P, i
     for (int q = 0; q < N * N; ++q) p[q] = pt[q];
 }
 
-// A wave walks the items (t, c0) of its tokens, c0 = 0, 64, 128, ... < nc: lane l handles
-// chunk c0 + l of each of the four rows. The next item's loads are issued before the
-// current item is mixed and stored (loads and stores retire in order, so a wait for loads
-// issued after a store would also wait for that store), into the other of two buffers so
-// that no register copy waits for them. Lanes past the end of a row take its last chunk:
-// they load, mix and store the same bytes as that chunk's own lane, so every memory
-// instruction is issued by the whole wave and the waits count exactly.
-template <int DX, int N>
+// A wave walks the items (t, c0) of its tokens: lane l handles chunk c0 + l of each of the
+// N rows. With one wave per token (WPT = 1) c0 = 0, 64, 128, ... < nc; with WPT waves per
+// token, wave s of the token takes c0 = 64 s, 64 (s + WPT), ..., so that the token's waves
+// stream adjacent kilobytes of each row together. (Eight rows per token are sixteen or
+// twenty-four separate streams per wave; measured on a plain copy of this pattern, HBM
+// delivers about 10% more when four waves share a token's rows than when one wave walks
+// them alone. Four rows stream best one token per wave.) The next item's loads are issued
+// before the current item is mixed and stored (loads and stores retire in order, so a
+// wait for loads issued after a store would also wait for that store), into the other of
+// two buffers so that no register copy waits for them. Lanes past the end of a row take
+// its last chunk: they load, mix and store the same bytes as that chunk's own lane, so
+// every memory instruction is issued by the whole wave and the waits count exactly.
+template <int WPT>
+struct MixWalk {  // a wave's first token and chunk, and the strides of its walk
+    static constexpr int kTokensPerBlock = kMixWaves / WPT;
+    static constexpr int64_t kStep = 64 * WPT;
+    static __device__ __forceinline__ int wave() {
+        return __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+    }
+    static __device__ __forceinline__ int64_t first_token() {
+        return static_cast<int64_t>(blockIdx.x) * kTokensPerBlock + wave() / WPT;
+    }
+    static __device__ __forceinline__ int64_t first_chunk() { return 64 * (wave() % WPT); }
+    static __device__ __forceinline__ int64_t token_stride() {
+        return static_cast<int64_t>(gridDim.x) * kTokensPerBlock;
+    }
+};
+
+template <int DX, int N, int WPT = 1>
 __global__ __launch_bounds__(kMixBlock) void mix_fwd_kernel(const float* __restrict__ P,
                                                              const v4u* __restrict__ X, v4u* __restrict__ Y,
                                                              int64_t B, int64_t nc) {
+    using W = MixWalk<WPT>;
     const int lane = threadIdx.x & 63;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kMixWaves;
-    int64_t t = static_cast<int64_t>(blockIdx.x) * kMixWaves +
-                __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
-    if (t >= B) return;  // uniform; nc >= 1 here
-    int64_t c0 = 0;
+    const int64_t stride = W::token_stride();
+    const int64_t cfirst = W::first_chunk();
+    int64_t t = W::first_token();
+    if (t >= B || cfirst >= nc) return;  // uniform over the wave; nc >= 1 here
+    int64_t c0 = cfirst;
     auto offset = [&](int64_t tt, int64_t cc0) {
         const int64_t cc = cc0 + lane;
         return N * nc * tt + (cc < nc ? cc : nc - 1);
@@ -1139,9 +1161,9 @@ __global__ __launch_bounds__(kMixBlock) void mix_fwd_kernel(const float* __restr
     // mix the item in `cur` while the next one (or, after the last, this one again) loads
     // into `nxt`
     auto step = [&](const v4u cur[N], v4u nxt[N]) {
-        int64_t tn = t, cn = c0 + 64;
+        int64_t tn = t, cn = c0 + W::kStep;
         if (cn >= nc) {
-            cn = 0;
+            cn = cfirst;
             tn = t + stride;
         }
         const bool more = tn < B;
@@ -1160,9 +1182,9 @@ __global__ __launch_bounds__(kMixBlock) void mix_fwd_kernel(const float* __restr
     // loads are then used unconditionally by the next one (so they stay where they are
     // issued), and every path into a step leaves the same loads and stores in flight (so the
     // wait for `cur` does not cover the previous step's stores).
-    const int64_t items = ((B - t + stride - 1) / stride) * ((nc + 63) >> 6);
+    const int64_t items = ((B - t + stride - 1) / stride) * ((nc - cfirst + W::kStep - 1) / W::kStep);
     v4u a[N], b[N];
-    load_item(offset(t, 0), a);
+    load_item(offset(t, cfirst), a);
     step(a, b);
     int64_t k = 1;
     for (; k + 2 <= items; k += 2) {
@@ -1223,18 +1245,29 @@ __device__ __forceinline__ void wave_sum16(float v[16], int lane, float s[16]) {
 
 // The same walk; a token's dP is summed over the wave when its last item is done, while
 // the next item's loads are in flight. Lanes past the end of a row zero their X words, so
-// that the chunk they repeat adds nothing to dP.
-template <int DX, int N>
+// that the chunk they repeat adds nothing to dP. With several waves per token (n = 8 only,
+// all the block's waves on one token at a time) each wave leaves its sums in LDS and the
+// block's first wave adds them in wave order, so the result does not depend on timing.
+// That takes a barrier per token, which every wave must reach equally often: each wave
+// needs at least one item per token, nc >= 64 WPT (the launcher's condition).
+template <int DX, int N, int WPT = 1>
 __global__ __launch_bounds__(kMixBlock) void mix_bwd_kernel(const float* __restrict__ P,
                                                              const v4u* __restrict__ X,
                                                              const v4u* __restrict__ dY, v4u* __restrict__ dX,
                                                              float* __restrict__ dH, int64_t B, int64_t nc) {
+    static_assert(WPT == 1 || (N == 8 && WPT == kMixWaves), "several waves per token: n = 8, whole block");
+    using W = MixWalk<WPT>;
     constexpr int E = MixChunk<DX>::E;
     const int lane = threadIdx.x & 63;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kMixWaves;
-    int64_t t = static_cast<int64_t>(blockIdx.x) * kMixWaves +
-                __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
-    if (t >= B) return;
+    const int64_t stride = W::token_stride();
+    const int64_t cfirst = W::first_chunk();
+    int64_t t = W::first_token();
+    if (t >= B) return;  // uniform over the block when WPT > 1
+    // per-wave sums of the token's dP (WPT > 1), two buffers by token parity: a wave writes
+    // buffer q for token k + 2 only after the barrier of token k + 1, which the first wave
+    // reaches after it has read buffer q for token k
+    __shared__ float part[WPT > 1 ? 2 * kMixWaves * 64 : 1];
+    int parity = 0;
     constexpr int NN = N * N;
     float p[NN], acc[NN];  // acc: this lane's part of dP_ij = sum_c dY_i[c] X_j[c]
     auto token_matrix = [&](int64_t tt) { load_token_matrix<N>(P, tt, p); };
@@ -1252,8 +1285,23 @@ __global__ __launch_bounds__(kMixBlock) void mix_bwd_kernel(const float* __restr
                                           : v4f{out[12], out[13], out[14], out[15]};
                 reinterpret_cast<v4f*>(dH)[4 * t + lane] = row;
             }
-        } else {
+        } else if constexpr (WPT == 1) {
             dH[64 * t + lane] = wave_sum64_own(acc, lane);
+        } else {
+            float* buf = part + parity * (kMixWaves * 64);
+            const int w = W::wave();
+            buf[64 * w + lane] = wave_sum64_own(acc, lane);
+            // LDS-only fences: the next item's global loads stay in flight across the barrier
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+            if (w == 0) {
+                float sum = buf[lane];
+#pragma unroll
+                for (int q = 1; q < WPT; ++q) sum += buf[64 * q + lane];
+                dH[64 * t + lane] = sum;
+            }
+            parity ^= 1;
         }
 #pragma unroll
         for (int q = 0; q < NN; ++q) acc[q] = 0.f;
@@ -1269,7 +1317,7 @@ __global__ __launch_bounds__(kMixBlock) void mix_bwd_kernel(const float* __restr
             token_matrix(t);
         }
     }
-    int64_t c0 = 0;
+    int64_t c0 = cfirst;
     auto offset = [&](int64_t tt, int64_t cc0) {
         const int64_t cc = cc0 + lane;
         return N * nc * tt + (cc < nc ? cc : nc - 1);
@@ -1292,70 +1340,69 @@ __global__ __launch_bounds__(kMixBlock) void mix_bwd_kernel(const float* __restr
         constexpr int EW = E / 4;
 #pragma unroll
         for (int w = 0; w < 4; ++w) {  // one 32-bit word of the chunk at a time
-            float xv[N][EW], gv[N][EW];
+            if constexpr (DX == BIRKHOFF4_BF16) {
+                // two channels per word: bf16 dot products accumulated in fp32 (the products
+                // of two bf16 values are exact in fp32), on the packed words as loaded
+                uint32_t xw[N], gw[N];
 #pragma unroll
-            for (int j = 0; j < N; ++j) {
-                unpack_word<DX>(own ? xc[j] : v4u{0u, 0u, 0u, 0u}, w, xv[j]);
-                unpack_word<DX>(gc[j], w, gv[j]);
+                for (int j = 0; j < N; ++j) {
+                    const v4u xj = own ? xc[j] : v4u{0u, 0u, 0u, 0u};
+                    xw[j] = w == 0 ? xj.x : w == 1 ? xj.y : w == 2 ? xj.z : xj.w;
+                    gw[j] = w == 0 ? gc[j].x : w == 1 ? gc[j].y : w == 2 ? gc[j].z : gc[j].w;
+                }
+#pragma unroll
+                for (int i = 0; i < N; ++i)
+#pragma unroll
+                    for (int j = 0; j < N; ++j)
+                        acc[N * i + j] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, gw[i]),
+                                                                          __builtin_bit_cast(bf16x2, xw[j]),
+                                                                          acc[N * i + j], false);
+            } else {
+                float xv[N][EW], gv[N][EW];
+#pragma unroll
+                for (int j = 0; j < N; ++j) {
+                    unpack_word<DX>(own ? xc[j] : v4u{0u, 0u, 0u, 0u}, w, xv[j]);
+                    unpack_word<DX>(gc[j], w, gv[j]);
+                }
+#pragma unroll
+                for (int i = 0; i < N; ++i)
+#pragma unroll
+                    for (int j = 0; j < N; ++j)
+#pragma unroll
+                        for (int e = 0; e < EW; ++e)
+                            acc[N * i + j] = __builtin_fmaf(gv[i][e], xv[j][e], acc[N * i + j]);
             }
-#pragma unroll
-            for (int i = 0; i < N; ++i)
-#pragma unroll
-                for (int j = 0; j < N; ++j)
-#pragma unroll
-                    for (int e = 0; e < EW; ++e)
-                        acc[N * i + j] = __builtin_fmaf(gv[i][e], xv[j][e], acc[N * i + j]);
         }
     };
-    const int64_t items = ((B - t + stride - 1) / stride) * ((nc + 63) >> 6);
-    if constexpr (N == 4) {
-        // process the item in (xc, gc) while the next one loads into (xn, gn)
-        auto step = [&](const v4u xc[N], const v4u gc[N], v4u xn[N], v4u gn[N]) {
-            int64_t tn = t, cn = c0 + 64;
-            if (cn >= nc) {
-                cn = 0;
-                tn = t + stride;
-            }
-            const bool more = tn < B;
-            load_item(more ? offset(tn, cn) : offset(t, c0), xn, gn);
-            __builtin_amdgcn_sched_barrier(0);
-            process(xc, gc);
-            if (tn != t) {
-                finish_token();
-                if (more) token_matrix(tn);
-            }
-            t = tn;
-            c0 = cn;
-        };
-        // peeled first step and counted loop of two, as in the forward
-        v4u xa[N], ga[N], xb[N], gb[N];
-        load_item(offset(t, 0), xa, ga);
+    const int64_t items = ((B - t + stride - 1) / stride) * ((nc - cfirst + W::kStep - 1) / W::kStep);
+    // process the item in (xc, gc) while the next one loads into (xn, gn)
+    auto step = [&](const v4u xc[N], const v4u gc[N], v4u xn[N], v4u gn[N]) {
+        int64_t tn = t, cn = c0 + W::kStep;
+        if (cn >= nc) {
+            cn = cfirst;
+            tn = t + stride;
+        }
+        const bool more = tn < B;
+        load_item(more ? offset(tn, cn) : offset(t, c0), xn, gn);
+        __builtin_amdgcn_sched_barrier(0);
+        process(xc, gc);
+        if (tn != t) {
+            finish_token();
+            if (more) token_matrix(tn);
+        }
+        t = tn;
+        c0 = cn;
+    };
+    // peeled first step and counted loop of two, as in the forward
+    v4u xa[N], ga[N], xb[N], gb[N];
+    load_item(offset(t, c0), xa, ga);
+    step(xa, ga, xb, gb);
+    int64_t k = 1;
+    for (; k + 2 <= items; k += 2) {
+        step(xb, gb, xa, ga);
         step(xa, ga, xb, gb);
-        int64_t k = 1;
-        for (; k + 2 <= items; k += 2) {
-            step(xb, gb, xa, ga);
-            step(xa, ga, xb, gb);
-        }
-        if (k < items) step(xb, gb, xa, ga);
-    } else {
-        // n = 8: the 64 partial sums leave no room for a second buffer at two waves per SIMD
-        for (int64_t k = 0; k < items; ++k) {
-            v4u x[N], g[N];
-            load_item(offset(t, c0), x, g);
-            process(x, g);
-            int64_t tn = t, cn = c0 + 64;
-            if (cn >= nc) {
-                cn = 0;
-                tn = t + stride;
-            }
-            if (tn != t) {
-                finish_token();
-                if (tn < B) token_matrix(tn);
-            }
-            t = tn;
-            c0 = cn;
-        }
     }
+    if (k < items) step(xb, gb, xa, ga);
 }
 
 // ---------------------------------------------------------------------------
@@ -3021,21 +3068,32 @@ int64_t grid_for(int64_t B, int block, int cus, int per_cu) {
     return blocks < cap ? blocks : cap;
 }
 
-// Residual mixing: one token per wave at a time, grid-stride over the tokens.
+// Residual mixing, grid-stride over the tokens: one token per wave at a time for n = 4, and
+// for n = 8 one token per block (each wave a quarter of the chunks) once every row has at
+// least one chunk per wave, nc >= 64 kMixWaves, which the backward's per-token barrier needs.
+template <int N>
+bool mix_block_per_token(int64_t nc) {
+    return N == 8 && nc >= 64 * kMixWaves;
+}
+
 template <int DX, int N = 4>
 int launch_mix_fwd(const float* P, const void* X, void* Y, int64_t B, int64_t nc, hipStream_t stream, int cus) {
-    const int64_t grid = grid_for(B, kMixWaves, cus, kMixPerCu);
-    launch_kernel((mix_fwd_kernel<DX, N>), dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
-                       static_cast<const v4u*>(X), static_cast<v4u*>(Y), B, nc);
+    const bool bpt = mix_block_per_token<N>(nc);
+    const int64_t grid = grid_for(B, bpt ? 1 : kMixWaves, cus, kMixPerCu);
+    auto kern = bpt ? mix_fwd_kernel<DX, N, N == 8 ? kMixWaves : 1> : mix_fwd_kernel<DX, N, 1>;
+    launch_kernel(kern, dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
+                  static_cast<const v4u*>(X), static_cast<v4u*>(Y), B, nc);
     return launch_status();
 }
 
 template <int DX, int N = 4>
 int launch_mix_bwd(const float* P, const void* X, const void* dY, void* dX, float* dH, int64_t B, int64_t nc,
                    hipStream_t stream, int cus) {
-    const int64_t grid = grid_for(B, kMixWaves, cus, kMixPerCu);
-    launch_kernel((mix_bwd_kernel<DX, N>), dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
-                       static_cast<const v4u*>(X), static_cast<const v4u*>(dY), static_cast<v4u*>(dX), dH, B, nc);
+    const bool bpt = mix_block_per_token<N>(nc);
+    const int64_t grid = grid_for(B, bpt ? 1 : kMixWaves, cus, kMixPerCu);
+    auto kern = bpt ? mix_bwd_kernel<DX, N, N == 8 ? kMixWaves : 1> : mix_bwd_kernel<DX, N, 1>;
+    launch_kernel(kern, dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
+                  static_cast<const v4u*>(X), static_cast<const v4u*>(dY), static_cast<v4u*>(dX), dH, B, nc);
     return launch_status();
 }
 

@@ -209,8 +209,14 @@ def test_beyond_32bit_offsets():
 
 
 
+# The n = 8 kernels take one token per block (a quarter of each row's 16-byte chunks per wave)
+# from nc = 256 chunks a row on, one token per wave below: cases on both sides of the switch
+# (bf16 C = 2040, 2048, 2056 are nc = 255, 256, 257), ragged last chunks on each wave, and
+# fewer tokens than blocks.
 CASES8 = [(1, 8, torch.bfloat16, 1.0), (9, 40, torch.float32, 5.0), (300, 520, torch.bfloat16, 5.0),
-          (1000, 4096, torch.bfloat16, 20.0), (2049, 1028, torch.float32, 1.0), (64, 0, torch.bfloat16, 5.0)]
+          (1000, 4096, torch.bfloat16, 20.0), (2049, 1028, torch.float32, 1.0), (64, 0, torch.bfloat16, 5.0),
+          (130, 2040, torch.bfloat16, 5.0), (130, 2048, torch.bfloat16, 5.0), (257, 2056, torch.bfloat16, 5.0),
+          (517, 1032, torch.float32, 5.0), (3, 4096, torch.bfloat16, 5.0), (700, 1800, torch.float32, 5.0)]
 
 
 @pytest.mark.parametrize("B,C,dtype,sigma", CASES8,
