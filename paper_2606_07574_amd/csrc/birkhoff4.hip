@@ -1115,21 +1115,27 @@ __device__ __forceinline__ void load_token_matrix(const float* __restrict__ P, i
 // stream adjacent kilobytes of each row together. (Eight rows per token are sixteen or
 // twenty-four separate streams per wave; measured on a plain copy of this pattern, HBM
 // delivers about 10% more when four waves share a token's rows than when one wave walks
-// them alone. Four rows stream best one token per wave.) The next item's loads are issued
+// them alone. In the 8-stream backward two or eight waves per token measured 5-8% slower
+// than four. Four rows stream best one token per wave.) The next item's loads are issued
 // before the current item is mixed and stored (loads and stores retire in order, so a
 // wait for loads issued after a store would also wait for that store), into the other of
 // two buffers so that no register copy waits for them. Lanes past the end of a row take
 // its last chunk: they load, mix and store the same bytes as that chunk's own lane, so
 // every memory instruction is issued by the whole wave and the waits count exactly.
+// A block of kMixWaves waves takes kMixWaves tokens at a time (WPT = 1); with WPT > 1 the
+// block is the WPT waves of one token.
+constexpr int kMix8Wpt = 4;  // waves per token of the n = 8 kernels
+
 template <int WPT>
 struct MixWalk {  // a wave's first token and chunk, and the strides of its walk
-    static constexpr int kTokensPerBlock = kMixWaves / WPT;
+    static constexpr int kTokensPerBlock = WPT == 1 ? kMixWaves : 1;
+    static constexpr int kBlockThreads = WPT == 1 ? kMixBlock : 64 * WPT;
     static constexpr int64_t kStep = 64 * WPT;
     static __device__ __forceinline__ int wave() {
         return __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
     }
     static __device__ __forceinline__ int64_t first_token() {
-        return static_cast<int64_t>(blockIdx.x) * kTokensPerBlock + wave() / WPT;
+        return static_cast<int64_t>(blockIdx.x) * kTokensPerBlock + (WPT == 1 ? wave() : 0);
     }
     static __device__ __forceinline__ int64_t first_chunk() { return 64 * (wave() % WPT); }
     static __device__ __forceinline__ int64_t token_stride() {
@@ -1255,7 +1261,7 @@ __global__ __launch_bounds__(kMixBlock) void mix_bwd_kernel(const float* __restr
                                                              const v4u* __restrict__ X,
                                                              const v4u* __restrict__ dY, v4u* __restrict__ dX,
                                                              float* __restrict__ dH, int64_t B, int64_t nc) {
-    static_assert(WPT == 1 || (N == 8 && WPT == kMixWaves), "several waves per token: n = 8, whole block");
+    static_assert(WPT == 1 || (N == 8 && 64 * WPT <= kMixBlock), "several waves per token: n = 8 only");
     using W = MixWalk<WPT>;
     constexpr int E = MixChunk<DX>::E;
     const int lane = threadIdx.x & 63;
@@ -1266,7 +1272,7 @@ __global__ __launch_bounds__(kMixBlock) void mix_bwd_kernel(const float* __restr
     // per-wave sums of the token's dP (WPT > 1), two buffers by token parity: a wave writes
     // buffer q for token k + 2 only after the barrier of token k + 1, which the first wave
     // reaches after it has read buffer q for token k
-    __shared__ float part[WPT > 1 ? 2 * kMixWaves * 64 : 1];
+    __shared__ float part[WPT > 1 ? 2 * WPT * 64 : 1];
     int parity = 0;
     constexpr int NN = N * N;
     float p[NN], acc[NN];  // acc: this lane's part of dP_ij = sum_c dY_i[c] X_j[c]
@@ -1288,7 +1294,7 @@ __global__ __launch_bounds__(kMixBlock) void mix_bwd_kernel(const float* __restr
         } else if constexpr (WPT == 1) {
             dH[64 * t + lane] = wave_sum64_own(acc, lane);
         } else {
-            float* buf = part + parity * (kMixWaves * 64);
+            float* buf = part + parity * (WPT * 64);
             const int w = W::wave();
             buf[64 * w + lane] = wave_sum64_own(acc, lane);
             // LDS-only fences: the next item's global loads stay in flight across the barrier
@@ -3069,19 +3075,31 @@ int64_t grid_for(int64_t B, int block, int cus, int per_cu) {
 }
 
 // Residual mixing, grid-stride over the tokens: one token per wave at a time for n = 4, and
-// for n = 8 one token per block (each wave a quarter of the chunks) once every row has at
-// least one chunk per wave, nc >= 64 kMixWaves, which the backward's per-token barrier needs.
+// for n = 8 one token per block of kMix8Wpt waves once every row has at least one chunk per
+// wave, nc >= 64 kMix8Wpt, which the backward's per-token barrier needs. Both layouts size
+// the grid for the same number of waves per CU.
 template <int N>
 bool mix_block_per_token(int64_t nc) {
-    return N == 8 && nc >= 64 * kMixWaves;
+    return N == 8 && nc >= 64 * kMix8Wpt;
+}
+
+struct MixLaunch {
+    int64_t grid;
+    unsigned threads;
+};
+
+template <int N>
+MixLaunch mix_launch(int64_t B, int64_t nc, int cus) {
+    if (mix_block_per_token<N>(nc))
+        return {grid_for(B, 1, cus, kMixPerCu * kMixWaves / kMix8Wpt), MixWalk<kMix8Wpt>::kBlockThreads};
+    return {grid_for(B, kMixWaves, cus, kMixPerCu), kMixBlock};
 }
 
 template <int DX, int N = 4>
 int launch_mix_fwd(const float* P, const void* X, void* Y, int64_t B, int64_t nc, hipStream_t stream, int cus) {
-    const bool bpt = mix_block_per_token<N>(nc);
-    const int64_t grid = grid_for(B, bpt ? 1 : kMixWaves, cus, kMixPerCu);
-    auto kern = bpt ? mix_fwd_kernel<DX, N, N == 8 ? kMixWaves : 1> : mix_fwd_kernel<DX, N, 1>;
-    launch_kernel(kern, dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
+    const MixLaunch l = mix_launch<N>(B, nc, cus);
+    auto kern = mix_block_per_token<N>(nc) ? mix_fwd_kernel<DX, N, N == 8 ? kMix8Wpt : 1> : mix_fwd_kernel<DX, N, 1>;
+    launch_kernel(kern, dim3(static_cast<unsigned>(l.grid)), dim3(l.threads), 0, stream, P,
                   static_cast<const v4u*>(X), static_cast<v4u*>(Y), B, nc);
     return launch_status();
 }
@@ -3089,10 +3107,9 @@ int launch_mix_fwd(const float* P, const void* X, void* Y, int64_t B, int64_t nc
 template <int DX, int N = 4>
 int launch_mix_bwd(const float* P, const void* X, const void* dY, void* dX, float* dH, int64_t B, int64_t nc,
                    hipStream_t stream, int cus) {
-    const bool bpt = mix_block_per_token<N>(nc);
-    const int64_t grid = grid_for(B, bpt ? 1 : kMixWaves, cus, kMixPerCu);
-    auto kern = bpt ? mix_bwd_kernel<DX, N, N == 8 ? kMixWaves : 1> : mix_bwd_kernel<DX, N, 1>;
-    launch_kernel(kern, dim3(static_cast<unsigned>(grid)), dim3(kMixBlock), 0, stream, P,
+    const MixLaunch l = mix_launch<N>(B, nc, cus);
+    auto kern = mix_block_per_token<N>(nc) ? mix_bwd_kernel<DX, N, N == 8 ? kMix8Wpt : 1> : mix_bwd_kernel<DX, N, 1>;
+    launch_kernel(kern, dim3(static_cast<unsigned>(l.grid)), dim3(l.threads), 0, stream, P,
                   static_cast<const v4u*>(X), static_cast<const v4u*>(dY), static_cast<v4u*>(dX), dH, B, nc);
     return launch_status();
 }
