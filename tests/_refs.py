@@ -143,11 +143,13 @@ def _cramer3(h, g):
 
 
 def literal_newton_decimal(H, beta0=None, prec: int = 100, tol_exp: int = 60,
-                           max_iter: int = 400):
+                           max_iter: int = 400, full: bool = False):
     """Newton on f (Sec. 3.1) with the literal 4x4 gradient/Hessian (Sec. 3.2).
 
     Armijo halving on f, in ``prec``-digit decimal arithmetic; returns T* (as
-    Decimals) once every column sum is within 10^-tol_exp of one.
+    Decimals) once every column sum is within 10^-tol_exp of one, and with
+    ``full`` also beta (beta_4 = 0) and the row log-sum-exps lse_i, so that
+    alpha_i = -lse_i (eq. alpha_opt with unit rows).
     """
     with decimal.localcontext() as ctx:
         ctx.prec = prec
@@ -159,7 +161,7 @@ def literal_newton_decimal(H, beta0=None, prec: int = 100, tol_exp: int = 60,
             T, lse = _row_softmax_dec(Hd, beta)
             c = [sum(T[i][j] for i in range(4)) for j in range(4)]
             if max(abs(cj - 1) for cj in c) <= tol:
-                return T
+                return (T, beta, lse) if full else T
             g = [c[j] - 1 for j in range(3)]
             # h = diag(c) - T_{-m}^T T_{-m}   (Sec. 3.2)
             h = [[(c[j] if j == k else Decimal(0)) - sum(T[i][j] * T[i][k] for i in range(4))

@@ -125,3 +125,20 @@ def test_near_permutation_bounded():
     P, _, _ = oracle.fwd(ch.H)
     dH = oracle.bwd(P, ch.dP)
     assert np.abs(dH).max() < 3 * np.abs(ch.dP).max()
+
+
+@pytest.mark.parametrize("family,scale", [("gauss", 0.3), ("gauss", 1.0), ("gauss", 20.0), ("uniform", 1.0),
+                                          ("uniform", 10.0)])
+def test_literal_formula_from_independent_start(family, scale):
+    """eq. derivative written literally, at a T* that the literal Newton reached from
+    beta = 0 (independent of the oracle's forward), against the oracle's backward."""
+    prec = 60 if scale <= 5 else 80
+    gen = workloads.gauss if family == "gauss" else workloads.uniform
+    H, G = gen(8, scale, seed=31)
+    H = H.astype(np.float64)
+    P, _, _ = oracle.fwd(H)
+    dH = oracle.bwd(P, G)
+    for b in range(H.shape[0]):
+        T = _refs.literal_newton_decimal(H[b], prec=prec, tol_exp=prec // 2)
+        ref = _refs.literal_backward_decimal(T, G[b], prec=prec)
+        assert np.abs(dH[b] - ref).max() < 1e-11

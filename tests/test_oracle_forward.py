@@ -179,3 +179,43 @@ def test_workload_samples_converge():
         P, dual, it = oracle.fwd(ch.H)
         assert (it >= 0).all()
         assert oracle.marginal_errors(P)[0].max() <= 1.5e-13
+
+
+def _lap_inv_norm(P: np.ndarray) -> float:
+    """|L^-1|_inf of the reduced dual's Hessian at P: the Laplacian of the column graph
+    with weights sum_i P_ij P_ik, grounded at column 4. A column-sum residual r moves the
+    potentials by at most this times |r|_inf (to first order)."""
+    W = P.T @ P
+    np.fill_diagonal(W, 0.0)
+    L = -W[:3, :3]
+    L[np.arange(3), np.arange(3)] = W[:3].sum(axis=1)
+    with np.errstate(all="ignore"):
+        n = np.abs(np.linalg.inv(L)).sum(axis=1).max()
+    return float(n) if np.isfinite(n) else np.inf
+
+
+LITERAL_FAMILIES = [("gauss", 0.3), ("gauss", 1.0), ("gauss", 5.0), ("gauss", 20.0), ("gauss", 50.0),
+                    ("uniform", 1.0), ("uniform", 10.0)]
+
+
+@pytest.mark.parametrize("family,scale", LITERAL_FAMILIES)
+def test_literal_newton_from_zero(family, scale):
+    """The paper's literal Newton (Hessian diag(c) - T^T T, Cramer's rule, Armijo
+    halving) in decimals, started at beta = 0 and not at the oracle's solution,
+    reaches the oracle's P, and its dual (alpha = -lse, beta with beta_4 = 0) wherever
+    the conditioning of the reduced Hessian lets fp64 determine it."""
+    prec = 60 if scale <= 5 else (80 if scale <= 20 else 120)
+    gen = workloads.gauss if family == "gauss" else workloads.uniform
+    H, _ = gen(10, scale, seed=12, grad=False)
+    H = H.astype(np.float64)
+    P, dual, it = _fwd(H)
+    assert (it >= 0).all()
+    for b in range(H.shape[0]):
+        T, beta, lse = _refs.literal_newton_decimal(H[b], prec=prec, tol_exp=prec // 2, full=True)
+        Tf = _refs.dec_to_float(T)
+        assert np.abs(Tf - P[b]).max() < 1e-13
+        ref = np.array([-float(x) for x in lse] + [float(x) for x in beta])
+        assert ref[7] == 0.0 and dual[b, 7] == 0.0
+        # the oracle stops at column residual 1e-13; fp64 rounding of the sums adds ~1e-15
+        bound = 2.0 * _lap_inv_norm(Tf) * 1e-13 + 1e-13 * (1.0 + np.abs(ref).max())
+        assert np.abs(dual[b] - ref).max() <= bound
