@@ -1605,9 +1605,9 @@ __global__ __launch_bounds__(256, 3) void sk_bwd_reg_kernel(const void* __restri
 // lane. The forward is the 4 x 4 kernel's iteration written for 7 free potentials (the
 // row-softmax state in product form, trial steps capped in spread, Armijo with the
 // rounding-noise test, Levenberg-Marquardt shift, re-derivation of flushed entries). A
-// wave owns a range of problems; it initialises them 32 at a time with all its lanes (two
-// lanes per problem) into an LDS ring, and a lane whose problem finishes takes the next
-// one from the ring at once. The Newton system is the column Laplacian with 28 weights,
+// wave takes every nwv-th batch of 32 problems (nwv the resident waves of the grid); it
+// initialises a batch with all its lanes (two lanes per problem) into an LDS ring, and a
+// lane whose problem finishes takes the next one from the ring at once. The Newton system is the column Laplacian with 28 weights,
 // grounded at column 8 and solved by subtraction-free elimination of nodes 1..7.
 // ---------------------------------------------------------------------------
 constexpr int kB8Block = 256;
@@ -1615,10 +1615,6 @@ constexpr int kB8Waves = kB8Block / 64;
 constexpr int kB8Ring = 32;  // problems per initialisation batch (= ring slots per wave)
 constexpr int kB8Slot = 23;  // v4f per ring slot (22 used; odd, so that slots start in different banks)
 constexpr int kB8SlotOT = 27;  // the same with the two marginals (26 used)
-#ifndef B8_RANGES
-#define B8_RANGES 4096
-#endif
-constexpr int64_t kB8Ranges = B8_RANGES;  // wave ranges per launch (blocks are scheduled dynamically)
 
 // Index of the weight of column pair (j, k), j < k < 8, in a packed array of 28.
 __host__ __device__ constexpr int pw8(int j, int k) { return j * 8 - (j * (j + 1)) / 2 + (k - j - 1); }
@@ -1864,7 +1860,7 @@ template <int DT, bool WRITE_DUAL, bool WRITE_ITERS, bool OT>
 __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __restrict__ H, float* __restrict__ P,
                                                                 float* __restrict__ dual,
                                                                 int32_t* __restrict__ iters, int64_t B, float tol,
-                                                                int max_iter, int64_t per_wave,
+                                                                int max_iter,
                                                                 const float* __restrict__ av,
                                                                 const float* __restrict__ bv, float eta) {
     constexpr int NW = RawWords8<DT>::n;
@@ -1887,19 +1883,26 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
     v4f* const ring = ring_all[wv];
     int32_t* const order = order_all[wv];
     v4f* const marg = marg_all[OT ? wv : 0] + (OT ? 4 * lane : 0);
-    // The wave owns problems r0 .. r1 - 1.
-    const int64_t r0 = (static_cast<int64_t>(blockIdx.x) * kB8Waves + wv) * per_wave;
-    if (r0 >= B) return;  // uniform across the wave
-    const int64_t r1 = (r0 + per_wave < B) ? r0 + per_wave : B;
+    // The grid is the resident waves. Wave gw of the grid's nwv takes the batches of kB8Ring
+    // problems gw, gw + nwv, gw + 2 nwv, ...: it refills its lanes from one batch after the
+    // other without draining in between, and all waves run out of batches together.
+    const int64_t gw = static_cast<int64_t>(blockIdx.x) * kB8Waves + wv;
+    const int64_t nwv = static_cast<int64_t>(gridDim.x) * kB8Waves;
+    if (gw * kB8Ring >= B) return;  // uniform across the wave
+    // A problem is named by kB8Ring k + p for position p of the wave's k-th batch.
+    auto problem = [&](int32_t id) -> int64_t {
+        return (static_cast<int64_t>(id / kB8Ring) * nwv + gw) * kB8Ring + id % kB8Ring;
+    };
 
     // Raw words of the batch to initialise next (two lanes per problem), one batch ahead.
     uint32_t raw[NW];
 #pragma unroll
     for (int q = 0; q < NW; ++q) raw[q] = 0u;
-    int64_t bnext = r0;  // first problem of that batch (uniform)
+    int64_t bnext = gw * kB8Ring;  // first problem of that batch (uniform)
+    int32_t knext = 0;             // its index in the wave's sequence
     v4f pa = {1.f, 1.f, 1.f, 1.f}, pb0 = pa, pb1 = pa;  // OT: its marginals (this lane's four a_i, all b_j)
     auto prefetch = [&]() {
-        if (bnext + pb < r1) {
+        if (bnext + pb < B) {
             load_half8<DT>(H, bnext + pb, hf, raw);
             if constexpr (OT) {
                 const v4f* a4 = reinterpret_cast<const v4f*>(av) + 2 * (bnext + pb);
@@ -1915,7 +1918,7 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
 
     bool active = false;  // holds an unfinished problem
     bool setup = false;   // its Newton system must be formed at the current point
-    int32_t rel = 0;      // problem offset from r0
+    int32_t rel = 0;      // its name (see problem())
     float T[64], a[8], beta[7], g[8], W[28], ga[7], o[7];
 #pragma unroll
     for (int q = 0; q < 64; ++q) T[q] = 0.f;
@@ -1940,7 +1943,7 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
 #pragma unroll
         for (int q = 0; q < NW; ++q) asm volatile("" : "+v"(raw[q])::"memory");
         const int64_t bp = bnext + pb;
-        const bool valid = bp < r1;
+        const bool valid = bp < B;
         float cm[8];
         bool fin = true;
         // OT: this lane's four row masses and all eight column masses
@@ -2017,7 +2020,7 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
             sl[22 + hf] = pa;
             sl[24 + hf] = hf ? pb1 : pb0;
         }
-        sl[18 + hf] = hf ? v4f{bi[4], bi[5], bi[6], __int_as_float(static_cast<int32_t>(bp - r0))}
+        sl[18 + hf] = hf ? v4f{bi[4], bi[5], bi[6], __int_as_float(knext * kB8Ring + pb)}
                          : v4f{bi[0], bi[1], bi[2], bi[3]};
         sl[20 + hf] = hf ? v4f{gi[4], gi[5], gi[6], gi[7]} : v4f{gi[0], gi[1], gi[2], gi[3]};
         bool conv = gmax <= tol;
@@ -2056,7 +2059,8 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
             if constexpr (WRITE_ITERS)
                 if (hf == 0) iters[bp] = !fin ? BIRKHOFF4_NON_FINITE : (conv ? 0 : BIRKHOFF4_NOT_CONVERGED);
         }
-        bnext += kB8Ring;
+        bnext += nwv * kB8Ring;
+        ++knext;
         prefetch();
     };
 
@@ -2139,7 +2143,7 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
 #pragma unroll
                         for (int i = 0; i < 8; ++i) {
                             float h[8];
-                            load_row8<DT>(H, r0 + rel, i, h);
+                            load_row8<DT>(H, problem(rel), i, h);
 #pragma unroll
                             for (int j = 0; j < 8; ++j)
                                 if (T[8 * i + j] == 0.f)
@@ -2178,10 +2182,10 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
                 if constexpr (OT) {
                     float ma8[8], mb8[8];
                     load_marg(ma8, mb8);
-                    store_output8_ot<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, r0 + rel, T, a, beta, ma8, eta,
+                    store_output8_ot<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, problem(rel), T, a, beta, ma8, eta,
                                                               conv ? evals : BIRKHOFF4_NOT_CONVERGED);
                 } else {
-                    store_output8<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, r0 + rel, T, a, beta,
+                    store_output8<WRITE_DUAL, WRITE_ITERS>(P, dual, iters, problem(rel), T, a, beta,
                                                            conv ? evals : BIRKHOFF4_NOT_CONVERGED);
                 }
                 active = false;
@@ -2233,7 +2237,7 @@ __global__ __launch_bounds__(kB8Block, 2) void newton8_fwd_kernel(const void* __
                 break;
             }
             icur = nfresh;
-            if (bnext >= r1) break;  // nothing left to initialise
+            if (bnext >= B) break;  // nothing left to initialise
             init_batch();
             wm = __ballot(!active);
         }
@@ -3019,19 +3023,37 @@ int dispatch_fwd_hess(const void* H, float* P, float* dual, int32_t* iters, floa
     return launch_fwd<DT, false, false, true>(H, P, dual, iters, B, tol, max_iter, stream, cus, dev, hess);
 }
 
-// n = 8: one range of problems per wave, blocks scheduled by the hardware.
+// Blocks of the n = 8 forward resident at once on one CU, from the occupancy calculator;
+// queried once per instantiation and device.
+template <int DT, bool WD, bool WI, bool OT>
+int fwd8_blocks_per_cu(int dev) {
+    static int cached[kMaxDevices];
+    if (cached[dev] == 0) {
+        int nb = 0, cur = 0;
+        if (hipGetDevice(&cur) != hipSuccess || cur != dev ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, newton8_fwd_kernel<DT, WD, WI, OT>, kB8Block, 0) !=
+                hipSuccess || nb <= 0)
+            nb = 1;
+        cached[dev] = nb;
+    }
+    return cached[dev];
+}
+
+// n = 8: the grid is the resident waves (fewer for small B), each taking every nwv-th batch.
 template <int DT, bool WD, bool WI, bool OT = false>
 int launch_fwd8(const void* H, float* P, float* dual, int32_t* iters, int64_t B, float tol, int max_iter,
                 hipStream_t stream, const float* a = nullptr, const float* b = nullptr, float eta = 1.f) {
-    // about kB8Ranges ranges in all (several per resident wave slot), at least 64 problems each
-    const int64_t waves_min = (B + kMaxGrid * kB8Waves - 1) / (kMaxGrid * kB8Waves);
-    int64_t per_wave = (B + kB8Ranges - 1) / kB8Ranges;
-    if (per_wave < 64) per_wave = 64;
-    if (per_wave < waves_min) per_wave = waves_min;
-    const int64_t waves = (B + per_wave - 1) / per_wave;
-    const int64_t grid = (waves + kB8Waves - 1) / kB8Waves;
+    int cus = 0, dev = 0;
+    if (int e = device_cus(stream, &cus, &dev)) return e;
+    const int64_t batches = (B + kB8Ring - 1) / kB8Ring;
+    int64_t grid = static_cast<int64_t>(cus) * fwd8_blocks_per_cu<DT, WD, WI, OT>(dev);
+    const int64_t needed = (batches + kB8Waves - 1) / kB8Waves;
+    if (grid > needed) grid = needed;
+    // a problem is named in 32 bits by its wave's batch count and its position in the batch
+    const int64_t per_wave = (batches + grid * kB8Waves - 1) / (grid * kB8Waves);
+    if (per_wave > INT32_MAX / kB8Ring) return BIRKHOFF4_ERR_SIZE;
     launch_kernel((newton8_fwd_kernel<DT, WD, WI, OT>), dim3(static_cast<unsigned>(grid)), dim3(kB8Block), 0,
-                       stream, H, P, dual, iters, B, tol, max_iter, per_wave, a, b, eta);
+                  stream, H, P, dual, iters, B, tol, max_iter, a, b, eta);
     return launch_status();
 }
 

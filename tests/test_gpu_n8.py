@@ -72,7 +72,10 @@ def test_scales(sigma):
     check(H, P, dual, G, dH, f"sigma={sigma}")
 
 
-@pytest.mark.parametrize("B", [1, 2, 63, 64, 65, 255, 257, 1000, 4097])
+# The forward's grid is the resident waves, each taking every nwv-th batch of 32 problems:
+# batch counts below, at and above one batch per wave, and several batches per wave with a
+# ragged last batch.
+@pytest.mark.parametrize("B", [1, 2, 31, 32, 33, 63, 64, 65, 255, 257, 1000, 4097, 65535, 65569, 300007])
 def test_ragged_batches(B):
     say(f"test: n=8 ragged B={B}")
     H, G = gauss8(B, 3.0, seed=B)
