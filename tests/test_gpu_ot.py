@@ -120,7 +120,8 @@ def test_separable_cost():
     assert np.abs(T - expect).max() < 1e-5
 
 
-@pytest.mark.parametrize("B", [1, 63, 64, 65, 1000, 70001])
+# batch counts below, at and above one 64-problem batch per resident wave, and several per wave
+@pytest.mark.parametrize("B", [1, 63, 64, 65, 1000, 70001, 131072, 300007])
 def test_ragged(B):
     say(f"test: OT ragged B={B}")
     M, a, b, G = problem(B, 3.0, seed=B)
