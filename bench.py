@@ -608,9 +608,11 @@ def bench_mix_streams(args, dev, stream, B=1 << 15, C=4096, n=4) -> dict:
     ach = res["kernels"][dom]["achieved_GBs"]
     res["roofline"] = {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                        "frac": round(ach / HBM_PEAK_GBS, 4),
-                       "traffic": profile_figure(f"kernel_trace_{res['workload']}.md",
-                                                 "mix_bwd_hbm_bytes_per_launch" if dom == "mix_bwd"
-                                                 else "mix_fwd_hbm_bytes_per_launch")}
+                       # both stream counts are profiled in one file, the 4-stream workload's
+                       "traffic": profile_figure(f"kernel_trace_mix_streams_b2e15_c{C}.md",
+                                                 ("mix" if n == 4 else "mix8")
+                                                 + ("_bwd" if dom == "mix_bwd" else "_fwd")
+                                                 + "_hbm_bytes_per_launch")}
     log(f"mix streams: {res}")
     if not args.no_cpu_baseline:
         from oracle.mix import mix_bwd as o_bwd, mix_fwd as o_fwd
