@@ -89,7 +89,14 @@ enum {
  *       evaluation of the dual at a trial point: a damped Newton step, or a
  *       backtracking of it with a larger Levenberg-Marquardt shift). 0 returns T at the initial point, which is the
  *       row softmax of H after the columns are centred (beta_j^(0) = mean of
- *       column 4 minus mean of column j).
+ *       column 4 minus mean of column j). A step moves the column
+ *       potentials apart by at most 8 (natural-log units), so logits whose
+ *       solution lies far from the centred start need more: at H ~ N(0, s^2)
+ *       64 steps converge every matrix up to s = 100 and leave up to 30 % at
+ *       s = 500-1000, where 1000 steps converge them all.
+ *   Range: finite logits up to about 5e37 in magnitude are handled; larger
+ *       ones can overflow the fp32 scaling by log2(e) and are then reported
+ *       like a non-finite input.
  */
 int birkhoff4_fwd(const float* H, float* P, float* dual, int64_t B, float tol,
                   int max_iter, hipStream_t stream);
