@@ -313,6 +313,94 @@ def bench_b4096(args, dev) -> dict:
             "newton_steps": step_stats(it.cpu().numpy()), "max_marginal_err": float(marg.max().item())}
 
 
+# The paper's runtime table (Sec. 5, Table 3): median run times on N(0,10^2) logits, normalised
+# so that its own CUDA solver takes 1, on an NVIDIA RTX 6000 Ada. Columns: an unfused PyTorch
+# Sinkhorn (Vanilla), Triton Sinkhorn, mHC.cu, TileLang examples (TLE), TileKernels (TK) and
+# its TileLang Newton solver (Proj-TL); rows by batch size (1K = 1024).
+PAPER_RUNTIME = {
+    "columns": ["Vanilla", "Triton", "mHC.cu", "TLE", "TK", "Proj-TL"],
+    "fwd": {512: [49.778, 9.449, 2.908, 3.092, 2.862, 2.925], 2048: [49.974, 18.811, 2.977, 3.106, 2.867, 2.946],
+            8192: [49.289, 89.064, 4.307, 3.644, 2.830, 2.859], 32768: [22.879, 197.626, 2.354, 5.399, 2.262, 1.377],
+            131072: [12.419, 337.584, 1.674, 6.887, 3.001, 1.235]},
+    "fwd_bwd": {512: [126.380, 9.754, 3.548, 3.066, 3.058, 3.071], 2048: [125.481, 12.835, 3.595, 3.046, 3.034, 3.048],
+                8192: [124.970, 56.654, 4.367, 3.076, 8.498, 3.048],
+                32768: [103.678, 213.621, 7.809, 4.984, 22.028, 2.497],
+                131072: [51.518, 376.858, 22.310, 6.329, 28.345, 1.208]},
+}
+
+
+def bench_runtime_table(args, dev, stream, reps: int = 51) -> dict:
+    """The paper's runtime sweep on this hardware: N(0,10^2) logits at its five batch sizes,
+    median over `reps` calls of the event-timed forward and forward + backward, for the Newton
+    path (no dual, default kernel variant) and for this library's fused 20-step Sinkhorn-Knopp
+    pair, with SK-20 / Newton ratios beside the paper's normalised columns (context only: other
+    hardware, other implementations)."""
+    import torch
+
+    import paper_2606_07574_amd as b4
+    import workloads
+    lib = b4.lib()
+    sptr = stream.cuda_stream
+    F32 = b4.F32
+    rows = []
+    for B in (512, 2048, 8192, 32768, 131072):
+        H32, G32 = workloads.gauss(B, 10.0, seed=900 + B.bit_length())
+        H, G = torch.from_numpy(H32).to(dev), torch.from_numpy(G32).to(dev)
+        P, dH, Psk, dHs = (torch.empty_like(H) for _ in range(4))
+
+        def newton_fwd():
+            rc = lib.birkhoff4_fwd_ex2(H.data_ptr(), F32, P.data_ptr(), None, None, B, args.tol, args.max_iter,
+                                       b4.AUTO, sptr)
+            if rc:
+                raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+
+        def newton_bwd():
+            rc = lib.birkhoff4_bwd_ex(P.data_ptr(), G.data_ptr(), F32, dH.data_ptr(), B, sptr)
+            if rc:
+                raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+
+        def sk_fwd():
+            rc = lib.birkhoff4_sk_fwd(H.data_ptr(), F32, Psk.data_ptr(), B, PAPER_CAP, sptr)
+            if rc:
+                raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+
+        def sk_bwd():
+            rc = lib.birkhoff4_sk_bwd(H.data_ptr(), F32, G.data_ptr(), F32, dHs.data_ptr(), B, PAPER_CAP, sptr)
+            if rc:
+                raise RuntimeError(lib.birkhoff4_strerror(rc).decode())
+
+        def median_us(calls):
+            ts = []
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            for r in range(reps + 3):
+                torch.cuda.synchronize()
+                e0.record(stream)
+                for c in calls:
+                    c()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                if r >= 3:
+                    ts.append(e0.elapsed_time(e1) * 1e3)
+            return float(np.median(ts))
+
+        nf, nfb = median_us([newton_fwd]), median_us([newton_fwd, newton_bwd])
+        sf, sfb = median_us([sk_fwd]), median_us([sk_fwd, sk_bwd])
+        row = {"B": B, "newton_fwd_us": round(nf, 2), "newton_fwd_bwd_us": round(nfb, 2), "sk20_fwd_us": round(sf, 2),
+               "sk20_fwd_bwd_us": round(sfb, 2), "sk20_over_newton_fwd": round(sf / nf, 3),
+               "sk20_over_newton_fwd_bwd": round(sfb / nfb, 3),
+               "paper_fwd": dict(zip(PAPER_RUNTIME["columns"], PAPER_RUNTIME["fwd"][B])),
+               "paper_fwd_bwd": dict(zip(PAPER_RUNTIME["columns"], PAPER_RUNTIME["fwd_bwd"][B]))}
+        log(f"runtime table: {row}")
+        rows.append(row)
+        del H, G, P, dH, Psk, dHs
+    return {"logits": "N(0,10^2), fp32", "timing": f"median over {reps} event-timed calls, synchronised between calls",
+            "newton": f"default kernel variant (four lanes per problem up to B = 32768), no dual, tol {args.tol}, "
+                      f"max_iter {args.max_iter}",
+            "sk20": "this library's fused 20-step Sinkhorn-Knopp forward and exact reverse-mode backward",
+            "paper": "Sec. 5 Table 3, median times normalised to the paper's CUDA solver (= 1), NVIDIA RTX 6000 Ada",
+            "rows": rows}
+
+
 def bench_accuracy(args, dev) -> dict:
     """The paper's accuracy tables on this hardware: 10,000 matrices from each of its four input
     families, L1 marginal error of the Newton forward and of the 20-step Sinkhorn-Knopp baseline
@@ -422,6 +510,7 @@ def main() -> int:
     ap.add_argument("--no-small", action="store_true", help="skip the small-batch launch timing")
     ap.add_argument("--no-mix", action="store_true", help="skip the residual-mixing measurement")
     ap.add_argument("--mix-only", action="store_true", help="time only the residual-mixing pair (for profiler runs)")
+    ap.add_argument("--runtime-only", action="store_true", help="only the paper's runtime sweep (N(0,10^2), 0.5K-128K)")
     ap.add_argument("--small-only", action="store_true", help="time only the small-batch cases")
     ap.add_argument("--no-extras", action="store_true",
                     help="time only the given workload's path, none of the other measurements (for profiler runs)")
@@ -467,6 +556,9 @@ def main() -> int:
         return 0
     if args.small_only:
         print(json.dumps({"small_batch": bench_small_batch(dev)}), flush=True)
+        return 0
+    if args.runtime_only:
+        print(json.dumps({"runtime_table": bench_runtime_table(args, dev, stream)}), flush=True)
         return 0
     if args.ot8_only:
         print(json.dumps({"ot8": bench_ot(args, dev, stream, n=8)}), flush=True)
@@ -523,6 +615,7 @@ def main() -> int:
             del r
         out["configs"] = cfg
         out["accuracy_tables"] = bench_accuracy(args, dev)
+        out["runtime_table"] = bench_runtime_table(args, dev, stream)
     if not args.no_n8 and extras:
         out["n8"] = bench_n8(args, dev, stream)
     if not args.no_ot and extras:
