@@ -1012,12 +1012,13 @@ __global__ __launch_bounds__(kBwdBlock) void implicit_bwd_kernel(const float* __
 // Residual mixing of the mHC layer (Sec. 2.1): the streams of a token are mixed by its
 // projected matrix, x <- H^res x
 // ---------------------------------------------------------------------------
-// A token carries n = 4 streams of C channels, [B][4][C] row-major. The forward writes
-// Y_i = sum_j P_ij X_j; the backward writes dX_j = sum_i P_ij dY_i and forms
+// A token carries n = 4 (or 8) streams of C channels, [B][n][C] row-major. The forward
+// writes Y_i = sum_j P_ij X_j; the backward writes dX_j = sum_i P_ij dY_i and forms
 // dP_ij = sum_c dY_i[c] X_j[c], from which dH follows as in the projection's backward. A
-// wave owns one token at a time: P is uniform over the wave (scalar loads) and the lanes
-// stream 16-byte chunks of the four rows, so that each load or store instruction covers
-// 1 KB of one row. Every stream byte is touched once: non-temporal loads and stores.
+// wave works on one token at a time (with n = 8, the four waves of a block on the same
+// token): P is uniform over the wave (scalar loads) and the lanes stream 16-byte chunks of
+// the rows, so that each load or store instruction covers 1 KB of one row. Every stream
+// byte is touched once: non-temporal loads and stores.
 constexpr int kMixBlock = 256;
 constexpr int kMixWaves = kMixBlock / 64;
 constexpr int kMixPerCu = 8;  // blocks per CU the grid is sized for
@@ -3075,7 +3076,9 @@ int dispatch_ot8_fwd(const float* M, const float* a, const float* b, float eta, 
     return launch_fwd8<F, false, false, true>(M, T, dual, iters, B, tol, max_iter, stream, a, b, eta);
 }
 
-// General OT: one range of problems per wave (as for n = 8).
+// General OT: one range of problems per wave, blocks scheduled by the hardware (its problems
+// take few trials and its ranges are small, so the strided batches of the n = 8 forward do
+// not pay here).
 template <bool WD, bool WI>
 int launch_ot_fwd(const float* M, const float* a, const float* b, float eta, float* T, float* dual, int32_t* iters,
                   int64_t B, float tol, int max_iter, hipStream_t stream) {
