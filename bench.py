@@ -454,7 +454,7 @@ def cpu_info() -> dict:
 
 def bench_cpu_baseline(args, ch, w) -> dict:
     """The oracle as it stands (fp64, its own tolerance 1e-13) on the headline workload's first
-    matrices, fwd + bwd, on the machine's CPU share of threads; its 1-thread rate on a smaller sample
+    matrices, fwd + bwd, on the host's CPU share of threads for one GPU; its 1-thread rate on a smaller sample
     at 1e-13 and at the GPU's tolerance; and the host's core count and CPU model."""
     import oracle
     n = min(args.cpu_sample, w.B)
@@ -478,7 +478,7 @@ def bench_cpu_baseline(args, ch, w) -> dict:
     info = cpu_info()
     res = {"value": round(v, 1), "unit": "proj/s", "cores": threads, "kind": "oracle",
            "sample": f"first {n} matrices of {w.name}; fp64 oracle forward (tol {oracle.DEFAULT_TOL:g}) + "
-                     f"backward, {threads} threads (the GPU box's CPU share for one GPU), {dt:.1f} s",
+                     f"backward, {threads} threads (the host's CPU share for one GPU), {dt:.1f} s",
            **info,
            "at_gpu_tol": {"value": round(vg, 1), "tol": args.tol, "threads": threads, "seconds": round(dtg, 2)},
            "one_thread": {"value": round(v1, 1), "tol": oracle.DEFAULT_TOL, "sample": n1, "seconds": round(dt1, 2)},

@@ -240,7 +240,7 @@ def test_binding_rejects_mismatched_outputs():
 
 
 @pytest.mark.parametrize("B", [1000, 100003])
-def test_north_star_signatures(B):
+def test_plain_signatures(B):
     # birkhoff4_fwd(H, P, dual, B, tol, max_iter, stream) and birkhoff4_bwd(P, dual, dP, dH, B,
     # stream) called directly through the C ABI on device buffers (fp32, the default dispatch:
     # the four-lanes-per-problem forward below 2^15 problems, the throughput forward above)
