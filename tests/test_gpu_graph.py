@@ -137,10 +137,12 @@ def test_graph_many_launches():
     graph_roundtrip(fn, sets, "16 pairs")
 
 
-@pytest.mark.parametrize("n", [4, 8])
-def test_graph_mix(n):
-    say(f"test: graph capture of the residual-mixing pair, {n} streams")
-    sets = [list(workloads.mix_streams_device(3001, 264, 70 + k, "cuda", n)) for k in range(N_SETS)]
+# C = 2048 bf16 channels (256 chunks a row) puts the 8-stream kernels on one token per block
+@pytest.mark.parametrize("n,C", [(4, 264), (8, 264), (8, 2048)])
+def test_graph_mix(n, C):
+    say(f"test: graph capture of the residual-mixing pair, {n} streams, C={C}")
+    sets = [list(workloads.mix_streams_device(3001 if C < 1024 else 700, C, 70 + k, "cuda", n))
+            for k in range(N_SETS)]
     mfwd, mbwd = (b4.mix_fwd, b4.mix_bwd) if n == 4 else (b4.mix8_fwd, b4.mix8_bwd)
 
     def fn(H, X, G):
